@@ -1,0 +1,148 @@
+"""CPU oracle for the edge-feature join (Connected Content Retriever, §3.1, Eq. 1).
+
+TEST INFRASTRUCTURE: only the test suite, the smoke check and the benchmark's CPU-baseline leg
+may import this package. The product path (the HIP library and its binding) never does.
+
+The arithmetic lives in ``cc_oracle.c`` (plain C, built with gcc); this file only builds and
+loads it and marshals numpy / CPU-torch arrays. ``join`` returns the full model-input rows
+``[doc row | edge segment per lookup]``, the hit mask and the invalid-candidate count, exactly
+as the C header comment defines them.
+
+Parity pins: the three search methods (lower bound, naive scan, hash) are cross-checked in the
+CPU tests against a pure-Python scan of Eq. 1, against NumPy's ``searchsorted`` route through
+Alg. 1, against invariants, and against the hand-worked fixtures in ``tests/golden``.
+"""
+from __future__ import annotations
+
+import ctypes
+import subprocess
+from pathlib import Path
+from typing import Optional
+
+import numpy as np
+
+LOWER_BOUND, SCAN, HASH = 0, 1, 2
+
+_HERE = Path(__file__).resolve().parent
+SRC = _HERE / "cc_oracle.c"
+LIB = _HERE / "libccoracle.so"
+
+_lib = None
+
+
+def build(out: Optional[Path] = None, src: Optional[Path] = None, werror: bool = True) -> Path:
+    """Compile the oracle into a shared library (gcc, no GPU involved)."""
+    out = Path(out) if out else LIB
+    src = Path(src) if src else SRC
+    tmp = out.with_suffix(".so.tmp")
+    flags = ["-Wall", "-Wextra"] + (["-Werror"] if werror else ["-w"])
+    subprocess.check_call(["gcc", "-O2", "-std=c99", *flags, "-fPIC", "-shared", "-o", str(tmp),
+                           str(src)])
+    tmp.replace(out)
+    return out
+
+
+def load(path: Optional[Path] = None):
+    """Load a compiled oracle (building the default one if nothing is built yet)."""
+    p = Path(path) if path else LIB
+    if path is None and not p.exists():
+        build()
+    lib = ctypes.CDLL(str(p))
+    i64, vp = ctypes.c_int64, ctypes.c_void_p
+    lib.ccor_join.restype = i64
+    lib.ccor_join.argtypes = [ctypes.c_int,
+                              i64, vp, vp, i64,
+                              i64, vp, vp,
+                              vp, vp,
+                              vp, i64,
+                              vp,
+                              i64, vp,
+                              vp, i64, vp]
+    return lib
+
+
+def _default_lib():
+    global _lib
+    if _lib is None:
+        _lib = load()
+    return _lib
+
+
+def as_bytes(a) -> np.ndarray:
+    """A 2-D array of any element type as a contiguous uint8 array of its rows' bytes."""
+    if hasattr(a, "detach"):               # torch tensor (CPU)
+        import torch
+        t = a.detach().cpu().contiguous()
+        if t.dim() == 1:
+            t = t.reshape(-1, 1)
+        width = int(np.prod(t.shape[1:])) * t.element_size()
+        return t.view(torch.uint8).numpy().reshape(t.shape[0], width)
+    a = np.ascontiguousarray(a)
+    if a.ndim == 1:
+        a = a.reshape(-1, 1)
+    width = int(np.prod(a.shape[1:])) * a.itemsize
+    return a.view(np.uint8).reshape(a.shape[0], width)
+
+
+def _i64(a) -> np.ndarray:
+    if hasattr(a, "detach"):
+        a = a.detach().cpu().numpy()
+    return np.ascontiguousarray(a, dtype=np.int64)
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def join(author_id, doc_rows, cand_offsets, cand_idx, key_offsets, keys, edge_rows,
+         default_row=None, n_lookups: int = 1, extra_keys=None, out_stride: Optional[int] = None,
+         method: int = LOWER_BOUND, lib=None, fill: int = 0):
+    """Run the oracle join; returns (out uint8 [total, stride], hit int8 [total, L], invalid).
+
+    ``extra_keys`` is a list of ``n_lookups - 1`` arrays of per-candidate keys. ``out`` starts
+    filled with the byte ``fill`` so that a row the join forgets to write shows up.
+    """
+    lib = lib or _default_lib()
+    author_id = _i64(author_id)
+    doc = as_bytes(doc_rows)
+    edge = as_bytes(edge_rows)
+    co, ci, ko, ks = _i64(cand_offsets), _i64(cand_idx), _i64(key_offsets), _i64(keys)
+    n_docs, wd = author_id.shape[0], doc.shape[1]
+    if doc.shape[0] != n_docs:
+        raise ValueError("doc_rows and author_id disagree on n_docs")
+    we = edge.shape[1]
+    if edge.shape[0] != ks.shape[0]:
+        raise ValueError("edge_rows and keys disagree on K")
+    total = int(co[-1])
+    if ci.shape[0] != total:
+        raise ValueError("cand_idx length != cand_offsets[-1]")
+    stride = wd + n_lookups * we if out_stride is None else out_stride
+    dflt = None
+    if default_row is not None:
+        dflt = as_bytes(default_row).reshape(-1)
+        if dflt.shape[0] != we:
+            raise ValueError("default_row width != edge row width")
+    ex = None
+    if n_lookups > 1:
+        if extra_keys is None or len(extra_keys) != n_lookups - 1:
+            raise ValueError("n_lookups - 1 extra key arrays are required")
+        ex = np.ascontiguousarray(np.concatenate([_i64(e) for e in extra_keys]))
+        if ex.shape[0] != (n_lookups - 1) * total:
+            raise ValueError("extra key arrays must have one key per candidate")
+    out = np.full((total, stride), fill, dtype=np.uint8)
+    hit = np.zeros((total, n_lookups), dtype=np.int8)
+    inv = lib.ccor_join(method, n_docs, _ptr(author_id), _ptr(doc), wd,
+                        co.shape[0] - 1, _ptr(co), _ptr(ci), _ptr(ko), _ptr(ks),
+                        _ptr(edge), we, _ptr(dflt), n_lookups, _ptr(ex),
+                        _ptr(out), stride, _ptr(hit))
+    if inv < 0:
+        raise ValueError("oracle rejected its arguments")
+    return out, hit, int(inv)
+
+
+def join_single(author_id, doc_rows, cand_idx, keys, edge_rows, **kw):
+    """One viewer: the batched form with offsets [0, N] and [0, K]."""
+    n = len(cand_idx)
+    k = len(keys)
+    return join(author_id, doc_rows, np.array([0, n]), cand_idx, np.array([0, k]), keys,
+                edge_rows, **kw)

@@ -1,0 +1,277 @@
+"""Pins that tie the CPU oracle to something other than itself.
+
+Each pin takes a loaded oracle library (``oracle.load(path)``) so the planted-mistake test can
+run the same pins against deliberately broken copies of the oracle. The references used here
+are independent of the oracle's code:
+
+* ``pin_golden``      -- the hand-worked Eq. 1 example in ``tests/golden/eq1_worked.json``;
+* ``pin_scan``        -- a pure-Python scan of Eq. 1 on tiny random inputs (the naive O(N K)
+                         scan of §3.1), including duplicates, int64 extremes, invalid positions;
+* ``pin_alg1``        -- NumPy's stable ``argsort`` + ``searchsorted(side="left")`` route through
+                         the four steps of Alg. 1, given the keys in shuffled order;
+* ``pin_invariants``  -- properties of the result on generated workloads: hit iff the key is
+                         in the viewer's key set, miss rows equal the default row, valid doc
+                         segments equal the store row, equivariance under a permutation of the
+                         candidates, batched == per-viewer concatenation, the second lookup does
+                         not disturb the first, and the hit count equals the membership count.
+"""
+from __future__ import annotations
+
+import json
+import sys
+from pathlib import Path
+
+import numpy as np
+import torch
+
+import oracle
+import workload as W
+
+GOLDEN = Path(__file__).resolve().parent / "golden"
+METHODS = (oracle.LOWER_BOUND, oracle.SCAN, oracle.HASH)
+FILL = 0xCD
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def _run(lib, tc: W.TinyCase, method, **kw):
+    b = tc.batch
+    extra = [b.actor] if tc.n_lookups == 2 else None
+    return oracle.join(tc.author_id, tc.doc_rows, b.cand_offsets, b.cand_idx, b.key_offsets,
+                       b.keys, b.edge_rows, default_row=tc.default_row,
+                       n_lookups=tc.n_lookups, extra_keys=extra, method=method, lib=lib,
+                       fill=FILL, **kw)
+
+
+# --------------------------------------------------------------------------------------------
+def pin_golden(lib):
+    g = json.loads((GOLDEN / "eq1_worked.json").read_text())
+    i32 = lambda x: np.asarray(x, dtype=np.int32)
+    author = np.asarray(g["author_id"], dtype=np.int64)
+    doc, edge = i32(g["doc_rows"]), i32(g["edge_rows"])
+    want2 = i32(g["expected_out_two_lookups"])
+    hit2 = np.asarray(g["expected_hit_two_lookups"], dtype=np.int8)
+    for m in METHODS:
+        out, hit, inv = oracle.join(author, doc, g["cand_offsets"], g["cand_idx"],
+                                    g["key_offsets"], g["keys"], edge, n_lookups=2,
+                                    extra_keys=[g["actor_keys"]], method=m, lib=lib, fill=FILL)
+        assert np.array_equal(out.view(np.int32), want2), f"golden two-lookup rows, method {m}"
+        assert np.array_equal(hit, hit2), f"golden two-lookup hits, method {m}"
+        assert inv == g["expected_invalid"], f"golden invalid count, method {m}"
+        out1, hit1, inv1 = oracle.join(author, doc, g["cand_offsets"], g["cand_idx"],
+                                       g["key_offsets"], g["keys"], edge, method=m, lib=lib,
+                                       fill=FILL)
+        assert np.array_equal(out1.view(np.int32), want2[:, :8]), f"golden one-lookup, {m}"
+        assert np.array_equal(hit1[:, 0], hit2[:, 0]), f"golden one-lookup hits, {m}"
+        assert inv1 == g["expected_invalid"]
+        # A non-zero default row replaces every miss segment and nothing else.
+        dflt = np.array([-7, 8, -9, 10], dtype=np.int32)
+        out3, _, _ = oracle.join(author, doc, g["cand_offsets"], g["cand_idx"],
+                                 g["key_offsets"], g["keys"], edge, n_lookups=2,
+                                 extra_keys=[g["actor_keys"]], default_row=dflt.view(np.uint8),
+                                 method=m, lib=lib, fill=FILL)
+        want3 = want2.copy()
+        for j in range(want3.shape[0]):
+            for l in range(2):
+                if hit2[j, l] == 0:
+                    want3[j, 4 + 4 * l: 8 + 4 * l] = dflt
+        assert np.array_equal(out3.view(np.int32), want3), f"golden default row, method {m}"
+
+
+# --------------------------------------------------------------------------------------------
+def scan_reference(tc: W.TinyCase):
+    """Eq. 1 by a plain scan, in pure Python (tiny inputs only)."""
+    b = tc.batch
+    author = _np(tc.author_id).tolist()
+    doc = _np(tc.doc_rows)
+    edge = _np(b.edge_rows)
+    co, ko = _np(b.cand_offsets).tolist(), _np(b.key_offsets).tolist()
+    cand, keys = _np(b.cand_idx).tolist(), _np(b.keys).tolist()
+    actor = _np(b.actor).tolist() if tc.n_lookups == 2 else None
+    n_docs, wd, we = len(author), doc.shape[1], edge.shape[1]
+    L = tc.n_lookups
+    dflt = bytes(we) if tc.default_row is None else bytes(_np(tc.default_row).tolist())
+    rows, hits, invalid = [], [], 0
+    for v in range(len(co) - 1):
+        vkeys = keys[ko[v]:ko[v + 1]]
+        for j in range(co[v], co[v + 1]):
+            c = cand[j]
+            if not (0 <= c < n_docs):
+                invalid += 1
+                rows.append(bytes(wd) + dflt * L)
+                hits.append([0] * L)
+                continue
+            row = bytes(doc[c].tolist())
+            h = []
+            for l in range(L):
+                key = author[c] if l == 0 else actor[j]
+                found = None
+                for i, a in enumerate(vkeys):
+                    if a == key:
+                        found = i
+                        break
+                if found is None:
+                    row += dflt
+                    h.append(0)
+                else:
+                    row += bytes(edge[ko[v] + found].tolist())
+                    h.append(1)
+            rows.append(row)
+            hits.append(h)
+    return rows, hits, invalid
+
+
+def pin_scan(lib, seeds=range(60)):
+    for seed in seeds:
+        tc = W.tiny_case(seed)
+        rows, hits, invalid = scan_reference(tc)
+        for m in METHODS:
+            out, hit, inv = _run(lib, tc, m)
+            assert inv == invalid, f"seed {seed} method {m}: invalid count"
+            assert [bytes(r.tolist()) for r in out] == rows, f"seed {seed} method {m}: rows"
+            assert hit.tolist() == hits, f"seed {seed} method {m}: hit mask"
+
+
+# --------------------------------------------------------------------------------------------
+def alg1_numpy(d, a, F):
+    """Alg. 1 for one viewer with NumPy library routines (valid for K >= 1).
+
+    Step 1 sorts the affinity records (stable, so equal keys keep their input order),
+    Step 2 is searchsorted (leftmost insertion point), Step 3 clamps and validates,
+    Step 4 fills zeros and gathers the matched rows.
+    """
+    K = a.shape[0]
+    idx = np.argsort(a, kind="stable")
+    a_sorted, F_sorted = a[idx], F[idx]
+    pos = np.searchsorted(a_sorted, d, side="left")
+    pos_safe = np.minimum(pos, K - 1)
+    valid = (pos < K) & (a_sorted[pos_safe] == d)
+    O = np.zeros((d.shape[0], F.shape[1]), dtype=F.dtype)
+    O[valid] = F_sorted[pos_safe[valid]]
+    return O, valid
+
+
+def pin_alg1(lib, seeds=range(40)):
+    rng = np.random.default_rng(12345)
+    for seed in seeds:
+        tc = W.tiny_case(seed, max_viewers=1, n_lookups=1, k_values=[int(rng.integers(1, 40))])
+        b = tc.batch
+        keys, edge = _np(b.keys), oracle.as_bytes(b.edge_rows)
+        cand = _np(b.cand_idx)
+        n_docs = tc.author_id.numel()
+        ok = (cand >= 0) & (cand < n_docs)
+        d = _np(tc.author_id)[np.where(ok, cand, 0)]
+        # Alg. 1 receives the records in a shuffled order and sorts them itself (Step 1).
+        # Equal keys keep their relative order in the shuffle, so its stable sort puts them
+        # back in the order the oracle sees and the leftmost rule picks the same row.
+        slot = rng.permutation(keys.shape[0])          # record i goes to position slot[i]
+        for k in np.unique(keys):
+            members = np.flatnonzero(keys == k)
+            slot[members] = np.sort(slot[members])
+        shuffled_keys = np.empty_like(keys)
+        shuffled_edge = np.empty_like(edge)
+        shuffled_keys[slot], shuffled_edge[slot] = keys, edge
+        O, valid = alg1_numpy(d, shuffled_keys, shuffled_edge)
+        out, hit, _ = oracle.join(tc.author_id, tc.doc_rows, b.cand_offsets, b.cand_idx,
+                                  b.key_offsets, b.keys, b.edge_rows, lib=lib, fill=FILL)
+        wd = tc.doc_rows.shape[1]
+        assert np.array_equal(hit[ok, 0].astype(bool), valid[ok]), f"seed {seed}: Alg.1 valid"
+        assert np.array_equal(out[ok, wd:], O[ok]), f"seed {seed}: Alg.1 rows"
+
+
+# --------------------------------------------------------------------------------------------
+def _scaled_case(seed, cfg=2, lookups=False, viewers=3):
+    s, r = W.config(cfg, store_n_docs=60_000, store_n_authors=50_000, req_k=700,
+                    req_n_cand=4_000, req_n_viewers=viewers, req_actor=lookups, req_k_range=None)
+    st = W.make_store(s, seed)
+    reqs = W.make_requests(st, r, seed)
+    return st, reqs
+
+
+def pin_invariants(lib, seeds=(3, 4)):
+    for seed in seeds:
+        st, reqs = _scaled_case(seed, lookups=True)
+        b = W.pack(reqs)
+        author = _np(st.author_id)
+        doc = oracle.as_bytes(st.doc_rows)
+        wd = doc.shape[1]
+        we = oracle.as_bytes(b.edge_rows).shape[1]
+        g = W.gen("cpu", seed, 99)
+        dflt = torch.randint(0, 256, (we,), generator=g, dtype=torch.int64).to(torch.uint8)
+        # Plant a few invalid positions.
+        cand = b.cand_idx.clone()
+        cand[::97] = -1
+        cand[5::211] = st.spec.n_docs
+        out, hit, inv = oracle.join(st.author_id, st.doc_rows, b.cand_offsets, cand,
+                                    b.key_offsets, b.keys, b.edge_rows, default_row=dflt,
+                                    n_lookups=2, extra_keys=[b.actor], lib=lib, fill=FILL)
+        cn = _np(cand)
+        ok = (cn >= 0) & (cn < st.spec.n_docs)
+        assert inv == int((~ok).sum()), "invalid count"
+        edge = oracle.as_bytes(b.edge_rows)
+        co, ko = _np(b.cand_offsets), _np(b.key_offsets)
+        keys, actor = _np(b.keys), _np(b.actor)
+        dn = _np(dflt)
+        for v in range(len(reqs)):
+            sl = slice(co[v], co[v + 1])
+            vkeys = keys[ko[v]:ko[v + 1]]
+            first = {}
+            for i, k in enumerate(vkeys.tolist()):
+                first.setdefault(k, i)
+            for l, qk in enumerate((author[np.where(ok[sl], cn[sl], 0)], actor[sl])):
+                member = np.isin(qk, vkeys) & ok[sl]
+                h = hit[sl, l].astype(bool)
+                # (i) hit iff the key is in the viewer's key set (and the position is valid)
+                assert np.array_equal(h, member), f"seed {seed} viewer {v} lookup {l}: membership"
+                seg = out[sl, wd + l * we: wd + (l + 1) * we]
+                # (ii) a miss carries the default row
+                assert (seg[~h] == dn).all(), "miss segment != default row"
+                # hit rows are the edge row of that key
+                rows = np.array([ko[v] + first[k] for k in qk[h].tolist()], dtype=np.int64)
+                assert np.array_equal(seg[h], edge[rows]), "hit segment != edge row of key"
+                # (vii) number of hits == size of the multiset intersection
+                assert int(h.sum()) == int(member.sum())
+            # (iii) valid doc segments are the store rows, invalid ones are zero
+            assert np.array_equal(out[sl][ok[sl], :wd], doc[cn[sl][ok[sl]]]), "doc segment"
+            assert (out[sl][~ok[sl], :wd] == 0).all(), "invalid doc segment"
+        # (iv) equivariance: permuting candidates within each viewer permutes the rows
+        perm = np.concatenate([co[v] + np.random.default_rng(seed + v).permutation(co[v + 1] - co[v])
+                               for v in range(len(reqs))])
+        outp, hitp, invp = oracle.join(st.author_id, st.doc_rows, b.cand_offsets, cn[perm],
+                                       b.key_offsets, b.keys, b.edge_rows, default_row=dflt,
+                                       n_lookups=2, extra_keys=[actor[perm]], lib=lib, fill=FILL)
+        assert np.array_equal(outp, out[perm]) and np.array_equal(hitp, hit[perm])
+        assert invp == inv
+        # (v) batched == concatenation of single-viewer joins
+        parts = []
+        for v, q in enumerate(reqs):
+            o1, h1, _ = oracle.join_single(st.author_id, st.doc_rows, cn[co[v]:co[v + 1]], q.keys,
+                                           q.edge_rows, default_row=dflt, n_lookups=2,
+                                           extra_keys=[q.actor], lib=lib, fill=FILL)
+            parts.append((o1, h1))
+        assert np.array_equal(np.concatenate([p[0] for p in parts]), out), "batched != singles"
+        assert np.array_equal(np.concatenate([p[1] for p in parts]), hit)
+        # (vi) the first lookup of a two-lookup join equals the one-lookup join
+        o1, h1, _ = oracle.join(st.author_id, st.doc_rows, b.cand_offsets, cand, b.key_offsets,
+                                b.keys, b.edge_rows, default_row=dflt, lib=lib, fill=FILL)
+        assert np.array_equal(o1, out[:, :wd + we]) and np.array_equal(h1[:, 0], hit[:, 0])
+
+
+ALL_PINS = (pin_golden, pin_scan, pin_alg1, pin_invariants)
+
+
+def run_all(lib_path=None):
+    lib = oracle.load(lib_path)
+    for p in ALL_PINS:
+        p(lib)
+
+
+if __name__ == "__main__":      # used by the planted-mistake test, one broken oracle per run
+    try:
+        run_all(sys.argv[1])
+    except AssertionError as e:
+        print("PIN FAILED:", e)
+        sys.exit(3)
+    sys.exit(0)

@@ -1,0 +1,246 @@
+"""Benchmark of the edge-feature join on one MI355X (prints one JSON line).
+
+Workload: the production-shaped single-viewer request (10M-document store with Zipf(1.1)
+author ids, 64 bf16 document columns; K = 5,000 sorted affinity keys with 32 bf16 columns;
+N = 50,000 candidates, 70% in-network). A step joins 64 distinct such requests in one
+cc_join_batched launch (3.2M candidates). Steps cycle through 4 distinct batches so that
+only the store's hot columns can stay in the caches between steps.
+
+Reported:
+  value           joined candidates/s over the K timed steps (inputs resident in HBM)
+  p50/p99         per-request latency of single cc_join calls (hip events on the stream)
+  roofline        algorithmic bytes per launch / mean launch time, against 8 TB/s
+  cold            the same step with the caches flushed (1 GiB write) before each launch
+  cpu_baseline    the CPU oracle on the host cores, on a bounded sample of the same requests
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+from pathlib import Path
+
+ROOT = Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+METRIC = "joined candidates/sec + achieved HBM GB/s (% peak); p99 per-request join ms"
+PEAK_GBPS = 8000.0
+REQS_PER_STEP = 64
+N_BATCHES = 4
+KERNEL_SRC = ROOT / "paper_2609_22441_amd" / "csrc" / "join_kernels.hip"
+TRAFFIC = ROOT / "profiles" / "traffic_production_x64.json"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--latency-calls", type=int, default=1024)
+    ap.add_argument("--cold-steps", type=int, default=20)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=2)
+    return ap.parse_args()
+
+
+def algorithmic_bytes(torch, st, batch, wd, we, n_lookups=1):
+    """Bytes the method must move for one launch: per candidate its index, author id, doc row,
+    output row and hit byte; per viewer its keys and each distinct edge row that is hit."""
+    n = batch.cand_idx.numel()
+    per_cand = 8 + 8 + wd + (wd + n_lookups * we) + n_lookups
+    keys_bytes = batch.keys.numel() * 8
+    co, ko = batch.cand_offsets.tolist(), batch.key_offsets.tolist()
+    rows = 0
+    for v in range(len(co) - 1):
+        a = st.author_id[batch.cand_idx[co[v]:co[v + 1]]]
+        rows += int(torch.isin(torch.unique(a), batch.keys[ko[v]:ko[v + 1]]).sum())
+    return n * per_cand + keys_bytes + rows * we
+
+
+def kernel_hash():
+    return hashlib.sha256(KERNEL_SRC.read_bytes()).hexdigest()[:16]
+
+
+def load_traffic():
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they match this kernel."""
+    if not TRAFFIC.exists():
+        return None
+    t = json.loads(TRAFFIC.read_text())
+    return t.get("bytes_per_launch") if t.get("kernel_sha") == kernel_hash() else None
+
+
+def cpu_baseline(st_cpu, reqs_cpu, seconds):
+    import oracle
+    lib = oracle.load()
+    cores = len(os.sched_getaffinity(0))
+    threads = max(1, min(cores, 16))
+    author, rows = st_cpu
+    done = [0]
+
+    def one(q):
+        oracle.join_single(author, rows, q.cand_idx, q.keys, q.edge_rows, lib=lib)
+        return q.cand_idx.numel()
+
+    t0 = time.perf_counter()
+    n_req = 0
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        while time.perf_counter() - t0 < seconds:
+            for c in ex.map(one, reqs_cpu[:threads]):
+                done[0] += c
+                n_req += 1
+    dt = time.perf_counter() - t0
+    return {"value": done[0] / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_req} single-viewer requests of the benchmark workload "
+                      f"({reqs_cpu[0].cand_idx.numel()} candidates each), lower-bound oracle, "
+                      f"one request per thread, {dt:.1f} s wall"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the join runs on a single MI355X and this build "
+              "has no multi-GPU path; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_22441_amd as P
+    from paper_2609_22441_amd import binding
+    import workload as W
+
+    if not binding.LIB_PATH.exists():
+        import __graft_entry__
+        __graft_entry__.build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    s, r = W.CONFIGS[2]
+    st = W.make_store(s, args.seed, device=dev)
+    store = P.cc_store_create(st.author_id, st.doc_rows)
+    batches = []
+    for i in range(N_BATCHES):
+        reqs = W.make_requests(st, r, args.seed, first_viewer=i * REQS_PER_STEP,
+                               n_viewers=REQS_PER_STEP)
+        batches.append((reqs, W.pack(reqs)))
+    wd = st.doc_rows.shape[1] * st.doc_rows.element_size()
+    we = r.edge_cols * 2
+    total = batches[0][1].cand_idx.numel()
+    out = torch.empty(total, wd + we, dtype=torch.uint8, device=dev)
+    hit = torch.empty(total, 1, dtype=torch.int8, device=dev)
+    alg = [algorithmic_bytes(torch, st, b, wd, we) for _, b in batches]
+    torch.cuda.synchronize()
+
+    def step(i):
+        b = batches[i % N_BATCHES][1]
+        P.cc_join_batched(store, b.cand_offsets, b.cand_idx, b.key_offsets, b.keys, b.edge_rows,
+                          out, hit)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for i in range(args.steps):
+        step(i)
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = e0.elapsed_time(e1)
+    ms_step = ms_total / args.steps
+    cands_per_s = total * args.steps / (ms_total / 1e3)
+    alg_per_launch = sum(alg[i % N_BATCHES] for i in range(args.steps)) / args.steps
+    achieved = alg_per_launch / (ms_step / 1e3) / 1e9
+
+    # Cold caches: overwrite 1 GiB before each launch, time the launch alone.
+    cold = None
+    if args.cold_steps:
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        ts = []
+        for i in range(args.cold_steps):
+            flush.fill_(i & 0xFF)
+            a, bb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            step(i)
+            bb.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(bb))
+        del flush
+        ms_cold = sorted(ts)[len(ts) // 2]
+        cold = {"ms_per_step_median": ms_cold, "candidates_per_s": total / (ms_cold / 1e3),
+                "hbm_gbps": alg[0] / (ms_cold / 1e3) / 1e9}
+
+    # Per-request latency: single cc_join calls cycling through 64 distinct requests.
+    lat = None
+    if args.latency_calls:
+        singles = [(q, torch.empty(q.cand_idx.numel(), wd + we, dtype=torch.uint8, device=dev),
+                    torch.empty(q.cand_idx.numel(), 1, dtype=torch.int8, device=dev))
+                   for q in batches[0][0]]
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.latency_calls)]
+        for i in range(32):
+            q, o, h = singles[i % len(singles)]
+            P.cc_join(store, q.cand_idx, q.keys, q.edge_rows, o, h)
+        torch.cuda.synchronize()
+        for i, (a, bb) in enumerate(evs):
+            q, o, h = singles[i % len(singles)]
+            a.record()
+            P.cc_join(store, q.cand_idx, q.keys, q.edge_rows, o, h)
+            bb.record()
+        torch.cuda.synchronize()
+        ms = sorted(a.elapsed_time(bb) for a, bb in evs)
+        pick = lambda p: ms[min(len(ms) - 1, int(p * len(ms)))]
+        lat = {"p50_ms": pick(0.50), "p99_ms": pick(0.99), "calls": len(ms),
+               "candidates_per_request": singles[0][0].cand_idx.numel()}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        reqs_cpu = [W.Request(q.keys.cpu(), q.edge_rows.cpu(), q.cand_idx.cpu(), None)
+                    for q in batches[0][0][:16]]
+        cpu = cpu_baseline((st.author_id.cpu(), st.doc_rows.cpu()), reqs_cpu, args.cpu_seconds)
+
+    P.cc_store_destroy(store)
+    line = {
+        "metric": METRIC,
+        "value": cands_per_s,
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {
+            "workload": "production single-viewer shape x64 per step: 10M-doc store "
+                        "(Zipf(1.1) authors, 64 bf16 doc cols), K=5000 keys with 32 bf16 edge "
+                        "cols, N=50000 candidates (70% in-network); one cc_join_batched launch "
+                        "of 64 requests",
+            "requests_per_step": REQS_PER_STEP,
+            "candidates_per_step": total,
+            "payload": "bf16 rows copied bit-exact",
+            "distinct_batches": N_BATCHES,
+        },
+        "hbm_gbps": achieved,
+        "hbm_frac_of_peak": achieved / PEAK_GBPS,
+        "latency": lat,
+        "p99_ms": None if lat is None else lat["p99_ms"],
+        "cold": cold,
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": PEAK_GBPS, "unit": "GB/s",
+            "frac": achieved / PEAK_GBPS, "traffic": load_traffic(),
+            "kernel": "join_kernel<8,4,1>", "algorithmic_bytes_per_launch": alg_per_launch,
+        },
+        "cpu_baseline": cpu,
+        "wall_s_timed_region": wall,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

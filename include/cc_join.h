@@ -1,0 +1,228 @@
+/*
+ * cc_join.h -- C ABI of the MI355X edge-feature join library (libccjoin.so).
+ *
+ * The operation is the edge-feature join of Connected Content Retriever (§3.1, Eq. 1 and
+ * Alg. 1): every candidate document carries an author id; the viewer's affinity records are
+ * a sorted list of author ids with one feature row each; a candidate whose author id is in
+ * the list receives that feature row, otherwise the zero row. The library fuses this with the
+ * gather of the candidate's own document-feature row from a device-resident store (§6.3: the
+ * document features live in GPU memory and are resolved by position), so that one call writes
+ * the model-input slice
+ *
+ *      out[j] = [ doc_rows[cand_idx[j]] | edge row of lookup 0 | edge row of lookup 1 ... ]
+ *
+ * and a hit mask. All row data are opaque byte strings: the library never converts, rounds or
+ * canonicalises a value (NaN payloads, signed zeros and subnormals are copied bit for bit).
+ *
+ * General conventions
+ *   - Every per-call array is caller-owned device memory unless stated otherwise; it must
+ *     stay alive until the work enqueued on `stream` has completed.
+ *   - The join calls enqueue work on `stream` and return; they never synchronise and never
+ *     allocate. Host-checkable argument errors return before anything is enqueued.
+ *   - Data-dependent conditions that a check would need a synchronisation to see have
+ *     defined, memory-safe outcomes instead of errors (see cc_join_batched).
+ *   - No C++ exception crosses this interface.
+ *   - A store is read-only after creation: concurrent joins on one store, from any threads
+ *     and streams, are safe.
+ */
+#ifndef CC_JOIN_H
+#define CC_JOIN_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define CC_API __attribute__((visibility("default")))
+#else
+#define CC_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct cc_store cc_store;   /* opaque; device-resident document store */
+
+typedef enum cc_status {
+    CC_OK = 0,
+    CC_ERR_INVALID_ARGUMENT = 1,   /* a host-checkable argument is wrong; nothing enqueued   */
+    CC_ERR_OUT_OF_MEMORY = 2,      /* device allocation failed (store creation only)        */
+    CC_ERR_DEVICE = 3,             /* a HIP call failed; see cc_last_device_error()         */
+    CC_ERR_UNSORTED_KEYS = 4,      /* only from cc_validate_keys                            */
+    CC_ERR_NOT_SUPPORTED = 5       /* no usable gfx950 device                               */
+} cc_status;
+
+/* Where cc_store_create reads its source arrays from. */
+#define CC_SRC_HOST 1u
+#define CC_SRC_DEVICE 2u
+
+/*
+ * cc_store_create -- copy a document store into library-owned device memory.
+ *
+ * §6.3 (Eq. 5): each document's feature tensors are stored in GPU memory and addressed by the
+ * document's position. Position p holds author_ids[p] and the row doc_rows[p].
+ *
+ *   out_store      receives the new store handle (set to NULL on error).
+ *   n_docs         number of documents, >= 0.
+ *   author_ids     [n_docs] int64 author id of each document (any int64 value).
+ *   doc_rows       [n_docs][doc_row_bytes] row-major document-feature rows.
+ *   doc_row_bytes  bytes per row; a positive multiple of 16.
+ *   flags          CC_SRC_HOST (sources are host memory) or CC_SRC_DEVICE (device memory).
+ *   stream         the copies are enqueued on this stream; the sources must stay valid until
+ *                  it has completed them. The store is usable by work later on the same stream
+ *                  (other streams must wait for it).
+ *
+ * The store is created on the current HIP device and stays on it. Layout in HBM: author ids
+ * as one int64 column, rows as one row-major array, both 256-byte aligned, plus an 8-byte
+ * counter of invalid candidate positions seen by joins.
+ * Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_OUT_OF_MEMORY (nothing leaked), CC_ERR_DEVICE,
+ * CC_ERR_NOT_SUPPORTED.
+ */
+CC_API cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *author_ids,
+                          const void *doc_rows, int32_t doc_row_bytes, uint32_t flags,
+                          hipStream_t stream);
+
+/* Free a store. The caller guarantees that no join using it is still in flight.
+ * NULL is accepted and ignored. */
+CC_API cc_status cc_store_destroy(cc_store *store);
+
+/* Report a store's size. Either output pointer may be NULL. */
+CC_API cc_status cc_store_info(const cc_store *store, int64_t *n_docs, int32_t *doc_row_bytes);
+
+/* Read the number of invalid candidate positions (outside [0, n_docs)) that joins on this
+ * store have met since creation or the last reset. Synchronises `stream` (debug/metrics). */
+CC_API cc_status cc_store_invalid_count(const cc_store *store, int64_t *count, hipStream_t stream);
+
+/* Reset that counter to zero, ordered on `stream` (no synchronisation). */
+CC_API cc_status cc_store_reset_invalid_count(cc_store *store, hipStream_t stream);
+
+/*
+ * cc_join -- one viewer: Eq. 1 for N candidates against K affinity records (§3.1, Alg. 1
+ * Steps 2-4; the keys arrive already sorted, i.e. after Alg. 1 Step 1).
+ *
+ *   store          document store (author id and doc row per position).
+ *   cand_idx       [n_cand] int64 candidate positions in the store (the output of the
+ *                  id -> position resolution of §6.3.1, where -1 means "not found").
+ *   n_cand         number of candidates, >= 0.
+ *   edge_keys      [n_keys] int64 viewer's affinity author ids, ascending in signed order.
+ *   n_keys         K >= 0; K = 0 makes every candidate a miss.
+ *   edge_feats     [n_keys][edge_row_bytes] feature row of each key (row i belongs to key i).
+ *   edge_row_bytes bytes per edge row; a positive multiple of 16.
+ *   default_row    [edge_row_bytes] row written on a miss, or NULL for zero bytes.
+ *   out            [n_cand][out_row_stride] output; row j gets
+ *                  [doc row (doc_row_bytes) | edge row or default (edge_row_bytes)];
+ *                  bytes past that width in each row are not written.
+ *   out_row_stride bytes between output rows; a multiple of 16, >= doc_row_bytes +
+ *                  edge_row_bytes.
+ *   hit_mask       [n_cand] int8: 1 when the author id was found, else 0.
+ *   stream         work is enqueued here.
+ *
+ * Alignment: edge_feats, default_row and out must be 16-byte aligned; cand_idx and
+ * edge_keys 8-byte aligned. This is cc_join_batched with one viewer and one lookup.
+ */
+CC_API cc_status cc_join(const cc_store *store,
+                  const int64_t *cand_idx, int64_t n_cand,
+                  const int64_t *edge_keys, int64_t n_keys,
+                  const void *edge_feats, int32_t edge_row_bytes,
+                  const void *default_row,
+                  void *out, int64_t out_row_stride,
+                  int8_t *hit_mask,
+                  hipStream_t stream);
+
+/*
+ * cc_join_batched -- B viewers in one launch, in CSR form (Alg. 1 is stated for a batch of B
+ * requests; ragged sizes are kept as offsets instead of padding), with one or two lookups per
+ * candidate.
+ *
+ *   n_viewers      B >= 0.
+ *   cand_offsets   [B+1] int64 device: viewer v owns candidates [cand_offsets[v],
+ *                  cand_offsets[v+1]); cand_offsets[0] = 0, non-decreasing,
+ *                  cand_offsets[B] = total_cand.
+ *   cand_idx       [total_cand] int64 candidate positions.
+ *   total_cand     host copy of cand_offsets[B].
+ *   key_offsets    [B+1] int64 device: viewer v owns keys/edge rows [key_offsets[v],
+ *                  key_offsets[v+1]); same rules, key_offsets[B] = total_keys.
+ *   edge_keys      [total_keys] int64, ascending within each viewer.
+ *   total_keys     host copy of key_offsets[B].
+ *   edge_feats     [total_keys][edge_row_bytes].
+ *   default_row    [edge_row_bytes] or NULL (zero bytes).
+ *   n_lookups      L in {1, 2}. Lookup 0 uses the store's author id of the candidate; lookup 1
+ *                  uses extra_keys[0][j] (e.g. the first-degree member who engaged with the
+ *                  post). Both search the same viewer's keys.
+ *   extra_keys     host array of L-1 device pointers, each [total_cand] int64; NULL when L=1.
+ *   out            [total_cand][out_row_stride]; row j = [doc row | lookup 0 row | lookup 1
+ *                  row]; out_row_stride is a multiple of 16 and >= doc_row_bytes +
+ *                  L * edge_row_bytes.
+ *   hit_mask       [total_cand][L] int8.
+ *
+ * Defined outcomes for data the host cannot check without synchronising:
+ *   - cand_idx[j] outside [0, n_docs): doc segment = zero bytes, every edge segment = the
+ *     default row, hit bits 0, and the store's invalid counter is incremented.
+ *   - Keys that are non-decreasing with repeats: the leftmost equal key's row is used.
+ *   - Keys that are not sorted, or offsets that break the rules above: the result is
+ *     unspecified but every memory access stays inside the arrays whose sizes total_cand and
+ *     total_keys describe (offsets are clamped to those sizes).
+ * Errors: CC_ERR_INVALID_ARGUMENT (null or misaligned pointers, bad sizes, L not in {1,2}),
+ * CC_ERR_DEVICE (the launch failed).
+ */
+CC_API cc_status cc_join_batched(const cc_store *store, int32_t n_viewers,
+                          const int64_t *cand_offsets, const int64_t *cand_idx,
+                          int64_t total_cand,
+                          const int64_t *key_offsets, const int64_t *edge_keys,
+                          int64_t total_keys,
+                          const void *edge_feats, int32_t edge_row_bytes,
+                          const void *default_row,
+                          int32_t n_lookups, const int64_t *const *extra_keys,
+                          void *out, int64_t out_row_stride, int8_t *hit_mask,
+                          hipStream_t stream);
+
+/*
+ * Launch tuning for cc_join_batched_tuned. A zero field means "choose automatically".
+ *   fence_stride   power of two >= 1: the search keeps every fence_stride-th key of a viewer
+ *                  in LDS and finishes with one read of the keys between two fences
+ *                  (1 = the whole key list in LDS).
+ *   lds_keys       capacity of the LDS key table, in keys (<= 19456, i.e. 152 KiB).
+ *   workgroups     number of workgroups of the launch.
+ * Results never depend on these values, only speed does.
+ */
+typedef struct cc_tuning {
+    int32_t fence_stride;
+    int32_t lds_keys;
+    int32_t workgroups;
+    int32_t reserved;
+} cc_tuning;
+
+/* cc_join_batched with explicit launch tuning (NULL = automatic). Same contract. */
+CC_API cc_status cc_join_batched_tuned(const cc_store *store, int32_t n_viewers,
+                                const int64_t *cand_offsets, const int64_t *cand_idx,
+                                int64_t total_cand,
+                                const int64_t *key_offsets, const int64_t *edge_keys,
+                                int64_t total_keys,
+                                const void *edge_feats, int32_t edge_row_bytes,
+                                const void *default_row,
+                                int32_t n_lookups, const int64_t *const *extra_keys,
+                                void *out, int64_t out_row_stride, int8_t *hit_mask,
+                                const cc_tuning *tuning, hipStream_t stream);
+
+/*
+ * cc_validate_keys -- debug helper: check that each viewer's keys are strictly increasing
+ * (the precondition under which the join result is unique, §3.1 Alg. 1 Step 1 output).
+ * Synchronises `stream`. Returns CC_OK, or CC_ERR_UNSORTED_KEYS with *first_bad_viewer set to
+ * the lowest offending viewer (otherwise it is set to -1). Offsets must satisfy the rules of
+ * cc_join_batched (they are clamped to total_keys).
+ */
+CC_API cc_status cc_validate_keys(const int64_t *key_offsets, const int64_t *edge_keys,
+                           int32_t n_viewers, int64_t total_keys, int64_t *first_bad_viewer,
+                           hipStream_t stream);
+
+/* Static string naming a status code. */
+CC_API const char *cc_status_string(cc_status status);
+
+/* The hipError_t of the last CC_ERR_DEVICE returned on the calling thread (0 if none). */
+CC_API int cc_last_device_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CC_JOIN_H */

@@ -1,0 +1,12 @@
+"""MI355X-native edge-feature join (Connected Content Retriever, §3.1 and §6.3).
+
+The work happens in ``libccjoin.so`` (hand-written HIP kernels for gfx950 behind the C ABI in
+``include/cc_join.h``). This package is a thin ctypes binding with the same function names; it
+only marshals arguments (device pointers, sizes, the stream) and raises ``CCError`` on a
+non-OK status. There is no fallback: if the library is not built, every call raises.
+"""
+from .binding import (  # noqa: F401
+    CCError, Tuning, cc_join, cc_join_batched, cc_last_device_error, cc_status_string,
+    cc_store_create, cc_store_destroy, cc_store_info, cc_store_invalid_count,
+    cc_store_reset_invalid_count, cc_validate_keys, lib, LIB_PATH, EXPORTS,
+)

@@ -1,0 +1,376 @@
+// C ABI of the edge-feature join library: argument validation, the device document store, and
+// launch geometry. The kernels live in join_kernels.hip.
+#include <stdint.h>
+#include <string.h>
+
+#include <new>
+
+#include <hip/hip_runtime.h>
+
+#include "cc_join.h"
+#include "join_internal.h"
+
+struct cc_store {
+    int device;
+    int64_t n_docs;
+    int32_t doc_row_bytes;
+    int64_t *d_author;               // [n_docs]
+    uint8_t *d_rows;                 // [n_docs][doc_row_bytes]
+    unsigned long long *d_invalid;   // invalid-position counter
+};
+
+namespace {
+
+thread_local int g_last_device_error = 0;
+
+cc_status device_error(hipError_t e) {
+    g_last_device_error = (int)e;
+    return CC_ERR_DEVICE;
+}
+
+bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+bool mul_ok(int64_t a, int64_t b, int64_t *r) { return !__builtin_mul_overflow(a, b, r); }
+
+// Keeps the store's device current for the duration of a call.
+class DeviceGuard {
+public:
+    explicit DeviceGuard(int dev) {
+        err_ = hipGetDevice(&prev_);
+        if (err_ == hipSuccess && prev_ != dev) {
+            err_ = hipSetDevice(dev);
+            switched_ = err_ == hipSuccess;
+        }
+    }
+    ~DeviceGuard() {
+        if (switched_)
+            (void)hipSetDevice(prev_);
+    }
+    hipError_t error() const { return err_; }
+
+private:
+    int prev_ = 0;
+    hipError_t err_ = hipSuccess;
+    bool switched_ = false;
+};
+
+struct DeviceInfo {
+    int cus = 256;
+};
+
+DeviceInfo device_info(int dev) {
+    DeviceInfo info;
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+        info.cus = v;
+    return info;
+}
+
+cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *cand_offsets,
+                    const int64_t *cand_idx, int64_t total_cand, const int64_t *key_offsets,
+                    const int64_t *edge_keys, int64_t total_keys, const void *edge_feats,
+                    int32_t edge_row_bytes, const void *default_row, int32_t n_lookups,
+                    const int64_t *extra, void *out, int64_t out_row_stride, int8_t *hit_mask,
+                    const cc_tuning *tuning, hipStream_t stream) {
+    // ---- host-side validation; nothing touches the device before it passes ----
+    if (!store || n_viewers < 0 || total_cand < 0 || total_keys < 0)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (edge_row_bytes <= 0 || (edge_row_bytes & 15))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_lookups != 1 && n_lookups != 2)
+        return CC_ERR_INVALID_ARGUMENT;
+    const int64_t width = (int64_t)store->doc_row_bytes + (int64_t)n_lookups * edge_row_bytes;
+    if (out_row_stride < width || (out_row_stride & 15))
+        return CC_ERR_INVALID_ARGUMENT;
+    int64_t bytes = 0;
+    if (!mul_ok(total_cand, out_row_stride, &bytes) || !mul_ok(total_keys, edge_row_bytes, &bytes) ||
+        !mul_ok(total_cand, n_lookups, &bytes))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_viewers > 0 && cand_offsets == nullptr && key_offsets == nullptr) {
+        // single-viewer form (cc_join): offsets are implicit
+    } else if (n_viewers > 0 && (!cand_offsets || !key_offsets)) {
+        return CC_ERR_INVALID_ARGUMENT;
+    }
+    if (total_cand > 0 && (n_viewers == 0 || !cand_idx || !out || !hit_mask))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (total_keys > 0 && (!edge_keys || !edge_feats))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_lookups == 2 && total_cand > 0 && !extra)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (!aligned(out, 16) || !aligned(edge_feats, 16) || !aligned(default_row, 16) ||
+        !aligned(cand_idx, 8) || !aligned(edge_keys, 8) || !aligned(cand_offsets, 8) ||
+        !aligned(key_offsets, 8) || !aligned(extra, 8))
+        return CC_ERR_INVALID_ARGUMENT;
+    int32_t lds_cap = ccj::kDefaultLdsKeys, stride = 0, wgs = 0;
+    if (tuning) {
+        if (tuning->fence_stride < 0 || tuning->lds_keys < 0 || tuning->workgroups < 0 ||
+            tuning->lds_keys > ccj::kMaxLdsKeys)
+            return CC_ERR_INVALID_ARGUMENT;
+        if (tuning->fence_stride & (tuning->fence_stride - 1))
+            return CC_ERR_INVALID_ARGUMENT;
+        if (tuning->lds_keys)
+            lds_cap = tuning->lds_keys;
+        stride = tuning->fence_stride;
+        wgs = tuning->workgroups;
+    }
+    if (total_cand == 0)
+        return CC_OK;
+
+    DeviceGuard guard(store->device);
+    if (guard.error() != hipSuccess)
+        return device_error(guard.error());
+
+    ccj::JoinArgs a;
+    a.author = store->d_author;
+    a.doc = store->d_rows;
+    a.n_docs = store->n_docs;
+    a.doc_bytes = store->doc_row_bytes;
+    a.edge_bytes = edge_row_bytes;
+    a.cand_offsets = cand_offsets;
+    a.cand_idx = cand_idx;
+    a.total_cand = total_cand;
+    a.key_offsets = key_offsets;
+    a.keys = edge_keys;
+    a.total_keys = total_keys;
+    a.edge = static_cast<const uint8_t *>(edge_feats);
+    a.def_row = static_cast<const uint8_t *>(default_row);
+    a.extra = extra;
+    a.out = static_cast<uint8_t *>(out);
+    a.out_stride = out_row_stride;
+    a.hit = hit_mask;
+    a.invalid_counter = store->d_invalid;
+    a.n_viewers = cand_offsets ? n_viewers : 1;
+    a.fence_stride = stride;
+    // The LDS table never needs more entries than the largest viewer has keys.
+    a.lds_keys = (int32_t)(total_keys < lds_cap ? (total_keys > 0 ? total_keys : 1) : lds_cap);
+
+    // Launch geometry: about one resident wave of workgroups, each owning a contiguous range of
+    // whole sub-tiles; the count is a multiple of 8 so that each XCD gets an equal share.
+    const int64_t tiles = (total_cand + ccj::kBlock - 1) / ccj::kBlock;
+    int64_t n_wg = wgs;
+    if (n_wg <= 0) {
+        const int64_t lds_bytes = (int64_t)a.lds_keys * 8 + (1 + n_lookups) * ccj::kBlock * 8;
+        int64_t per_cu = (160 * 1024) / lds_bytes;
+        per_cu = per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu);
+        n_wg = (int64_t)device_info(store->device).cus * per_cu;
+    }
+    if (n_wg > tiles)
+        n_wg = tiles;
+    const int64_t tiles_per_wg = (tiles + n_wg - 1) / n_wg;
+    a.per_wg = tiles_per_wg * ccj::kBlock;
+    n_wg = (total_cand + a.per_wg - 1) / a.per_wg;
+    n_wg = (n_wg + 7) & ~int64_t(7);
+    if (n_wg > (int64_t)1 << 30)
+        return CC_ERR_INVALID_ARGUMENT;
+    a.n_wg = (int32_t)n_wg;
+
+    hipError_t e = ccj::launch_join(a, n_lookups, stream);
+    if (e != hipSuccess)
+        return device_error(e);
+    return CC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *author_ids,
+                          const void *doc_rows, int32_t doc_row_bytes, uint32_t flags,
+                          hipStream_t stream) {
+    if (!out_store)
+        return CC_ERR_INVALID_ARGUMENT;
+    *out_store = nullptr;
+    if (n_docs < 0 || doc_row_bytes <= 0 || (doc_row_bytes & 15))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (flags != CC_SRC_HOST && flags != CC_SRC_DEVICE)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_docs > 0 && (!author_ids || !doc_rows))
+        return CC_ERR_INVALID_ARGUMENT;
+    int64_t row_total = 0, id_total = 0;
+    if (!mul_ok(n_docs, doc_row_bytes, &row_total) || !mul_ok(n_docs, 8, &id_total))
+        return CC_ERR_INVALID_ARGUMENT;
+
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e == hipErrorNoDevice ? CC_ERR_NOT_SUPPORTED : device_error(e);
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess)
+        return device_error(e);
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return CC_ERR_NOT_SUPPORTED;
+
+    cc_store *s = new (std::nothrow) cc_store();
+    if (!s)
+        return CC_ERR_OUT_OF_MEMORY;
+    s->device = dev;
+    s->n_docs = n_docs;
+    s->doc_row_bytes = doc_row_bytes;
+    auto fail = [&](hipError_t err) {
+        (void)hipFree(s->d_author);
+        (void)hipFree(s->d_rows);
+        (void)hipFree(s->d_invalid);
+        delete s;
+        if (err == hipErrorOutOfMemory || err == hipErrorMemoryAllocation) {
+            g_last_device_error = (int)err;
+            (void)hipGetLastError();
+            return CC_ERR_OUT_OF_MEMORY;
+        }
+        return device_error(err);
+    };
+    if ((e = hipMalloc(&s->d_author, (size_t)(id_total > 0 ? id_total : 256))) != hipSuccess)
+        return fail(e);
+    if ((e = hipMalloc(&s->d_rows, (size_t)(row_total > 0 ? row_total : 256))) != hipSuccess)
+        return fail(e);
+    if ((e = hipMalloc(&s->d_invalid, sizeof(unsigned long long))) != hipSuccess)
+        return fail(e);
+    const hipMemcpyKind kind = flags == CC_SRC_HOST ? hipMemcpyHostToDevice
+                                                    : hipMemcpyDeviceToDevice;
+    if (n_docs > 0) {
+        if ((e = hipMemcpyAsync(s->d_author, author_ids, (size_t)id_total, kind, stream)) != hipSuccess)
+            return fail(e);
+        if ((e = hipMemcpyAsync(s->d_rows, doc_rows, (size_t)row_total, kind, stream)) != hipSuccess)
+            return fail(e);
+    }
+    if ((e = hipMemsetAsync(s->d_invalid, 0, sizeof(unsigned long long), stream)) != hipSuccess)
+        return fail(e);
+    *out_store = s;
+    return CC_OK;
+}
+
+cc_status cc_store_destroy(cc_store *store) {
+    if (!store)
+        return CC_OK;
+    DeviceGuard guard(store->device);
+    (void)hipFree(store->d_author);
+    (void)hipFree(store->d_rows);
+    (void)hipFree(store->d_invalid);
+    delete store;
+    return CC_OK;
+}
+
+cc_status cc_store_info(const cc_store *store, int64_t *n_docs, int32_t *doc_row_bytes) {
+    if (!store)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_docs)
+        *n_docs = store->n_docs;
+    if (doc_row_bytes)
+        *doc_row_bytes = store->doc_row_bytes;
+    return CC_OK;
+}
+
+cc_status cc_store_invalid_count(const cc_store *store, int64_t *count, hipStream_t stream) {
+    if (!store || !count)
+        return CC_ERR_INVALID_ARGUMENT;
+    DeviceGuard guard(store->device);
+    unsigned long long v = 0;
+    hipError_t e = hipMemcpyAsync(&v, store->d_invalid, sizeof(v), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(stream);
+    if (e != hipSuccess)
+        return device_error(e);
+    *count = (int64_t)v;
+    return CC_OK;
+}
+
+cc_status cc_store_reset_invalid_count(cc_store *store, hipStream_t stream) {
+    if (!store)
+        return CC_ERR_INVALID_ARGUMENT;
+    DeviceGuard guard(store->device);
+    hipError_t e = hipMemsetAsync(store->d_invalid, 0, sizeof(unsigned long long), stream);
+    return e == hipSuccess ? CC_OK : device_error(e);
+}
+
+cc_status cc_join(const cc_store *store, const int64_t *cand_idx, int64_t n_cand,
+                  const int64_t *edge_keys, int64_t n_keys, const void *edge_feats,
+                  int32_t edge_row_bytes, const void *default_row, void *out,
+                  int64_t out_row_stride, int8_t *hit_mask, hipStream_t stream) {
+    return join_impl(store, 1, nullptr, cand_idx, n_cand, nullptr, edge_keys, n_keys, edge_feats,
+                     edge_row_bytes, default_row, 1, nullptr, out, out_row_stride, hit_mask,
+                     nullptr, stream);
+}
+
+cc_status cc_join_batched_tuned(const cc_store *store, int32_t n_viewers,
+                                const int64_t *cand_offsets, const int64_t *cand_idx,
+                                int64_t total_cand, const int64_t *key_offsets,
+                                const int64_t *edge_keys, int64_t total_keys,
+                                const void *edge_feats, int32_t edge_row_bytes,
+                                const void *default_row, int32_t n_lookups,
+                                const int64_t *const *extra_keys, void *out,
+                                int64_t out_row_stride, int8_t *hit_mask,
+                                const cc_tuning *tuning, hipStream_t stream) {
+    if (n_viewers > 0 && (!cand_offsets || !key_offsets))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_lookups == 2 && !extra_keys)
+        return CC_ERR_INVALID_ARGUMENT;
+    const int64_t *extra = (n_lookups == 2) ? extra_keys[0] : nullptr;
+    return join_impl(store, n_viewers, cand_offsets, cand_idx, total_cand, key_offsets,
+                     edge_keys, total_keys, edge_feats, edge_row_bytes, default_row, n_lookups,
+                     extra, out, out_row_stride, hit_mask, tuning, stream);
+}
+
+cc_status cc_join_batched(const cc_store *store, int32_t n_viewers, const int64_t *cand_offsets,
+                          const int64_t *cand_idx, int64_t total_cand,
+                          const int64_t *key_offsets, const int64_t *edge_keys,
+                          int64_t total_keys, const void *edge_feats, int32_t edge_row_bytes,
+                          const void *default_row, int32_t n_lookups,
+                          const int64_t *const *extra_keys, void *out, int64_t out_row_stride,
+                          int8_t *hit_mask, hipStream_t stream) {
+    return cc_join_batched_tuned(store, n_viewers, cand_offsets, cand_idx, total_cand,
+                                 key_offsets, edge_keys, total_keys, edge_feats, edge_row_bytes,
+                                 default_row, n_lookups, extra_keys, out, out_row_stride,
+                                 hit_mask, nullptr, stream);
+}
+
+cc_status cc_validate_keys(const int64_t *key_offsets, const int64_t *edge_keys,
+                           int32_t n_viewers, int64_t total_keys, int64_t *first_bad_viewer,
+                           hipStream_t stream) {
+    if (!first_bad_viewer || n_viewers < 0 || total_keys < 0)
+        return CC_ERR_INVALID_ARGUMENT;
+    *first_bad_viewer = -1;
+    if (n_viewers > 0 && !key_offsets)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (total_keys > 0 && !edge_keys)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (!aligned(key_offsets, 8) || !aligned(edge_keys, 8))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_viewers == 0 || total_keys == 0)
+        return CC_OK;
+    unsigned long long *d_bad = nullptr;
+    hipError_t e = hipMalloc(&d_bad, sizeof(*d_bad));
+    if (e != hipSuccess)
+        return device_error(e);
+    unsigned long long bad = ~0ull;
+    e = hipMemcpyAsync(d_bad, &bad, sizeof(bad), hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess)
+        e = ccj::launch_validate_keys(key_offsets, edge_keys, n_viewers, total_keys, d_bad, stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(&bad, d_bad, sizeof(bad), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(stream);
+    (void)hipFree(d_bad);
+    if (e != hipSuccess)
+        return device_error(e);
+    if (bad != ~0ull) {
+        *first_bad_viewer = (int64_t)bad;
+        return CC_ERR_UNSORTED_KEYS;
+    }
+    return CC_OK;
+}
+
+const char *cc_status_string(cc_status status) {
+    switch (status) {
+    case CC_OK: return "CC_OK";
+    case CC_ERR_INVALID_ARGUMENT: return "CC_ERR_INVALID_ARGUMENT";
+    case CC_ERR_OUT_OF_MEMORY: return "CC_ERR_OUT_OF_MEMORY";
+    case CC_ERR_DEVICE: return "CC_ERR_DEVICE";
+    case CC_ERR_UNSORTED_KEYS: return "CC_ERR_UNSORTED_KEYS";
+    case CC_ERR_NOT_SUPPORTED: return "CC_ERR_NOT_SUPPORTED";
+    }
+    return "CC_UNKNOWN_STATUS";
+}
+
+int cc_last_device_error(void) { return g_last_device_error; }
+
+}  // extern "C"

@@ -1,0 +1,49 @@
+// Internal interface between the C ABI layer (cc_api.hip) and the kernels (join_kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ccj {
+
+constexpr int kBlock = 256;          // threads per workgroup = candidates per sub-tile
+constexpr int kWindow = 15;          // keys between two fences read from L2 in one step
+constexpr int kMaxLdsKeys = 19456;   // LDS key table limit (152 KiB of the 160 KiB per CU)
+constexpr int kDefaultLdsKeys = 4096;
+
+struct JoinArgs {
+    const int64_t *author;       // store: author id per position
+    const uint8_t *doc;          // store: rows, doc_bytes each
+    int64_t n_docs;
+    int32_t doc_bytes;
+    int32_t edge_bytes;
+    const int64_t *cand_offsets; // [B+1] or nullptr for one viewer
+    const int64_t *cand_idx;
+    int64_t total_cand;
+    const int64_t *key_offsets;  // [B+1] or nullptr for one viewer
+    const int64_t *keys;
+    int64_t total_keys;
+    const uint8_t *edge;
+    const uint8_t *def_row;      // nullptr = zero bytes
+    const int64_t *extra;        // keys of lookup 1 (n_lookups == 2)
+    uint8_t *out;
+    int64_t out_stride;
+    int8_t *hit;
+    unsigned long long *invalid_counter;
+    int32_t n_viewers;
+    int32_t lds_keys;            // capacity of the dynamic LDS key table
+    int32_t fence_stride;        // 0 = chosen per viewer segment
+    int32_t n_wg;                // workgroups launched (a multiple of 8)
+    int64_t per_wg;              // candidates per workgroup (a multiple of kBlock)
+};
+
+// Enqueue the join kernel matching the row widths and lookup count. Returns the HIP error of
+// the launch.
+hipError_t launch_join(const JoinArgs &args, int n_lookups, hipStream_t stream);
+
+// Enqueue the key-order check; *first_bad (device) must hold UINT64_MAX beforehand.
+hipError_t launch_validate_keys(const int64_t *key_offsets, const int64_t *keys,
+                                int32_t n_viewers, int64_t total_keys,
+                                unsigned long long *first_bad, hipStream_t stream);
+
+}  // namespace ccj

@@ -1,0 +1,100 @@
+"""CPU-side checks of the C ABI: the library loads, exports what the header declares, and
+rejects bad host arguments before touching a device (no compute calls here)."""
+from __future__ import annotations
+
+import ctypes
+import re
+from pathlib import Path
+
+import pytest
+
+import paper_2609_22441_amd as P
+from paper_2609_22441_amd import binding as B
+
+ROOT = Path(__file__).resolve().parents[1]
+
+
+def _declared():
+    text = (ROOT / "include" / "cc_join.h").read_text()
+    return sorted(set(re.findall(r"^CC_API\s+[\w\s\*]*?\b(cc_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_binding_surface():
+    assert _declared() == sorted(B.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(str(B.LIB_PATH))
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    assert P.cc_status_string(0) == "CC_OK"
+    assert P.cc_status_string(1) == "CC_ERR_INVALID_ARGUMENT"
+    assert P.cc_status_string(5) == "CC_ERR_NOT_SUPPORTED"
+    assert P.cc_status_string(99) == "CC_UNKNOWN_STATUS"
+    assert P.cc_last_device_error() == 0
+
+
+@pytest.mark.parametrize("n_docs,ids,rows,width,flags", [
+    (-1, None, None, 16, 1),          # negative size
+    (4, 8, 8, 24, 1),                 # row width not a multiple of 16
+    (4, 8, 8, 0, 1),                  # zero row width
+    (4, None, 8, 16, 1),              # missing author ids
+    (4, 8, None, 16, 1),              # missing rows
+    (0, None, None, 16, 3),           # unknown source flag
+    (1 << 62, 8, 8, 16, 1),           # byte size overflows int64
+])
+def test_store_create_rejects_bad_arguments(n_docs, ids, rows, width, flags):
+    lib = B.lib()
+    h = ctypes.c_void_p(1234)
+    st = lib.cc_store_create(ctypes.byref(h), n_docs, ids, rows, width, flags, None)
+    assert st == B.CC_ERR_INVALID_ARGUMENT
+    assert h.value is None
+
+
+def test_store_create_without_output_pointer():
+    assert B.lib().cc_store_create(None, 0, None, None, 16, 1, None) == B.CC_ERR_INVALID_ARGUMENT
+
+
+def test_join_rejects_null_store():
+    lib = B.lib()
+    assert lib.cc_join(None, None, 0, None, 0, None, 16, None, None, 32, None, None) == 1
+    assert lib.cc_join_batched(None, 0, None, None, 0, None, None, 0, None, 16, None, 1, None,
+                               None, 32, None, None) == 1
+
+
+def test_store_queries_reject_null():
+    lib = B.lib()
+    n = ctypes.c_int64()
+    assert lib.cc_store_info(None, ctypes.byref(n), None) == 1
+    assert lib.cc_store_invalid_count(None, ctypes.byref(n), None) == 1
+    assert lib.cc_store_reset_invalid_count(None, None) == 1
+    assert lib.cc_store_destroy(None) == 0
+
+
+def test_validate_keys_rejects_bad_arguments():
+    lib = B.lib()
+    bad = ctypes.c_int64(7)
+    assert lib.cc_validate_keys(None, None, 1, 0, None, None) == 1           # no output
+    assert lib.cc_validate_keys(None, None, 1, 0, ctypes.byref(bad), None) == 1  # no offsets
+    assert lib.cc_validate_keys(8, None, 1, 5, ctypes.byref(bad), None) == 1     # no keys
+    assert lib.cc_validate_keys(12, 16, 1, 5, ctypes.byref(bad), None) == 1      # misaligned
+    assert lib.cc_validate_keys(None, None, 0, 0, ctypes.byref(bad), None) == 0  # nothing to do
+    assert bad.value == -1
+
+
+def test_library_has_no_cpu_fallback(monkeypatch, tmp_path):
+    """The binding refuses to run when the HIP library is missing (no silent fallback)."""
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "LIB_PATH", tmp_path / "missing.so")
+    with pytest.raises(RuntimeError, match="not built"):
+        B.lib()
+
+
+def test_product_path_does_not_import_the_oracle():
+    for f in (ROOT / "paper_2609_22441_amd").rglob("*"):
+        if f.suffix in (".py", ".hip", ".h", ".cpp"):
+            text = f.read_text()
+            assert "oracle" not in text.lower().replace("oracle-free", ""), f

@@ -1,0 +1,124 @@
+"""GPU parity at the five workload shapes' full sizes, bit-exact against the oracle.
+
+Workloads 2-4 share one 10M-document store. Workload 5 holds a 200M-document store (27 GB)
+that is generated on the device; the oracle then runs on the candidate rows gathered from the
+generator's tensors (a compacted store holding exactly the documents the candidates name),
+which gives it the same answer as the full store.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_22441_amd as P
+import workload as W
+from gpu_common import assert_same, gpu_join, note, oracle_join, row_bytes
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+STORE_SEED = 2
+
+
+@pytest.fixture(scope="module")
+def store10m():
+    note("generating the 10M-document store")
+    s, _ = W.CONFIGS[2]
+    st = W.make_store(s, STORE_SEED, device=DEV)
+    h = P.cc_store_create(st.author_id, st.doc_rows)
+    torch.cuda.synchronize()
+    cpu = (st.author_id.cpu(), st.doc_rows.cpu())
+    yield st, h, cpu
+    P.cc_store_destroy(h)
+
+
+def _check(st, handle, cpu, reqs, n_lookups, single=False, what=""):
+    b = W.pack(reqs)
+    wd, we = row_bytes(st.doc_rows), row_bytes(b.edge_rows)
+    note(f"{what}: {b.n_viewers} viewers, {b.cand_idx.numel()} candidates, "
+         f"{b.keys.numel()} keys")
+    got = gpu_join(handle, None, b, wd, we, n_lookups, single=single)
+    want = oracle_join(cpu[0], cpu[1], b.to("cpu"), n_lookups)
+    assert_same(got, want, what)
+    return got
+
+
+@pytest.mark.timeout(300)
+def test_config1_single_viewer_tiny():
+    s, r = W.CONFIGS[1]
+    st = W.make_store(s, 1, device=DEV)
+    h = P.cc_store_create(st.author_id, st.doc_rows)
+    try:
+        reqs = W.make_requests(st, r, 1)
+        _, hit = _check(st, h, (st.author_id.cpu(), st.doc_rows.cpu()), reqs, 1, single=True,
+                        what="workload 1")
+        assert 0.005 < hit.mean() < 0.02          # ~1% expected
+    finally:
+        P.cc_store_destroy(h)
+
+
+@pytest.mark.timeout(300)
+def test_config2_single_viewer_production(store10m):
+    st, h, cpu = store10m
+    _, r = W.CONFIGS[2]
+    reqs = W.make_requests(st, r, 2)
+    _, hit = _check(st, h, cpu, reqs, 1, single=True, what="workload 2")
+    assert 0.6 < hit.mean() < 0.8                  # ~70.7% expected
+
+
+@pytest.mark.timeout(300)
+def test_config2_batched_as_benchmarked(store10m):
+    """64 production-shaped requests in one batched launch (the benchmark's step)."""
+    st, h, cpu = store10m
+    _, r = W.CONFIGS[2]
+    reqs = W.make_requests(st, r, 2, n_viewers=64)
+    _check(st, h, cpu, reqs, 1, what="workload 2 x64 batched")
+
+
+@pytest.mark.timeout(300)
+def test_config3_batched_ragged(store10m):
+    st, h, cpu = store10m
+    _, r = W.CONFIGS[3]
+    reqs = W.make_requests(st, r, 3)
+    ks = [q.keys.numel() for q in reqs]
+    assert min(ks) >= 100 and max(ks) <= 30_000
+    _check(st, h, cpu, reqs, 1, what="workload 3")
+
+
+@pytest.mark.timeout(300)
+def test_config4_double_join(store10m):
+    st, h, cpu = store10m
+    _, r = W.CONFIGS[4]
+    reqs = W.make_requests(st, r, 4)
+    _, hit = _check(st, h, cpu, reqs, 2, what="workload 4")
+    assert 0.6 < hit[:, 0].mean() < 0.8 and 0.45 < hit[:, 1].mean() < 0.55
+
+
+@pytest.mark.timeout(900)
+def test_config5_large_scale():
+    s, r = W.CONFIGS[5]
+    note("generating the 200M-document store on the device")
+    st = W.make_store(s, 5, device=DEV)
+    reqs = W.make_requests(st, r, 5)
+    st._by_author = None
+    b = W.pack(reqs)
+    wd, we = row_bytes(st.doc_rows), row_bytes(b.edge_rows)
+    # The oracle's store: only the documents the candidates name, in first-seen order.
+    uniq, inv = torch.unique(b.cand_idx, return_inverse=True)
+    mini_author = st.author_id[uniq].cpu()
+    mini_rows = st.doc_rows[uniq].cpu()
+    h = P.cc_store_create(st.author_id, st.doc_rows)
+    torch.cuda.synchronize()
+    del st
+    torch.cuda.empty_cache()
+    try:
+        note(f"workload 5: {b.n_viewers} viewers, {b.cand_idx.numel()} candidates, "
+             f"{b.keys.numel()} keys")
+        got = gpu_join(h, None, b, wd, we, 1)
+        bc = b.to("cpu")
+        bc.cand_idx = inv.cpu()
+        want = oracle_join(mini_author, mini_rows, bc, 1)
+        assert_same(got, want, "workload 5")
+        assert got[1].mean() > 0.99                # every candidate is in-network
+    finally:
+        P.cc_store_destroy(h)

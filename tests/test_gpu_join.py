@@ -1,0 +1,294 @@
+"""GPU parity of the HIP join against the oracle: edge cases, every search strategy, the
+argument checks that need a real store, and the store's counters. Bit-exact (tolerance 0)."""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_22441_amd as P
+from paper_2609_22441_amd import binding as B
+import workload as W
+from gpu_common import FILL, assert_same, gpu_join, note, oracle_join, row_bytes
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+# (fence_stride, lds_keys, workgroups): automatic, whole list in LDS, fixed strides, tiny LDS
+# tables that force strides beyond the 16-key window, and a single workgroup doing everything.
+TUNINGS = [None, (1, 4096, 0), (4, 0, 0), (16, 8, 0), (0, 2, 0), (2, 3, 8), (0, 0, 1)]
+
+
+def _tuning(t):
+    return None if t is None else P.Tuning(*t, 0)
+
+
+def _tiny(tc, tuning=None, stride_extra=0, what=""):
+    b = tc.batch.to(DEV)
+    wd, we = row_bytes(tc.doc_rows), row_bytes(tc.batch.edge_rows)
+    stride = wd + tc.n_lookups * we + stride_extra
+    store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+    try:
+        d = None if tc.default_row is None else tc.default_row.to(DEV)
+        got = gpu_join(store, None, b, wd, we, tc.n_lookups, default_row=d, stride=stride,
+                       tuning=_tuning(tuning))
+        want = oracle_join(tc.author_id, tc.doc_rows, tc.batch, tc.n_lookups,
+                           default_row=tc.default_row, stride=stride)
+        assert_same(got, want, what)
+        assert P.cc_store_invalid_count(store) == want[2], f"{what}: invalid count"
+    finally:
+        P.cc_store_destroy(store)
+
+
+@pytest.mark.parametrize("tuning", TUNINGS)
+def test_tiny_random_cases(tuning):
+    note(f"tiny random cases, tuning {tuning}")
+    for seed in range(40):
+        tc = W.tiny_case(seed, max_k=120, max_n=700, max_viewers=5)
+        _tiny(tc, tuning, stride_extra=16 * (seed % 2), what=f"seed {seed} tuning {tuning}")
+
+
+def test_duplicate_keys_leftmost():
+    note("duplicate keys")
+    for seed in range(20):
+        tc = W.tiny_case(1000 + seed, max_k=200, max_n=500, dup_keys=True)
+        for t in (None, (4, 0, 0), (0, 2, 0)):
+            _tiny(tc, t, what=f"dup seed {seed} tuning {t}")
+
+
+def test_empty_and_degenerate_viewers():
+    note("empty viewers, K=0, N=0")
+    # viewers with no candidates, no keys, and both, in every position
+    for seed in range(12):
+        tc = W.tiny_case(2000 + seed, max_k=30, max_n=40, max_viewers=6,
+                         k_values=[0, 5, 0, 17, 1, 0])
+        _tiny(tc, what=f"degenerate seed {seed}")
+
+
+def test_no_candidates_is_a_no_op():
+    st = W.tiny_case(3)
+    store = P.cc_store_create(st.author_id.to(DEV), st.doc_rows.to(DEV))
+    try:
+        empty = torch.empty(0, dtype=torch.int64, device=DEV)
+        keys = torch.tensor([1, 2], dtype=torch.int64, device=DEV)
+        edge = torch.zeros(2, 16, dtype=torch.uint8, device=DEV)
+        out = torch.empty(0, row_bytes(st.doc_rows) + 16, dtype=torch.uint8, device=DEV)
+        hit = torch.empty(0, 1, dtype=torch.int8, device=DEV)
+        P.cc_join(store, empty, keys, edge, out, hit)
+        torch.cuda.synchronize()
+    finally:
+        P.cc_store_destroy(store)
+
+
+def _scaled_store(seed, cfg=2, **kw):
+    kw = {"store_n_docs": 300_000, "store_n_authors": 200_000, **kw}
+    s, r = W.config(cfg, **kw)
+    st = W.make_store(s, seed, device=DEV)
+    return st, r
+
+
+@pytest.mark.parametrize("k", [1, 2, 15, 16, 17, 511, 512, 513, 4095, 4096, 4097, 8192, 8193,
+                               19456, 19457, 40000, 100_000])
+def test_key_count_thresholds(k):
+    """K around every table-size and stride boundary, automatic tuning, two lookups."""
+    note(f"K threshold {k}")
+    st, r = _scaled_store(7, cfg=4, store_n_authors=10_000_000, req_k=k, req_n_cand=6_000,
+                          req_n_viewers=2)
+    reqs = W.make_requests(st, r, 7)
+    b = W.pack(reqs)
+    store = P.cc_store_create(st.author_id, st.doc_rows)
+    try:
+        wd, we = row_bytes(st.doc_rows), row_bytes(b.edge_rows)
+        for t in (None, (1, 19456, 0), (8, 0, 0)):
+            got = gpu_join(store, None, b, wd, we, 2, tuning=_tuning(t))
+            want = oracle_join(st.author_id.cpu(), st.doc_rows.cpu(), b.to("cpu"), 2)
+            assert_same(got, want, f"K={k} tuning {t}")
+    finally:
+        P.cc_store_destroy(store)
+
+
+def test_single_viewer_entry_point():
+    note("cc_join single viewer, scaled production shape")
+    st, r = _scaled_store(9, req_k=3000, req_n_cand=20_000)
+    q = W.make_request(st, r, 9, 0)
+    b = W.pack([q])
+    store = P.cc_store_create(st.author_id, st.doc_rows)
+    try:
+        wd, we = row_bytes(st.doc_rows), row_bytes(b.edge_rows)
+        dflt = torch.arange(we, dtype=torch.uint8, device=DEV)
+        got = gpu_join(store, None, b, wd, we, 1, default_row=dflt, single=True)
+        want = oracle_join(st.author_id.cpu(), st.doc_rows.cpu(), b.to("cpu"), 1,
+                           default_row=dflt)
+        assert_same(got, want, "cc_join")
+    finally:
+        P.cc_store_destroy(store)
+
+
+def test_special_bit_patterns_are_copied_exactly():
+    note("NaN payloads, signed zeros, subnormals")
+    st, r = _scaled_store(10, req_k=2000, req_n_cand=10_000, req_n_viewers=3)
+    g = W.gen(DEV, 10, 77)
+    W.salt_special_values(st.doc_rows, 0.2, g)
+    reqs = W.make_requests(st, r, 10)
+    for q in reqs:
+        W.salt_special_values(q.edge_rows, 0.2, g)
+    b = W.pack(reqs)
+    store = P.cc_store_create(st.author_id, st.doc_rows)
+    try:
+        wd, we = row_bytes(st.doc_rows), row_bytes(b.edge_rows)
+        got = gpu_join(store, None, b, wd, we, 1)
+        want = oracle_join(st.author_id.cpu(), st.doc_rows.cpu(), b.to("cpu"), 1)
+        assert_same(got, want, "special values")
+    finally:
+        P.cc_store_destroy(store)
+
+
+def test_fp32_rows_of_the_tiny_shape():
+    note("fp32 rows (16 + 8 columns)")
+    s, r = W.config(1, store_n_docs=100_000)
+    st = W.make_store(s, 12, device=DEV)
+    b = W.pack([W.make_request(st, r, 12, 0)])
+    store = P.cc_store_create(st.author_id, st.doc_rows)
+    try:
+        wd, we = row_bytes(st.doc_rows), row_bytes(b.edge_rows)
+        got = gpu_join(store, None, b, wd, we, 1, single=True)
+        want = oracle_join(st.author_id.cpu(), st.doc_rows.cpu(), b.to("cpu"), 1)
+        assert_same(got, want, "fp32")
+    finally:
+        P.cc_store_destroy(store)
+
+
+def test_odd_row_widths_use_the_generic_copy():
+    note("generic widths 48 + 80 bytes")
+    tc = W.tiny_case(4242, max_k=100, max_n=900, doc_bytes=48, edge_bytes=80, n_lookups=2)
+    _tiny(tc, what="generic widths")
+
+
+def test_invalid_counter_and_reset():
+    note("invalid counter")
+    tc = W.tiny_case(77, max_n=500, n_lookups=1)
+    b = tc.batch.to(DEV)
+    n_docs = tc.author_id.numel()
+    b.cand_idx[::3] = -1
+    b.cand_idx[1::7] = n_docs
+    store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+    try:
+        wd, we = row_bytes(tc.doc_rows), row_bytes(tc.batch.edge_rows)
+        ci = b.cand_idx.cpu()
+        bad = int(((ci < 0) | (ci >= n_docs)).sum())
+        gpu_join(store, None, b, wd, we, 1)
+        gpu_join(store, None, b, wd, we, 1)
+        assert P.cc_store_invalid_count(store) == 2 * bad
+        P.cc_store_reset_invalid_count(store)
+        assert P.cc_store_invalid_count(store) == 0
+        assert P.cc_store_info(store) == (n_docs, wd)
+    finally:
+        P.cc_store_destroy(store)
+
+
+def test_validate_keys():
+    note("cc_validate_keys")
+    ko = torch.tensor([0, 3, 3, 7, 9], dtype=torch.int64, device=DEV)
+    good = torch.tensor([1, 5, 9, -4, 0, 2, 8, 3, 4], dtype=torch.int64, device=DEV)
+    assert P.cc_validate_keys(ko, good) == -1
+    dup = good.clone()
+    dup[5] = 0                      # viewer 2 now has a repeat
+    assert P.cc_validate_keys(ko, dup) == 2
+    uns = good.clone()
+    uns[8] = 1                      # viewer 3 now descends
+    assert P.cc_validate_keys(ko, uns) == 3
+
+
+def test_argument_errors_with_a_real_store():
+    note("host argument checks")
+    tc = W.tiny_case(5, n_lookups=1, doc_bytes=32, edge_bytes=16)
+    store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+    lib = B.lib()
+    try:
+        n = 8
+        cand = torch.zeros(n, dtype=torch.int64, device=DEV)
+        keys = torch.arange(4, dtype=torch.int64, device=DEV)
+        edge = torch.zeros(4, 16, dtype=torch.uint8, device=DEV)
+        out = torch.zeros(n, 64, dtype=torch.uint8, device=DEV)
+        hit = torch.zeros(n, 2, dtype=torch.int8, device=DEV)
+        s = torch.cuda.current_stream().cuda_stream
+        p = lambda t: t.data_ptr()
+
+        def join(**kw):
+            a = dict(cand=p(cand), n=n, keys=p(keys), k=4, edge=p(edge), ew=16, d=None,
+                     out=p(out), stride=48, hit=p(hit))
+            a.update(kw)
+            return lib.cc_join(store, a["cand"], a["n"], a["keys"], a["k"], a["edge"], a["ew"],
+                               a["d"], a["out"], a["stride"], a["hit"], s)
+
+        assert join() == 0
+        assert join(out=p(out) + 8) == 1                    # misaligned output
+        assert join(edge=p(edge) + 4) == 1                  # misaligned edge rows
+        assert join(cand=p(cand) + 4) == 1                  # misaligned candidates
+        assert join(d=p(edge) + 8) == 1                     # misaligned default row
+        assert join(stride=40) == 1                         # stride below the row width
+        assert join(stride=56) == 1                         # stride not a multiple of 16
+        assert join(ew=24) == 1                             # edge width not a multiple of 16
+        assert join(n=-1) == 1
+        assert join(k=-1) == 1
+        assert join(cand=None) == 1
+        assert join(keys=None) == 1                         # K > 0 needs keys
+        assert join(keys=None, edge=None, k=0) == 0         # K = 0 needs neither
+        co = torch.tensor([0, n], dtype=torch.int64, device=DEV)
+        ko = torch.tensor([0, 4], dtype=torch.int64, device=DEV)
+
+        def batched(L=1, extra=None, **kw):
+            return lib.cc_join_batched(store, 1, p(co), p(cand), n, p(ko), p(keys), 4, p(edge),
+                                       16, None, L, extra, p(out), kw.get("stride", 64),
+                                       p(hit), s)
+
+        assert batched() == 0
+        assert batched(L=3) == 1
+        assert batched(L=2) == 1                            # no extra key arrays
+        arr = (ctypes.c_void_p * 1)(None)
+        assert batched(L=2, extra=arr) == 1                 # null extra key array
+        arr = (ctypes.c_void_p * 1)(p(cand))
+        assert batched(L=2, extra=arr) == 0
+        assert batched(L=2, extra=arr, stride=48) == 1      # two lookups need 64 bytes
+        assert lib.cc_join_batched(store, 1, None, p(cand), n, p(ko), p(keys), 4, p(edge), 16,
+                                   None, 1, None, p(out), 64, p(hit), s) == 1
+        tun = P.Tuning(3, 0, 0, 0)                          # stride not a power of two
+        assert lib.cc_join_batched_tuned(store, 1, p(co), p(cand), n, p(ko), p(keys), 4,
+                                         p(edge), 16, None, 1, None, p(out), 64, p(hit),
+                                         ctypes.byref(tun), s) == 1
+        tun = P.Tuning(0, 20000, 0, 0)                      # LDS table too large
+        assert lib.cc_join_batched_tuned(store, 1, p(co), p(cand), n, p(ko), p(keys), 4,
+                                         p(edge), 16, None, 1, None, p(out), 64, p(hit),
+                                         ctypes.byref(tun), s) == 1
+        torch.cuda.synchronize()
+    finally:
+        P.cc_store_destroy(store)
+
+
+def test_concurrent_streams_share_a_store():
+    note("two streams, one store")
+    st, r = _scaled_store(13, req_k=2500, req_n_cand=15_000, req_n_viewers=2)
+    reqs = W.make_requests(st, r, 13)
+    store = P.cc_store_create(st.author_id, st.doc_rows)
+    try:
+        torch.cuda.synchronize()
+        wd = row_bytes(st.doc_rows)
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+        outs = []
+        for q, sm in zip(reqs, streams):
+            b = W.pack([q])
+            we = row_bytes(b.edge_rows)
+            out = torch.full((b.cand_idx.numel(), wd + we), FILL, dtype=torch.uint8, device=DEV)
+            hit = torch.zeros(b.cand_idx.numel(), 1, dtype=torch.int8, device=DEV)
+            with torch.cuda.stream(sm):
+                P.cc_join(store, b.cand_idx, b.keys, b.edge_rows, out, hit, stream=sm)
+            outs.append((b, out, hit))
+        torch.cuda.synchronize()
+        for i, (b, out, hit) in enumerate(outs):
+            want = oracle_join(st.author_id.cpu(), st.doc_rows.cpu(), b.to("cpu"), 1)
+            assert_same((out.cpu().numpy(), hit.cpu().numpy()), want, f"stream {i}")
+    finally:
+        P.cc_store_destroy(store)

@@ -219,6 +219,8 @@ def _keys(store: Store, r: RequestSpec, k: int, g, device):
     elif r.key_mode == "top1_half":
         h1 = k // 2
         top = store.top_ids
+        if top.numel() < h1:
+            raise ValueError(f"{h1} keys requested from only {top.numel()} top-1% ids")
         first = top[torch.randperm(top.numel(), generator=g, device=device)[:h1]]
         second = _uniform_unique(m, k - h1, first, g, device)
         keys = torch.cat([first, second])

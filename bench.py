@@ -41,10 +41,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--latency-calls", type=int, default=1024)
-    ap.add_argument("--cold-steps", type=int, default=20)
+    ap.add_argument("--cold-steps", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=2)
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="also run a plain 256 MiB device copy (known bytes) for counter scaling")
     return ap.parse_args()
 
 
@@ -196,6 +198,14 @@ def main():
         lat = {"p50_ms": pick(0.50), "p99_ms": pick(0.99), "calls": len(ms),
                "candidates_per_request": singles[0][0].cand_idx.numel()}
 
+    if args.calibration_copy:
+        src = torch.empty(1 << 28, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     cpu = None
     if not args.no_cpu_baseline:
         reqs_cpu = [W.Request(q.keys.cpu(), q.edge_rows.cpu(), q.cand_idx.cpu(), None)
@@ -234,7 +244,7 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_GBPS, "unit": "GB/s",
             "frac": achieved / PEAK_GBPS, "traffic": load_traffic(),
-            "kernel": "join_kernel<8,4,1>", "algorithmic_bytes_per_launch": alg_per_launch,
+            "kernel": "join_kernel<8, 4, 1, true>", "algorithmic_bytes_per_launch": alg_per_launch,
         },
         "cpu_baseline": cpu,
         "wall_s_timed_region": wall,

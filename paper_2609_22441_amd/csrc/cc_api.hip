@@ -17,6 +17,7 @@ struct cc_store {
     int64_t *d_author;               // [n_docs]
     uint8_t *d_rows;                 // [n_docs][doc_row_bytes]
     unsigned long long *d_invalid;   // invalid-position counter
+    uint8_t *d_zero;                 // ccj::kZeroRowBytes zero bytes, read in place of absent rows
 };
 
 namespace {
@@ -53,18 +54,6 @@ private:
     hipError_t err_ = hipSuccess;
     bool switched_ = false;
 };
-
-struct DeviceInfo {
-    int cus = 256;
-};
-
-DeviceInfo device_info(int dev) {
-    DeviceInfo info;
-    int v = 0;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
-        info.cus = v;
-    return info;
-}
 
 cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *cand_offsets,
                     const int64_t *cand_idx, int64_t total_cand, const int64_t *key_offsets,
@@ -104,7 +93,7 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
     int32_t lds_cap = ccj::kDefaultLdsKeys, stride = 0, wgs = 0;
     if (tuning) {
         if (tuning->fence_stride < 0 || tuning->lds_keys < 0 || tuning->workgroups < 0 ||
-            tuning->lds_keys > ccj::kMaxLdsKeys)
+            tuning->lds_keys > ccj::kMaxLdsKeys || tuning->workgroups > (1 << 30))
             return CC_ERR_INVALID_ARGUMENT;
         if (tuning->fence_stride & (tuning->fence_stride - 1))
             return CC_ERR_INVALID_ARGUMENT;
@@ -134,6 +123,7 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
     a.total_keys = total_keys;
     a.edge = static_cast<const uint8_t *>(edge_feats);
     a.def_row = static_cast<const uint8_t *>(default_row);
+    a.zero_row = store->d_zero;
     a.extra = extra;
     a.out = static_cast<uint8_t *>(out);
     a.out_stride = out_row_stride;
@@ -144,27 +134,7 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
     // The LDS table never needs more entries than the largest viewer has keys.
     a.lds_keys = (int32_t)(total_keys < lds_cap ? (total_keys > 0 ? total_keys : 1) : lds_cap);
 
-    // Launch geometry: about one resident wave of workgroups, each owning a contiguous range of
-    // whole sub-tiles; the count is a multiple of 8 so that each XCD gets an equal share.
-    const int64_t tiles = (total_cand + ccj::kBlock - 1) / ccj::kBlock;
-    int64_t n_wg = wgs;
-    if (n_wg <= 0) {
-        const int64_t lds_bytes = (int64_t)a.lds_keys * 8 + (1 + n_lookups) * ccj::kBlock * 8;
-        int64_t per_cu = (160 * 1024) / lds_bytes;
-        per_cu = per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu);
-        n_wg = (int64_t)device_info(store->device).cus * per_cu;
-    }
-    if (n_wg > tiles)
-        n_wg = tiles;
-    const int64_t tiles_per_wg = (tiles + n_wg - 1) / n_wg;
-    a.per_wg = tiles_per_wg * ccj::kBlock;
-    n_wg = (total_cand + a.per_wg - 1) / a.per_wg;
-    n_wg = (n_wg + 7) & ~int64_t(7);
-    if (n_wg > (int64_t)1 << 30)
-        return CC_ERR_INVALID_ARGUMENT;
-    a.n_wg = (int32_t)n_wg;
-
-    hipError_t e = ccj::launch_join(a, n_lookups, stream);
+    hipError_t e = ccj::launch_join(a, n_lookups, wgs, store->device, stream);
     if (e != hipSuccess)
         return device_error(e);
     return CC_OK;
@@ -211,6 +181,7 @@ cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *a
         (void)hipFree(s->d_author);
         (void)hipFree(s->d_rows);
         (void)hipFree(s->d_invalid);
+        (void)hipFree(s->d_zero);
         delete s;
         if (err == hipErrorOutOfMemory || err == hipErrorMemoryAllocation) {
             g_last_device_error = (int)err;
@@ -225,6 +196,8 @@ cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *a
         return fail(e);
     if ((e = hipMalloc(&s->d_invalid, sizeof(unsigned long long))) != hipSuccess)
         return fail(e);
+    if ((e = hipMalloc(&s->d_zero, ccj::kZeroRowBytes)) != hipSuccess)
+        return fail(e);
     const hipMemcpyKind kind = flags == CC_SRC_HOST ? hipMemcpyHostToDevice
                                                     : hipMemcpyDeviceToDevice;
     if (n_docs > 0) {
@@ -234,6 +207,8 @@ cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *a
             return fail(e);
     }
     if ((e = hipMemsetAsync(s->d_invalid, 0, sizeof(unsigned long long), stream)) != hipSuccess)
+        return fail(e);
+    if ((e = hipMemsetAsync(s->d_zero, 0, ccj::kZeroRowBytes, stream)) != hipSuccess)
         return fail(e);
     *out_store = s;
     return CC_OK;
@@ -246,6 +221,7 @@ cc_status cc_store_destroy(cc_store *store) {
     (void)hipFree(store->d_author);
     (void)hipFree(store->d_rows);
     (void)hipFree(store->d_invalid);
+    (void)hipFree(store->d_zero);
     delete store;
     return CC_OK;
 }

@@ -9,7 +9,8 @@ namespace ccj {
 constexpr int kBlock = 256;          // threads per workgroup = candidates per sub-tile
 constexpr int kWindow = 15;          // keys between two fences read from L2 in one step
 constexpr int kMaxLdsKeys = 19456;   // LDS key table limit (152 KiB of the 160 KiB per CU)
-constexpr int kDefaultLdsKeys = 4096;
+constexpr int kDefaultLdsKeys = 8192;   // 64 KiB: within the register-limited occupancy
+constexpr int kZeroRowBytes = 1024;    // >= the widest row of a compile-time specialisation
 
 struct JoinArgs {
     const int64_t *author;       // store: author id per position
@@ -25,6 +26,7 @@ struct JoinArgs {
     int64_t total_keys;
     const uint8_t *edge;
     const uint8_t *def_row;      // nullptr = zero bytes
+    const uint8_t *zero_row;     // kZeroRowBytes of zeros in device memory (store-owned)
     const int64_t *extra;        // keys of lookup 1 (n_lookups == 2)
     uint8_t *out;
     int64_t out_stride;
@@ -33,13 +35,15 @@ struct JoinArgs {
     int32_t n_viewers;
     int32_t lds_keys;            // capacity of the dynamic LDS key table
     int32_t fence_stride;        // 0 = chosen per viewer segment
-    int32_t n_wg;                // workgroups launched (a multiple of 8)
-    int64_t per_wg;              // candidates per workgroup (a multiple of kBlock)
+    int32_t n_wg;                // workgroups launched (a multiple of 8); set by launch_join
+    int64_t per_wg;              // candidates per workgroup (multiple of kBlock); set by launch_join
 };
 
-// Enqueue the join kernel matching the row widths and lookup count. Returns the HIP error of
-// the launch.
-hipError_t launch_join(const JoinArgs &args, int n_lookups, hipStream_t stream);
+// Enqueue the join kernel matching the row widths and lookup count on `device` (current).
+// `workgroups` > 0 fixes the grid; 0 sizes it from the kernel's occupancy. Returns the HIP
+// error of the launch.
+hipError_t launch_join(JoinArgs &args, int n_lookups, int32_t workgroups, int device,
+                       hipStream_t stream);
 
 // Enqueue the key-order check; *first_bad (device) must hold UINT64_MAX beforehand.
 hipError_t launch_validate_keys(const int64_t *key_offsets, const int64_t *keys,

@@ -23,10 +23,32 @@
 //            read those (at most S) keys from global memory (L2) in one step and count.
 //   hit    : some key equal to x in the inspected window; because keys ascend, the lower
 //            bound is then the leftmost equal key.
+#include <atomic>
+#include <map>
+#include <mutex>
+#include <utility>
+
 #include "join_internal.h"
 
 namespace ccj {
 namespace {
+
+// Workgroup barrier that orders LDS accesses only. The barriers here protect the LDS tables;
+// global loads and stores may stay in flight across them (a full __syncthreads() would
+// drain every outstanding global access first).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// 16-byte chunk as a native vector (HIP's uint4 is a struct wrapper that the compiler may keep
+// in scratch memory when it sits in an array).
+typedef unsigned int chunk_t __attribute__((ext_vector_type(4)));
+
+// s_waitcnt operand for "vector memory count 0", leaving the export and LDS/scalar counters
+// unconstrained (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+constexpr int kWaitVmcnt0 = (0x7 << 4) | (0xF << 8);
 
 __device__ __forceinline__ int64_t clamp64(int64_t v, int64_t hi) {
     return v < 0 ? 0 : (v > hi ? hi : v);
@@ -44,6 +66,23 @@ __device__ __forceinline__ int64_t count_less(const int64_t *t, int64_t n, int64
     return (b - t) + (*b < x ? 1 : 0);
 }
 
+// Inspect keys lo .. lo+W-1 (indices clamped to K-1, so every load is in bounds and all W
+// loads are issued together): count those < x among the first len, and note any equal to x.
+// A clamped repeat of k[K-1] adds no false match: if k[K-1] == x it lies inside the window.
+template <int W>
+__device__ __forceinline__ void scan_window(const int64_t *gk, int64_t K, int64_t lo, int64_t len,
+                                            int64_t x, int64_t &cnt, bool &eq) {
+    int64_t k[W];
+#pragma unroll
+    for (int t = 0; t < W; ++t)
+        k[t] = gk[min(lo + t, K - 1)];
+#pragma unroll
+    for (int t = 0; t < W; ++t) {
+        cnt += (t < len && k[t] < x) ? 1 : 0;
+        eq |= (k[t] == x);
+    }
+}
+
 // Index in [0, K) of the leftmost key equal to x, or -1.
 __device__ __forceinline__ int64_t find_key(int64_t x, const int64_t *tab, int64_t M, int S,
                                             const int64_t *gk, int64_t K) {
@@ -54,29 +93,29 @@ __device__ __forceinline__ int64_t find_key(int64_t x, const int64_t *tab, int64
         return (g < K && tab[g] == x) ? g : -1;
     if (g == 0)
         return tab[0] == x ? 0 : -1;
-    const int64_t lo = (g - 1) * S + 1;
-    const int64_t hi = min(g * (int64_t)S, K);
-    const int64_t *w = gk + lo;
-    int64_t len = hi - lo;
-    // Wide strides (only when K exceeds 16x the LDS table): narrow in global memory first.
-    while (len > kWindow) {
-        const int64_t half = len >> 1;
-        w = (w[half] < x) ? w + half : w;
-        len -= half;
-    }
-    // The lower bound lies in [w, w + len]; inspect w[0..len] (w[len] may be past the end).
-    const int64_t avail = (gk + K) - w;
+    // k[(g-1)S] < x <= k[gS]: the lower bound lies in [lo, lo + len].
+    int64_t lo = (g - 1) * S + 1;
+    int64_t len = min(g * (int64_t)S, K) - lo;
     int64_t cnt = 0;
     bool eq = false;
-#pragma unroll
-    for (int t = 0; t <= kWindow; ++t) {
-        if (t <= len && t < avail) {
-            const int64_t k = w[t];
-            cnt += (t < len && k < x) ? 1 : 0;
-            eq |= (k == x);
+    switch (S) {
+    case 2: scan_window<2>(gk, K, lo, len, x, cnt, eq); break;
+    case 4: scan_window<4>(gk, K, lo, len, x, cnt, eq); break;
+    case 8: scan_window<8>(gk, K, lo, len, x, cnt, eq); break;
+    case 16: scan_window<16>(gk, K, lo, len, x, cnt, eq); break;
+    default: {
+        // Strides beyond 16 (only when K exceeds 16x the LDS table): narrow in global memory.
+        const int64_t *w = gk + lo;
+        while (len > kWindow) {
+            const int64_t half = len >> 1;
+            w = (w[half] < x) ? w + half : w;
+            len -= half;
         }
+        lo = w - gk;
+        scan_window<kWindow + 1>(gk, K, lo, len, x, cnt, eq);
     }
-    return eq ? (w - gk) + cnt : -1;
+    }
+    return eq ? lo + cnt : -1;
 }
 
 // Fence stride for one segment: the smallest power of two whose fence count fits the LDS
@@ -95,96 +134,178 @@ __device__ __forceinline__ int64_t range_index(int b, int n) {
     return (int64_t)(b & 7) * per_xcd + (b >> 3);
 }
 
-// Copy one sub-tile's output rows. DOC_CH / EDGE_CH are row widths in 16-byte chunks
-// (0 = read them from the arguments).
+// Copy a full sub-tile (kBlock rows) whose widths are compile-time chunk counts. Thread tid
+// takes chunks e = i * kBlock + tid of the sub-tile's output, i.e. row e / CH, 16-byte column
+// e % CH, so each wavefront store covers 1 KiB of contiguous output (whole 128-byte lines: a
+// line split between two stores with the streaming hint would be written back twice). Every
+// load and store is unconditional (absent rows are read from the store's zero row), so each
+// thread has all CH loads in flight before its first store. `between()` runs after the loads
+// are issued and before the stores (the caller issues the next sub-tile's dependent loads
+// there). Output rows are written with the non-temporal hint: they are not read again, and
+// keeping them out of the caches leaves room for the author column, keys and edge rows.
+template <int DOC_CH, int EDGE_CH, int NL, typename Between>
+__device__ __forceinline__ void copy_full_tile(const JoinArgs &a, const int64_t *s_src,
+                                               const int64_t (*s_row)[kBlock], int64_t t0,
+                                               const uint8_t *miss_row, Between between) {
+    constexpr int CH = DOC_CH + NL * EDGE_CH;
+    const int tid = threadIdx.x;
+    chunk_t v[CH];
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+        const int e = i * kBlock + tid;
+        const int row = e / CH, k = e % CH;
+        const bool is_doc = k < DOC_CH;
+        const int kk = is_doc ? 0 : k - DOC_CH;
+        const int l = kk / EDGE_CH, q = kk % EDGE_CH;
+        const int64_t d = s_src[row];
+        const int64_t r = s_row[l][row];
+        const uint8_t *pd = d >= 0 ? a.doc + d * (DOC_CH * 16) + k * 16 : a.zero_row + k * 16;
+        const uint8_t *pe = r >= 0 ? a.edge + r * (EDGE_CH * 16) + q * 16 : miss_row + q * 16;
+        v[i] = *reinterpret_cast<const chunk_t *>(is_doc ? pd : pe);
+    }
+    between();
+    uint8_t *o = a.out + t0 * a.out_stride;
+    if (a.out_stride == CH * 16) {
+        // Packed rows: chunk e sits at byte 16 * e of the sub-tile.
+        chunk_t *po = reinterpret_cast<chunk_t *>(o) + tid;
+#pragma unroll
+        for (int i = 0; i < CH; ++i)
+            __builtin_nontemporal_store(v[i], po + i * kBlock);
+    } else {
+#pragma unroll
+        for (int i = 0; i < CH; ++i) {
+            const int e = i * kBlock + tid;
+            const int row = e / CH, k = e % CH;
+            __builtin_nontemporal_store(
+                v[i], reinterpret_cast<chunk_t *>(o + row * a.out_stride + k * 16));
+        }
+    }
+}
+
+// Copy the first n rows of a sub-tile (any widths). Used for segments shorter than a sub-tile
+// and for row widths without a compile-time specialisation, so it favours few live registers
+// over loads in flight. DOC_CH / EDGE_CH are row widths in 16-byte chunks (0 = read them from
+// the arguments).
 template <int DOC_CH, int EDGE_CH, int NL>
 __device__ __forceinline__ void copy_rows(const JoinArgs &a, const int64_t *s_src,
                                           const int64_t (*s_row)[kBlock], int64_t t0, int n) {
     const int tid = threadIdx.x;
-    if constexpr (DOC_CH > 0) {
-        constexpr int CH = DOC_CH + NL * EDGE_CH;
-        uint4 v[CH];
+    const int dch = DOC_CH > 0 ? DOC_CH : (a.doc_bytes >> 4);
+    const int ech = EDGE_CH > 0 ? EDGE_CH : (a.edge_bytes >> 4);
+    const int dbytes = dch * 16, ebytes = ech * 16;
+    const int ch = dch + NL * ech;
+    const int total = n * ch;
+    constexpr int U = 4;
+    for (int base = 0; base < total; base += U * kBlock) {
+        chunk_t v[U];
 #pragma unroll
-        for (int i = 0; i < CH; ++i) {
-            const int e = i * kBlock + tid;
-            const int row = e / CH;
-            const int k = e - row * CH;
-            v[i] = make_uint4(0u, 0u, 0u, 0u);
-            if (row < n) {
-                const uint4 *src = nullptr;
-                if (k < DOC_CH) {
+        for (int u = 0; u < U; ++u) {
+            const int e = base + u * kBlock + tid;
+            v[u] = chunk_t{0u, 0u, 0u, 0u};
+            if (e < total) {
+                const int row = e / ch, k = e - (e / ch) * ch;
+                const chunk_t *src = nullptr;
+                if (k < dch) {
                     const int64_t c = s_src[row];
                     if (c >= 0)
-                        src = reinterpret_cast<const uint4 *>(a.doc + c * (DOC_CH * 16)) + k;
+                        src = reinterpret_cast<const chunk_t *>(a.doc + c * dbytes) + k;
                 } else {
-                    const int kk = k - DOC_CH;
-                    const int l = kk / EDGE_CH;
-                    const int q = kk - l * EDGE_CH;
+                    const int kk = k - dch;
+                    const int l = kk / ech;
+                    const int q = kk - l * ech;
                     const int64_t r = s_row[l][row];
                     if (r >= 0)
-                        src = reinterpret_cast<const uint4 *>(a.edge + r * (EDGE_CH * 16)) + q;
+                        src = reinterpret_cast<const chunk_t *>(a.edge + r * ebytes) + q;
                     else if (a.def_row)
-                        src = reinterpret_cast<const uint4 *>(a.def_row) + q;
+                        src = reinterpret_cast<const chunk_t *>(a.def_row) + q;
                 }
                 if (src)
-                    v[i] = *src;
+                    v[u] = *src;
             }
         }
 #pragma unroll
-        for (int i = 0; i < CH; ++i) {
-            const int e = i * kBlock + tid;
-            const int row = e / CH;
-            const int k = e - row * CH;
-            if (row < n)
-                reinterpret_cast<uint4 *>(a.out + (t0 + row) * a.out_stride)[k] = v[i];
-        }
-    } else {
-        const int dch = a.doc_bytes >> 4;
-        const int ech = a.edge_bytes >> 4;
-        const int ch = dch + NL * ech;
-        const int total = n * ch;
-        constexpr int U = 4;
-        for (int base = 0; base < total; base += U * kBlock) {
-            uint4 v[U];
-            int rows[U], ks[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int e = base + u * kBlock + tid;
-                rows[u] = e / ch;
-                ks[u] = e - rows[u] * ch;
-                v[u] = make_uint4(0u, 0u, 0u, 0u);
-                if (e < total) {
-                    const int row = rows[u], k = ks[u];
-                    const uint4 *src = nullptr;
-                    if (k < dch) {
-                        const int64_t c = s_src[row];
-                        if (c >= 0)
-                            src = reinterpret_cast<const uint4 *>(a.doc + c * a.doc_bytes) + k;
-                    } else {
-                        const int kk = k - dch;
-                        const int l = kk / ech;
-                        const int q = kk - l * ech;
-                        const int64_t r = s_row[l][row];
-                        if (r >= 0)
-                            src = reinterpret_cast<const uint4 *>(a.edge + r * a.edge_bytes) + q;
-                        else if (a.def_row)
-                            src = reinterpret_cast<const uint4 *>(a.def_row) + q;
-                    }
-                    if (src)
-                        v[u] = *src;
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int e = base + u * kBlock + tid;
-                if (e < total)
-                    reinterpret_cast<uint4 *>(a.out + (t0 + rows[u]) * a.out_stride)[ks[u]] = v[u];
+        for (int u = 0; u < U; ++u) {
+            const int e = base + u * kBlock + tid;
+            if (e < total) {
+                const int row = e / ch, k = e - (e / ch) * ch;
+                reinterpret_cast<chunk_t *>(a.out + (t0 + row) * a.out_stride)[k] = v[u];
             }
         }
     }
 }
 
+// Process candidates [s0, s1) of one viewer segment (s1 - s0 >= kBlock) in full sub-tiles.
+// Sub-tile k starts at min(s0 + k * kBlock, s1 - kBlock): the last one is moved back to end at
+// s1 and overlaps its predecessor (those rows are rewritten with the same bytes, and `fresh`
+// keeps them out of the invalid count).
+//
+// Software pipeline per thread. Each thread's dependent chain is position -> author id ->
+// search -> row copy. While sub-tile k is searched and copied, the positions of sub-tile k+2
+// are loaded (at the top of iteration k) and the author ids of sub-tile k+1 right after the
+// search of k, ahead of k's copy loads; by the next search they have landed. (Loads retire in
+// issue order, so a load issued just before the copy loads costs the copy nothing.) Prefetch
+// loads are unconditional, from indices clamped into range (a value fetched past the segment or
+// for an invalid position is never used): a load under a branch, or a second path into the
+// loop latch, would leave the compiler unable to count outstanding loads, and it would then
+// wait for every store of a sub-tile before the next one.
 template <int DOC_CH, int EDGE_CH, int NL>
+__device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t *s_src,
+                                           int64_t (*s_row)[kBlock], unsigned int *s_invalid,
+                                           const int64_t *s_tab, int64_t M, int S,
+                                           const int64_t *gk, int64_t K, int64_t kb, int64_t s0,
+                                           int64_t s1, const uint8_t *miss_row) {
+    const int tid = threadIdx.x;
+    const int64_t last_doc = a.n_docs > 0 ? a.n_docs - 1 : 0;
+    const int64_t ntiles = (s1 - s0 + kBlock - 1) / kBlock;
+    auto base = [&](int64_t k) { return min(s0 + k * kBlock, s1 - kBlock); };
+    int64_t c_cur = a.cand_idx[base(0) + tid];
+    int64_t c_nx1 = a.cand_idx[base(1) + tid];
+    int64_t e_cur = 0, e_nx1 = 0;
+    if constexpr (NL == 2) {
+        e_cur = a.extra[base(0) + tid];
+        e_nx1 = a.extra[base(1) + tid];
+    }
+    int64_t x_cur = a.author[clamp64(c_cur, last_doc)];
+    // Let the prologue loads land here (once per segment). Otherwise, where the loop entry and
+    // the back edge meet, the compiler keeps the prologue's short distance to the author-id
+    // load and waits for the previous sub-tile's stores before every search.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    for (int64_t k = 0; k < ntiles; ++k) {
+        const int64_t tb = base(k);
+        const int fresh = (int)(s0 + k * kBlock - tb);
+        const int64_t c_nx2 = a.cand_idx[base(k + 2) + tid];
+        int64_t e_nx2 = 0;
+        if constexpr (NL == 2)
+            e_nx2 = a.extra[base(k + 2) + tid];
+
+        const int64_t j = tb + tid;
+        const bool valid = c_cur >= 0 && c_cur < a.n_docs;
+        s_src[tid] = valid ? c_cur : -1;
+        if (!valid && tid >= fresh)
+            atomicAdd(s_invalid, 1u);
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            int64_t r = -1;
+            if (valid)
+                r = find_key(l == 0 ? x_cur : e_cur, s_tab, M, S, gk, K);
+            s_row[l][tid] = r >= 0 ? kb + r : -1;
+            a.hit[j * NL + l] = (int8_t)(r >= 0 ? 1 : 0);
+        }
+        const int64_t x_nx1 = a.author[clamp64(c_nx1, last_doc)];
+        lds_barrier();
+        copy_full_tile<DOC_CH, EDGE_CH, NL>(a, s_src, s_row, tb, miss_row, [] {});
+        lds_barrier();
+        c_cur = c_nx1;
+        c_nx1 = c_nx2;
+        x_cur = x_nx1;
+        e_cur = e_nx1;
+        e_nx1 = e_nx2;
+    }
+}
+
+// BATCHED selects the CSR form (viewer offsets in device memory); the single-viewer form has
+// one implicit viewer and skips the offset lookups.
+template <int DOC_CH, int EDGE_CH, int NL, bool BATCHED>
 __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
     extern __shared__ int64_t s_tab[];            // fence table, a.lds_keys entries
     __shared__ int64_t s_src[kBlock];             // doc position of each sub-tile row, or -1
@@ -198,8 +319,9 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
         return;
     if (tid == 0)
         s_invalid = 0;
+    const uint8_t *miss_row = a.def_row ? a.def_row : a.zero_row;
 
-    const bool batched = a.cand_offsets != nullptr;
+    constexpr bool batched = BATCHED;
     const int32_t B = batched ? a.n_viewers : 1;
     // First viewer whose candidate range ends after `begin`.
     int32_t v = 0;
@@ -233,11 +355,38 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
         const int64_t *gk = a.keys + kb;
         const int S = choose_stride(K, s1 - s0, a.lds_keys, a.fence_stride);
         const int64_t M = (K + S - 1) / S;
-        __syncthreads();                          // earlier readers of s_tab are done
-        for (int64_t i = tid; i < M; i += kBlock)
-            s_tab[i] = gk[i * S];
-        __syncthreads();
+        lds_barrier();                            // earlier readers of s_tab are done
+        // Stage the fences, 8 loads in flight per thread (indices clamped to M-1; the repeated
+        // writes of the last fence store the same value).
+        for (int64_t i0 = 0; i0 < M; i0 += 8 * kBlock) {
+            int64_t f[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                f[u] = gk[min(i0 + u * kBlock + tid, M - 1) * S];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                s_tab[min(i0 + u * kBlock + tid, M - 1)] = f[u];
+        }
+        lds_barrier();
 
+        // Segments of at least one sub-tile use full sub-tiles only: the last one is moved back
+        // to end at s1 and overlaps its predecessor (those rows are rewritten with the same
+        // bytes; `fresh` keeps them out of the invalid count).
+        //
+        // Two-stage pipeline per thread: while sub-tile t is searched and copied, the candidate
+        // positions of sub-tile t+1 are loaded (issued before the search) and their author ids
+        // (issued once t's copy loads are in flight), so the dependent chain
+        // position -> author id overlaps the previous sub-tile's copy.
+        const int64_t seg = s1 - s0;
+        if constexpr (DOC_CH > 0) {
+            if (seg >= kBlock) {
+                full_tiles<DOC_CH, EDGE_CH, NL>(a, s_src, s_row, &s_invalid, s_tab, M, S, gk, K, kb,
+                                                 s0, s1, miss_row);
+                continue;
+            }
+        }
+        // A segment shorter than a sub-tile (or widths without a specialisation): guarded
+        // sub-tiles, one candidate per thread.
         for (int64_t t0 = s0; t0 < s1; t0 += kBlock) {
             const int n = (int)min<int64_t>(kBlock, s1 - t0);
             if (tid < n) {
@@ -250,43 +399,101 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
 #pragma unroll
                 for (int l = 0; l < NL; ++l) {
                     int64_t r = -1;
-                    if (valid) {
-                        const int64_t x = (l == 0) ? a.author[c] : a.extra[j];
-                        r = find_key(x, s_tab, M, S, gk, K);
-                    }
+                    if (valid)
+                        r = find_key(l == 0 ? a.author[c] : a.extra[j], s_tab, M, S, gk, K);
                     s_row[l][tid] = r >= 0 ? kb + r : -1;
                     a.hit[j * NL + l] = (int8_t)(r >= 0 ? 1 : 0);
                 }
             }
-            __syncthreads();
+            lds_barrier();
             copy_rows<DOC_CH, EDGE_CH, NL>(a, s_src, s_row, t0, n);
-            __syncthreads();
+            lds_barrier();
         }
     }
+    lds_barrier();
     if (tid == 0 && s_invalid)
         atomicAdd(a.invalid_counter, (unsigned long long)s_invalid);
 }
 
-template <int D, int E, int L>
-hipError_t launch_one(const JoinArgs &a, hipStream_t stream) {
-    const size_t lds = (size_t)max(1, a.lds_keys) * sizeof(int64_t);
-    if (lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&join_kernel<D, E, L>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess)
-            return e;
+// Multiprocessor count per device (cached; devices are few).
+int cu_count(int device) {
+    static std::atomic<int> cache[64];
+    if (device >= 0 && device < 64) {
+        int v = cache[device].load(std::memory_order_relaxed);
+        if (v > 0)
+            return v;
     }
-    hipLaunchKernelGGL((join_kernel<D, E, L>), dim3(a.n_wg), dim3(kBlock), lds, stream, a);
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
+        v <= 0)
+        v = 256;
+    if (device >= 0 && device < 64)
+        cache[device].store(v, std::memory_order_relaxed);
+    return v;
+}
+
+// Resident workgroups per CU for one kernel at one dynamic LDS size (registers and LDS both
+// count), cached.
+int resident_per_cu(const void *fn, size_t lds) {
+    static std::mutex mu;
+    static std::map<std::pair<const void *, size_t>, int> cache;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = cache.find({fn, lds});
+    if (it != cache.end())
+        return it->second;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kBlock, lds) != hipSuccess || n < 1)
+        n = 1;
+    cache[{fn, lds}] = n;
+    return n;
+}
+
+template <int D, int E, int L, bool BATCHED>
+hipError_t launch_one(JoinArgs &a, int32_t workgroups, int device, hipStream_t stream) {
+    const void *fn = reinterpret_cast<const void *>(&join_kernel<D, E, L, BATCHED>);
+    const size_t lds = (size_t)max(1, a.lds_keys) * sizeof(int64_t);
+    static std::once_flag lds_limit;
+    hipError_t err = hipSuccess;
+    std::call_once(lds_limit, [&] {
+        err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  kMaxLdsKeys * (int)sizeof(int64_t));
+    });
+    if (err != hipSuccess)
+        return err;
+    // Grid: about 1.5 resident waves of workgroups (a slight oversubscription lets early
+    // finishers take the remaining ranges), each owning a contiguous range of whole
+    // sub-tiles, rounded to a multiple of 8 so that each XCD gets an equal share.
+    const int64_t tiles = (a.total_cand + kBlock - 1) / kBlock;
+    int64_t n_wg = workgroups;
+    if (n_wg <= 0)
+        n_wg = (int64_t)cu_count(device) * resident_per_cu(fn, lds) * 3 / 2;
+    if (n_wg > tiles)
+        n_wg = tiles;
+    if (n_wg < 1)
+        n_wg = 1;
+    const int64_t tiles_per_wg = (tiles + n_wg - 1) / n_wg;
+    a.per_wg = tiles_per_wg * kBlock;
+    n_wg = (a.total_cand + a.per_wg - 1) / a.per_wg;
+    n_wg = (n_wg + 7) & ~int64_t(7);
+    a.n_wg = (int32_t)n_wg;
+    hipLaunchKernelGGL((join_kernel<D, E, L, BATCHED>), dim3(a.n_wg), dim3(kBlock), lds, stream,
+                       a);
     return hipGetLastError();
 }
 
+template <int D, int E, int L>
+hipError_t launch_form(JoinArgs &a, int32_t wgs, int device, hipStream_t stream) {
+    return a.cand_offsets ? launch_one<D, E, L, true>(a, wgs, device, stream)
+                          : launch_one<D, E, L, false>(a, wgs, device, stream);
+}
+
 template <int L>
-hipError_t dispatch_widths(const JoinArgs &a, hipStream_t stream) {
+hipError_t dispatch_widths(JoinArgs &a, int32_t wgs, int device, hipStream_t stream) {
     const int d = a.doc_bytes >> 4, e = a.edge_bytes >> 4;
-    if (d == 4 && e == 2) return launch_one<4, 2, L>(a, stream);
-    if (d == 8 && e == 4) return launch_one<8, 4, L>(a, stream);
-    if (d == 8 && e == 8) return launch_one<8, 8, L>(a, stream);
-    return launch_one<0, 0, L>(a, stream);
+    if (d == 4 && e == 2) return launch_form<4, 2, L>(a, wgs, device, stream);
+    if (d == 8 && e == 4) return launch_form<8, 4, L>(a, wgs, device, stream);
+    if (d == 8 && e == 8) return launch_form<8, 8, L>(a, wgs, device, stream);
+    return launch_form<0, 0, L>(a, wgs, device, stream);
 }
 
 __global__ void validate_keys_kernel(const int64_t *key_offsets, const int64_t *keys,
@@ -305,8 +512,10 @@ __global__ void validate_keys_kernel(const int64_t *key_offsets, const int64_t *
 
 }  // namespace
 
-hipError_t launch_join(const JoinArgs &a, int n_lookups, hipStream_t stream) {
-    return n_lookups == 2 ? dispatch_widths<2>(a, stream) : dispatch_widths<1>(a, stream);
+hipError_t launch_join(JoinArgs &a, int n_lookups, int32_t workgroups, int device,
+                       hipStream_t stream) {
+    return n_lookups == 2 ? dispatch_widths<2>(a, workgroups, device, stream)
+                          : dispatch_widths<1>(a, workgroups, device, stream);
 }
 
 hipError_t launch_validate_keys(const int64_t *key_offsets, const int64_t *keys,

@@ -45,23 +45,94 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=2)
+    ap.add_argument("--all-configs", action="store_true",
+                    help="also time each of the five workload shapes (adds a 'configs' field)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (known bytes) for counter scaling")
     return ap.parse_args()
 
 
 def algorithmic_bytes(torch, st, batch, wd, we, n_lookups=1):
-    """Bytes the method must move for one launch: per candidate its index, author id, doc row,
-    output row and hit byte; per viewer its keys and each distinct edge row that is hit."""
+    """Bytes the method must move for one launch: per candidate its position, author id, doc
+    row, output row, hit bytes and (second lookup) its extra key; per viewer its keys and each
+    distinct edge row that some lookup hits."""
     n = batch.cand_idx.numel()
-    per_cand = 8 + 8 + wd + (wd + n_lookups * we) + n_lookups
+    per_cand = 8 + 8 + wd + (wd + n_lookups * we) + n_lookups + 8 * (n_lookups - 1)
     keys_bytes = batch.keys.numel() * 8
     co, ko = batch.cand_offsets.tolist(), batch.key_offsets.tolist()
     rows = 0
     for v in range(len(co) - 1):
-        a = st.author_id[batch.cand_idx[co[v]:co[v + 1]]]
-        rows += int(torch.isin(torch.unique(a), batch.keys[ko[v]:ko[v + 1]]).sum())
+        q = st.author_id[batch.cand_idx[co[v]:co[v + 1]]]
+        if n_lookups == 2:
+            q = torch.cat([q, batch.actor[co[v]:co[v + 1]]])
+        rows += int(torch.isin(torch.unique(q), batch.keys[ko[v]:ko[v + 1]]).sum())
     return n * per_cand + keys_bytes + rows * we
+
+
+def time_launches(torch, fn, iters, warm=5):
+    """Median and mean per-launch time (ms) of `fn` on the current stream."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(iters)]
+    for a, b in evs:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in evs)
+    return ms[len(ms) // 2], sum(ms) / len(ms)
+
+
+def all_configs(torch, P, W, dev, seed):
+    """Per-launch time and algorithmic bandwidth of each workload shape at full size."""
+    res = {}
+    st10 = None
+    for i in (1, 2, 3, 4, 5):
+        s, r = W.CONFIGS[i]
+        if i == 1:
+            st = W.make_store(s, seed, device=dev)
+        elif i in (2, 3, 4):
+            st10 = st10 or W.make_store(s, seed, device=dev)
+            st = st10
+        else:
+            st10 = None
+            torch.cuda.empty_cache()
+            st = W.make_store(s, seed, device=dev)
+        reqs = W.make_requests(st, r, seed)
+        b = W.pack(reqs)
+        L = 2 if r.actor else 1
+        wd = st.doc_rows.shape[1] * st.doc_rows.element_size()
+        we = r.edge_cols * b.edge_rows.element_size()
+        alg = algorithmic_bytes(torch, st, b, wd, we, L)
+        store = P.cc_store_create(st.author_id, st.doc_rows)
+        if i == 5:
+            st._by_author = None
+            del st
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+        n = b.cand_idx.numel()
+        out = torch.empty(n, wd + L * we, dtype=torch.uint8, device=dev)
+        hit = torch.empty(n, L, dtype=torch.int8, device=dev)
+        if r.n_viewers == 1 and L == 1:
+            fn = lambda: P.cc_join(store, b.cand_idx, b.keys, b.edge_rows, out, hit)
+            entry = "cc_join"
+        else:
+            ex = [b.actor] if L == 2 else None
+            fn = lambda: P.cc_join_batched(store, b.cand_offsets, b.cand_idx, b.key_offsets,
+                                           b.keys, b.edge_rows, out, hit, extra_keys=ex)
+            entry = "cc_join_batched"
+        med, mean = time_launches(torch, fn, 100 if n < 500_000 else 30)
+        P.cc_store_destroy(store)
+        res[str(i)] = {"entry": entry, "viewers": r.n_viewers, "candidates": n,
+                       "keys": b.keys.numel(), "lookups": L, "ms_median": med, "ms_mean": mean,
+                       "candidates_per_s": n / (med / 1e3), "algorithmic_bytes": alg,
+                       "hbm_gbps": alg / (med / 1e3) / 1e9,
+                       "hbm_frac_of_peak": alg / (med / 1e3) / 1e9 / PEAK_GBPS}
+        del out, hit, b, reqs
+        torch.cuda.empty_cache()
+    return res
 
 
 def kernel_hash():
@@ -213,6 +284,11 @@ def main():
         cpu = cpu_baseline((st.author_id.cpu(), st.doc_rows.cpu()), reqs_cpu, args.cpu_seconds)
 
     P.cc_store_destroy(store)
+    configs = None
+    if args.all_configs:
+        del batches, out, hit, st
+        torch.cuda.empty_cache()
+        configs = all_configs(torch, P, W, dev, args.seed)
     line = {
         "metric": METRIC,
         "value": cands_per_s,
@@ -248,6 +324,7 @@ def main():
         },
         "cpu_baseline": cpu,
         "wall_s_timed_region": wall,
+        "configs": configs,
     }
     print(json.dumps(line), flush=True)
 

@@ -181,7 +181,7 @@ CC_API cc_status cc_join_batched(const cc_store *store, int32_t n_viewers,
  *   fence_stride   power of two >= 1: the search keeps every fence_stride-th key of a viewer
  *                  in LDS and finishes with one read of the keys between two fences
  *                  (1 = the whole key list in LDS).
- *   lds_keys       capacity of the LDS key table, in keys (<= 19456, i.e. 152 KiB).
+ *   lds_keys       capacity of the LDS key table, in keys (<= 18432, i.e. 144 KiB).
  *   workgroups     number of workgroups of the launch (<= 2^30; rounded up to a multiple of 8).
  * Results never depend on these values, only speed does.
  */

@@ -8,7 +8,8 @@ namespace ccj {
 
 constexpr int kBlock = 256;          // threads per workgroup = candidates per sub-tile
 constexpr int kWindow = 15;          // keys between two fences read from L2 in one step
-constexpr int kMaxLdsKeys = 19456;   // LDS key table limit (152 KiB of the 160 KiB per CU)
+constexpr int kMaxLdsKeys = 18432;   // LDS key table limit: 144 KiB + at most 12 KiB of static
+                                     // tables stays within the 160 KiB a workgroup may use
 constexpr int kDefaultLdsKeys = 8192;   // 64 KiB: within the register-limited occupancy
 constexpr int kZeroRowBytes = 1024;    // >= the widest row of a compile-time specialisation
 

@@ -234,72 +234,112 @@ __device__ __forceinline__ void copy_rows(const JoinArgs &a, const int64_t *s_sr
     }
 }
 
+// Copy the fences f[i] = gk[i * S], i < M, into LDS, 16 loads in flight per thread (indices
+// clamped to M - 1; the repeated writes of the last fence store the same value).
+__device__ __forceinline__ void stage_fences(int64_t *s_tab, const int64_t *gk, int64_t M, int S) {
+    const int tid = threadIdx.x;
+    constexpr int U = 16;
+    for (int64_t i0 = 0; i0 < M; i0 += U * kBlock) {
+        int64_t f[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            f[u] = gk[min(i0 + u * kBlock + tid, M - 1) * S];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            s_tab[min(i0 + u * kBlock + tid, M - 1)] = f[u];
+    }
+}
+
+// Resolve one sub-tile starting at tb: per thread, the candidate's position check and search(es).
+// Writes the doc position (or -1) to src[tid] and the global edge row per lookup (or -1) to
+// row[l][tid], stores the hit bytes, and counts invalid positions of rows tid >= fresh.
+template <int NL>
+__device__ __forceinline__ void resolve_tile(const JoinArgs &a, int64_t *src,
+                                             int64_t (*row)[kBlock], unsigned int *s_invalid,
+                                             const int64_t *s_tab, int64_t M, int S,
+                                             const int64_t *gk, int64_t K, int64_t kb, int64_t tb,
+                                             int fresh, int64_t c, int64_t x0, int64_t x1) {
+    const int tid = threadIdx.x;
+    const int64_t j = tb + tid;
+    const bool valid = c >= 0 && c < a.n_docs;
+    src[tid] = valid ? c : -1;
+    if (!valid && tid >= fresh)
+        atomicAdd(s_invalid, 1u);
+#pragma unroll
+    for (int l = 0; l < NL; ++l) {
+        int64_t r = -1;
+        if (valid)
+            r = find_key(l == 0 ? x0 : x1, s_tab, M, S, gk, K);
+        row[l][tid] = r >= 0 ? kb + r : -1;
+        a.hit[j * NL + l] = (int8_t)(r >= 0 ? 1 : 0);
+    }
+}
+
 // Process candidates [s0, s1) of one viewer segment (s1 - s0 >= kBlock) in full sub-tiles.
-// Sub-tile k starts at min(s0 + k * kBlock, s1 - kBlock): the last one is moved back to end at
-// s1 and overlaps its predecessor (those rows are rewritten with the same bytes, and `fresh`
-// keeps them out of the invalid count).
+// Sub-tile k starts at base(k) = min(s0 + k * kBlock, s1 - kBlock): the last one is moved back
+// to end at s1 and overlaps its predecessor (those rows are rewritten with the same bytes, and
+// `fresh` keeps them out of the invalid count).
 //
-// Software pipeline per thread. Each thread's dependent chain is position -> author id ->
-// search -> row copy. While sub-tile k is searched and copied, the positions of sub-tile k+2
-// are loaded (at the top of iteration k) and the author ids of sub-tile k+1 right after the
-// search of k, ahead of k's copy loads; by the next search they have landed. (Loads retire in
-// issue order, so a load issued just before the copy loads costs the copy nothing.) Prefetch
-// loads are unconditional, from indices clamped into range (a value fetched past the segment or
-// for an invalid position is never used): a load under a branch, or a second path into the
-// loop latch, would leave the compiler unable to count outstanding loads, and it would then
-// wait for every store of a sub-tile before the next one.
-template <int DOC_CH, int EDGE_CH, int NL>
-__device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t *s_src,
-                                           int64_t (*s_row)[kBlock], unsigned int *s_invalid,
-                                           const int64_t *s_tab, int64_t M, int S,
-                                           const int64_t *gk, int64_t K, int64_t kb, int64_t s0,
-                                           int64_t s1, const uint8_t *miss_row) {
+// Software pipeline. A thread's dependent chain per candidate is position -> author id ->
+// search -> row copy. Iteration k issues sub-tile k's copy loads, then searches sub-tile k+1
+// into the other half of the double-buffered LDS tables, then issues the loads for later
+// sub-tiles (positions of k+3, author ids of k+2), then stores sub-tile k. Vector-memory
+// completions are counted in issue order, so a search's key-window loads, issued after the
+// copy loads, never wait for stores younger than the previous iteration's. The last iteration
+// searches its own sub-tile once more (identical hit bytes; `fresh` = kBlock counts nothing)
+// so that the loop body has no branch. All loads are unconditional from clamped indices: a
+// load under a branch, or a second path into the loop latch, would leave the compiler unable
+// to count outstanding loads, and it would then wait for every store of a sub-tile first.
+template <int DOC_CH, int EDGE_CH, int NL, typename Stage>
+__device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t (*s_src)[kBlock],
+                                           int64_t (*s_row)[NL][kBlock],
+                                           unsigned int *s_invalid, const int64_t *s_tab,
+                                           int64_t M, int S, const int64_t *gk, int64_t K,
+                                           int64_t kb, int64_t s0, int64_t s1,
+                                           const uint8_t *miss_row, Stage stage) {
     const int tid = threadIdx.x;
     const int64_t last_doc = a.n_docs > 0 ? a.n_docs - 1 : 0;
     const int64_t ntiles = (s1 - s0 + kBlock - 1) / kBlock;
     auto base = [&](int64_t k) { return min(s0 + k * kBlock, s1 - kBlock); };
-    int64_t c_cur = a.cand_idx[base(0) + tid];
-    int64_t c_nx1 = a.cand_idx[base(1) + tid];
-    int64_t e_cur = 0, e_nx1 = 0;
-    if constexpr (NL == 2) {
-        e_cur = a.extra[base(0) + tid];
-        e_nx1 = a.extra[base(1) + tid];
-    }
-    int64_t x_cur = a.author[clamp64(c_cur, last_doc)];
-    // Let the prologue loads land here (once per segment). Otherwise, where the loop entry and
-    // the back edge meet, the compiler keeps the prologue's short distance to the author-id
-    // load and waits for the previous sub-tile's stores before every search.
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-    for (int64_t k = 0; k < ntiles; ++k) {
-        const int64_t tb = base(k);
-        const int fresh = (int)(s0 + k * kBlock - tb);
-        const int64_t c_nx2 = a.cand_idx[base(k + 2) + tid];
-        int64_t e_nx2 = 0;
+    auto fresh = [&](int64_t k) { return (int)min<int64_t>(s0 + k * kBlock - base(k), kBlock); };
+    auto extra = [&](int64_t k) -> int64_t {
         if constexpr (NL == 2)
-            e_nx2 = a.extra[base(k + 2) + tid];
-
-        const int64_t j = tb + tid;
-        const bool valid = c_cur >= 0 && c_cur < a.n_docs;
-        s_src[tid] = valid ? c_cur : -1;
-        if (!valid && tid >= fresh)
-            atomicAdd(s_invalid, 1u);
-#pragma unroll
-        for (int l = 0; l < NL; ++l) {
-            int64_t r = -1;
-            if (valid)
-                r = find_key(l == 0 ? x_cur : e_cur, s_tab, M, S, gk, K);
-            s_row[l][tid] = r >= 0 ? kb + r : -1;
-            a.hit[j * NL + l] = (int8_t)(r >= 0 ? 1 : 0);
-        }
-        const int64_t x_nx1 = a.author[clamp64(c_nx1, last_doc)];
+            return a.extra[base(k) + tid];
+        return 0;
+    };
+    int64_t c1 = a.cand_idx[base(1) + tid];
+    int64_t c2 = a.cand_idx[base(2) + tid];
+    int64_t e1 = extra(1);
+    int64_t x1;
+    {
+        const int64_t c0 = a.cand_idx[base(0) + tid];
+        const int64_t e0 = extra(0);
+        const int64_t x0 = a.author[clamp64(c0, last_doc)];
+        x1 = a.author[clamp64(c1, last_doc)];
+        stage();
+        resolve_tile<NL>(a, s_src[0], s_row[0], s_invalid, s_tab, M, S, gk, K, kb, base(0),
+                         fresh(0), c0, x0, e0);
+    }
+    // Let the prologue loads land here (once per segment). Otherwise, where the loop entry and
+    // the back edge meet, the compiler keeps the prologue's short distances and waits for the
+    // previous sub-tile's stores before every search.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    lds_barrier();
+    for (int64_t k = 0; k < ntiles; ++k) {
+        const int p = (int)(k & 1);
+        copy_full_tile<DOC_CH, EDGE_CH, NL>(
+            a, s_src[p], s_row[p], base(k), miss_row, [&]() {
+                resolve_tile<NL>(a, s_src[p ^ 1], s_row[p ^ 1], s_invalid, s_tab, M, S, gk, K,
+                                 kb, base(k + 1), fresh(k + 1), c1, x1, e1);
+                const int64_t c3 = a.cand_idx[base(k + 3) + tid];
+                const int64_t e2 = extra(k + 2);
+                const int64_t x2 = a.author[clamp64(c2, last_doc)];
+                c1 = c2;
+                c2 = c3;
+                x1 = x2;
+                e1 = e2;
+            });
         lds_barrier();
-        copy_full_tile<DOC_CH, EDGE_CH, NL>(a, s_src, s_row, tb, miss_row, [] {});
-        lds_barrier();
-        c_cur = c_nx1;
-        c_nx1 = c_nx2;
-        x_cur = x_nx1;
-        e_cur = e_nx1;
-        e_nx1 = e_nx2;
     }
 }
 
@@ -308,8 +348,9 @@ __device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t *s_src,
 template <int DOC_CH, int EDGE_CH, int NL, bool BATCHED>
 __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
     extern __shared__ int64_t s_tab[];            // fence table, a.lds_keys entries
-    __shared__ int64_t s_src[kBlock];             // doc position of each sub-tile row, or -1
-    __shared__ int64_t s_row[NL][kBlock];         // global edge row per lookup, or -1
+    __shared__ int64_t s_src[2][kBlock];          // doc position of each sub-tile row, or -1
+    __shared__ int64_t s_row[2][NL][kBlock];      // global edge row per lookup, or -1
+                                                  // (two buffers: sub-tiles k and k+1)
     __shared__ unsigned int s_invalid;
 
     const int tid = threadIdx.x;
@@ -355,58 +396,36 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
         const int64_t *gk = a.keys + kb;
         const int S = choose_stride(K, s1 - s0, a.lds_keys, a.fence_stride);
         const int64_t M = (K + S - 1) / S;
-        lds_barrier();                            // earlier readers of s_tab are done
-        // Stage the fences, 8 loads in flight per thread (indices clamped to M-1; the repeated
-        // writes of the last fence store the same value).
-        for (int64_t i0 = 0; i0 < M; i0 += 8 * kBlock) {
-            int64_t f[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                f[u] = gk[min(i0 + u * kBlock + tid, M - 1) * S];
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                s_tab[min(i0 + u * kBlock + tid, M - 1)] = f[u];
-        }
-        lds_barrier();
-
-        // Segments of at least one sub-tile use full sub-tiles only: the last one is moved back
-        // to end at s1 and overlaps its predecessor (those rows are rewritten with the same
-        // bytes; `fresh` keeps them out of the invalid count).
-        //
-        // Two-stage pipeline per thread: while sub-tile t is searched and copied, the candidate
-        // positions of sub-tile t+1 are loaded (issued before the search) and their author ids
-        // (issued once t's copy loads are in flight), so the dependent chain
-        // position -> author id overlaps the previous sub-tile's copy.
+        // Stage the fences into LDS (after the previous segment's readers are done). Full
+        // segments stage after issuing their first loads, so the two latencies overlap.
+        auto stage = [&]() {
+            lds_barrier();
+            stage_fences(s_tab, gk, M, S);
+            lds_barrier();
+        };
         const int64_t seg = s1 - s0;
         if constexpr (DOC_CH > 0) {
             if (seg >= kBlock) {
-                full_tiles<DOC_CH, EDGE_CH, NL>(a, s_src, s_row, &s_invalid, s_tab, M, S, gk, K, kb,
-                                                 s0, s1, miss_row);
+                full_tiles<DOC_CH, EDGE_CH, NL>(a, s_src, s_row, &s_invalid, s_tab, M, S, gk, K,
+                                                kb, s0, s1, miss_row, stage);
                 continue;
             }
         }
         // A segment shorter than a sub-tile (or widths without a specialisation): guarded
         // sub-tiles, one candidate per thread.
+        stage();
         for (int64_t t0 = s0; t0 < s1; t0 += kBlock) {
             const int n = (int)min<int64_t>(kBlock, s1 - t0);
             if (tid < n) {
-                const int64_t j = t0 + tid;
-                const int64_t c = a.cand_idx[j];
-                const bool valid = c >= 0 && c < a.n_docs;
-                s_src[tid] = valid ? c : -1;
-                if (!valid)
-                    atomicAdd(&s_invalid, 1u);
-#pragma unroll
-                for (int l = 0; l < NL; ++l) {
-                    int64_t r = -1;
-                    if (valid)
-                        r = find_key(l == 0 ? a.author[c] : a.extra[j], s_tab, M, S, gk, K);
-                    s_row[l][tid] = r >= 0 ? kb + r : -1;
-                    a.hit[j * NL + l] = (int8_t)(r >= 0 ? 1 : 0);
-                }
+                const int64_t c = a.cand_idx[t0 + tid];
+                const bool ok = c >= 0 && c < a.n_docs;
+                const int64_t x0 = ok ? a.author[c] : 0;
+                const int64_t x1 = NL == 2 ? a.extra[t0 + tid] : 0;
+                resolve_tile<NL>(a, s_src[0], s_row[0], &s_invalid, s_tab, M, S, gk, K, kb, t0, 0,
+                                 c, x0, x1);
             }
             lds_barrier();
-            copy_rows<DOC_CH, EDGE_CH, NL>(a, s_src, s_row, t0, n);
+            copy_rows<DOC_CH, EDGE_CH, NL>(a, s_src[0], s_row[0], t0, n);
             lds_barrier();
         }
     }
@@ -450,6 +469,10 @@ int resident_per_cu(const void *fn, size_t lds) {
 
 template <int D, int E, int L, bool BATCHED>
 hipError_t launch_one(JoinArgs &a, int32_t workgroups, int device, hipStream_t stream) {
+    // The largest LDS table plus the kernel's static tables must fit a workgroup's 160 KiB.
+    static_assert(kMaxLdsKeys * sizeof(int64_t) + (2 + 2 * L) * kBlock * sizeof(int64_t) +
+                          sizeof(unsigned int) <= 160 * 1024,
+                  "LDS budget exceeded");
     const void *fn = reinterpret_cast<const void *>(&join_kernel<D, E, L, BATCHED>);
     const size_t lds = (size_t)max(1, a.lds_keys) * sizeof(int64_t);
     static std::once_flag lds_limit;

@@ -90,7 +90,7 @@ def _scaled_store(seed, cfg=2, **kw):
     return st, r
 
 
-@pytest.mark.parametrize("k", [1, 2, 15, 16, 17, 511, 512, 513, 4095, 4096, 4097, 8192, 8193,
+@pytest.mark.parametrize("k", [1, 2, 15, 16, 17, 511, 512, 513, 4095, 4096, 4097, 8192, 8193, 18432, 18433,
                                19456, 19457, 40000, 100_000])
 def test_key_count_thresholds(k):
     """K around every table-size and stride boundary, automatic tuning, two lookups."""
@@ -102,7 +102,7 @@ def test_key_count_thresholds(k):
     store = P.cc_store_create(st.author_id, st.doc_rows)
     try:
         wd, we = row_bytes(st.doc_rows), row_bytes(b.edge_rows)
-        for t in (None, (1, 19456, 0), (8, 0, 0)):
+        for t in (None, (1, 18432, 0), (8, 0, 0)):
             got = gpu_join(store, None, b, wd, we, 2, tuning=_tuning(t))
             want = oracle_join(st.author_id.cpu(), st.doc_rows.cpu(), b.to("cpu"), 2)
             assert_same(got, want, f"K={k} tuning {t}")

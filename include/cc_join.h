@@ -177,6 +177,35 @@ CC_API cc_status cc_join_batched(const cc_store *store, int32_t n_viewers,
                           hipStream_t stream);
 
 /*
+ * cc_join_batched_padded -- cc_join_batched writing the padded batch layout of §6.3 (batching
+ * and padding for variable-length requests, where requests with n_v candidates are scattered
+ * into one [B, n_max, features] tensor and padded slots are masked downstream).
+ *
+ * Viewer v's candidate i (i < min(n_v, n_max)) is written to row v * n_max + i of `out` and
+ * `hit_mask`; every other slot (a pad slot) gets zero bytes over the row width
+ * (doc_row_bytes + n_lookups * edge_row_bytes) and hit bits 0. valid_mask[v * n_max + i] is 1
+ * for a candidate's slot and 0 for a pad slot. A viewer with more than n_max candidates keeps
+ * its first n_max; the others produce no output and are not counted as invalid.
+ *
+ *   n_max          slots per viewer (>= 1 when n_viewers > 0).
+ *   out            [n_viewers][n_max][out_row_stride]
+ *   hit_mask       [n_viewers][n_max][n_lookups] int8
+ *   valid_mask     [n_viewers][n_max] int8
+ * Other arguments, alignment rules and errors as in cc_join_batched.
+ */
+CC_API cc_status cc_join_batched_padded(const cc_store *store, int32_t n_viewers,
+                                        const int64_t *cand_offsets, const int64_t *cand_idx,
+                                        int64_t total_cand,
+                                        const int64_t *key_offsets, const int64_t *edge_keys,
+                                        int64_t total_keys,
+                                        const void *edge_feats, int32_t edge_row_bytes,
+                                        const void *default_row,
+                                        int32_t n_lookups, const int64_t *const *extra_keys,
+                                        int64_t n_max, void *out, int64_t out_row_stride,
+                                        int8_t *hit_mask, int8_t *valid_mask,
+                                        hipStream_t stream);
+
+/*
  * Launch tuning for cc_join_batched_tuned. A zero field means "choose automatically".
  *   fence_stride   power of two >= 1: the search keeps every fence_stride-th key of a viewer
  *                  in LDS and finishes with one read of the keys between two fences

@@ -140,6 +140,49 @@ def join(author_id, doc_rows, cand_offsets, cand_idx, key_offsets, keys, edge_ro
     return out, hit, int(inv)
 
 
+def pad_scatter(rows, hit, cand_offsets, n_max: int):
+    """Padded batch layout of §6.3 (batching and padding for variable-length requests).
+
+    Step 1 computes the scatter indices (batch_idx, pos_idx) of every valid row, step 2 is the
+    flattened gather (here: the CSR rows the join produced, in order), step 3 scatters them into
+    T[b, n_max, ...]. Pad slots keep zero bytes, hit 0 and valid 0. A request longer than n_max
+    keeps its first n_max rows.
+    """
+    co = _i64(cand_offsets)
+    b = co.shape[0] - 1
+    n = np.minimum(co[1:] - co[:-1], n_max)
+    batch_idx = np.repeat(np.arange(b), n)
+    pos_idx = np.concatenate([np.arange(k) for k in n]) if b else np.zeros(0, np.int64)
+    src = np.concatenate([co[v] + np.arange(n[v]) for v in range(b)]) if b else pos_idx
+    T = np.zeros((b, n_max) + rows.shape[1:], dtype=rows.dtype)
+    H = np.zeros((b, n_max) + hit.shape[1:], dtype=hit.dtype)
+    valid = np.zeros((b, n_max), dtype=np.int8)
+    T[batch_idx, pos_idx] = rows[src]
+    H[batch_idx, pos_idx] = hit[src]
+    valid[batch_idx, pos_idx] = 1
+    return T, H, valid
+
+
+def join_padded(author_id, doc_rows, cand_offsets, cand_idx, key_offsets, keys, edge_rows,
+                n_max: int, **kw):
+    """The join in the padded batch layout: (T uint8 [B, n_max, stride], hit, valid, invalid)."""
+    co = _i64(cand_offsets)
+    # Candidates beyond n_max in a request are dropped before the join (they produce no row).
+    n = np.minimum(co[1:] - co[:-1], n_max)
+    keep = np.concatenate([co[v] + np.arange(n[v]) for v in range(len(n))]) if len(n) else \
+        np.zeros(0, np.int64)
+    co_kept = np.zeros(len(n) + 1, np.int64)
+    co_kept[1:] = np.cumsum(n)
+    ci = _i64(cand_idx)[keep]
+    extra = kw.pop("extra_keys", None)
+    if extra is not None:
+        extra = [_i64(e)[keep] for e in extra]
+    out, hit, inv = join(author_id, doc_rows, co_kept, ci, key_offsets, keys, edge_rows,
+                         extra_keys=extra, **kw)
+    T, H, valid = pad_scatter(out, hit, co_kept, n_max)
+    return T, H, valid, inv
+
+
 def join_single(author_id, doc_rows, cand_idx, keys, edge_rows, **kw):
     """One viewer: the batched form with offsets [0, N] and [0, K]."""
     n = len(cand_idx)

@@ -16,6 +16,7 @@ LIB_PATH = Path(__file__).resolve().with_name("libccjoin.so")
 EXPORTS = (
     "cc_store_create", "cc_store_destroy", "cc_store_info", "cc_store_invalid_count",
     "cc_store_reset_invalid_count", "cc_join", "cc_join_batched", "cc_join_batched_tuned",
+    "cc_join_batched_padded",
     "cc_validate_keys", "cc_status_string", "cc_last_device_error",
 )
 
@@ -63,6 +64,8 @@ def lib():
             "cc_join_batched_tuned": [vp, i32, vp, vp, i64, vp, vp, i64, vp, i32, vp, i32,
                                       ctypes.POINTER(vp), vp, i64, vp, ctypes.POINTER(Tuning),
                                       vp],
+            "cc_join_batched_padded": [vp, i32, vp, vp, i64, vp, vp, i64, vp, i32, vp, i32,
+                                       ctypes.POINTER(vp), i64, vp, i64, vp, vp, vp],
             "cc_validate_keys": [vp, vp, i32, i64, P64, vp],
             "cc_status_string": [st],
             "cc_last_device_error": [],
@@ -179,6 +182,27 @@ def cc_join_batched(store: int, cand_offsets, cand_idx, key_offsets, edge_keys, 
     else:
         _check(lib().cc_join_batched_tuned(*args, ctypes.byref(tuning), _stream(stream)),
                "cc_join_batched_tuned")
+
+
+def cc_join_batched_padded(store: int, cand_offsets, cand_idx, key_offsets, edge_keys,
+                           edge_feats, n_max: int, out, hit_mask, valid_mask, default_row=None,
+                           extra_keys: Optional[Sequence] = None,
+                           total_cand: Optional[int] = None, total_keys: Optional[int] = None,
+                           stream=None) -> None:
+    """B viewers written into the padded [B, n_max] layout (see include/cc_join.h)."""
+    n_lookups = 1 + (len(extra_keys) if extra_keys else 0)
+    ex = None
+    if extra_keys:
+        ex = (ctypes.c_void_p * len(extra_keys))(*[_ptr(e) for e in extra_keys])
+    ew = int(_prod(edge_feats.shape[1:])) * edge_feats.element_size()
+    tc = cand_idx.numel() if total_cand is None else total_cand
+    tk = edge_keys.numel() if total_keys is None else total_keys
+    stride = out.stride(-2) * out.element_size() if out.dim() == 3 else _out_stride(out)
+    _check(lib().cc_join_batched_padded(
+        store, cand_offsets.numel() - 1, _ptr(cand_offsets), _ptr(cand_idx), tc,
+        _ptr(key_offsets), _ptr(edge_keys), tk, _ptr(edge_feats), ew, _ptr(default_row),
+        n_lookups, ex, n_max, _ptr(out), stride, _ptr(hit_mask), _ptr(valid_mask),
+        _stream(stream)), "cc_join_batched_padded")
 
 
 def cc_validate_keys(key_offsets, edge_keys, total_keys: Optional[int] = None, stream=None):

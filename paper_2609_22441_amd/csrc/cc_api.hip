@@ -60,7 +60,9 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
                     const int64_t *edge_keys, int64_t total_keys, const void *edge_feats,
                     int32_t edge_row_bytes, const void *default_row, int32_t n_lookups,
                     const int64_t *extra, void *out, int64_t out_row_stride, int8_t *hit_mask,
-                    const cc_tuning *tuning, hipStream_t stream) {
+                    int64_t n_max, int8_t *valid_mask, const cc_tuning *tuning,
+                    hipStream_t stream) {
+    // n_max > 0 selects the padded layout (n_viewers * n_max output slots); 0 the CSR layout.
     // ---- host-side validation; nothing touches the device before it passes ----
     if (!store || n_viewers < 0 || total_cand < 0 || total_keys < 0)
         return CC_ERR_INVALID_ARGUMENT;
@@ -75,6 +77,17 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
     if (!mul_ok(total_cand, out_row_stride, &bytes) || !mul_ok(total_keys, edge_row_bytes, &bytes) ||
         !mul_ok(total_cand, n_lookups, &bytes))
         return CC_ERR_INVALID_ARGUMENT;
+    const bool padded = n_max > 0;
+    int64_t slots = 0;
+    if (n_max < 0)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (padded) {
+        if (!mul_ok(n_viewers, n_max, &slots) || !mul_ok(slots, out_row_stride, &bytes) ||
+            !mul_ok(slots, n_lookups, &bytes))
+            return CC_ERR_INVALID_ARGUMENT;
+        if (slots > 0 && (!out || !hit_mask || !valid_mask || !cand_offsets))
+            return CC_ERR_INVALID_ARGUMENT;
+    }
     if (n_viewers > 0 && cand_offsets == nullptr && key_offsets == nullptr) {
         // single-viewer form (cc_join): offsets are implicit
     } else if (n_viewers > 0 && (!cand_offsets || !key_offsets)) {
@@ -102,7 +115,7 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
         stride = tuning->fence_stride;
         wgs = tuning->workgroups;
     }
-    if (total_cand == 0)
+    if (total_cand == 0 && slots == 0)
         return CC_OK;
 
     DeviceGuard guard(store->device);
@@ -128,13 +141,18 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
     a.out = static_cast<uint8_t *>(out);
     a.out_stride = out_row_stride;
     a.hit = hit_mask;
+    a.n_max = n_max;
     a.invalid_counter = store->d_invalid;
     a.n_viewers = cand_offsets ? n_viewers : 1;
     a.fence_stride = stride;
     // The LDS table never needs more entries than the largest viewer has keys.
     a.lds_keys = (int32_t)(total_keys < lds_cap ? (total_keys > 0 ? total_keys : 1) : lds_cap);
 
-    hipError_t e = ccj::launch_join(a, n_lookups, wgs, store->device, stream);
+    hipError_t e = hipSuccess;
+    if (total_cand > 0)
+        e = ccj::launch_join(a, n_lookups, wgs, store->device, stream);
+    if (e == hipSuccess && padded)
+        e = ccj::launch_pad_fill(a, n_lookups, valid_mask, stream);
     if (e != hipSuccess)
         return device_error(e);
     return CC_OK;
@@ -263,8 +281,8 @@ cc_status cc_join(const cc_store *store, const int64_t *cand_idx, int64_t n_cand
                   int32_t edge_row_bytes, const void *default_row, void *out,
                   int64_t out_row_stride, int8_t *hit_mask, hipStream_t stream) {
     return join_impl(store, 1, nullptr, cand_idx, n_cand, nullptr, edge_keys, n_keys, edge_feats,
-                     edge_row_bytes, default_row, 1, nullptr, out, out_row_stride, hit_mask,
-                     nullptr, stream);
+                     edge_row_bytes, default_row, 1, nullptr, out, out_row_stride, hit_mask, 0,
+                     nullptr, nullptr, stream);
 }
 
 cc_status cc_join_batched_tuned(const cc_store *store, int32_t n_viewers,
@@ -283,7 +301,30 @@ cc_status cc_join_batched_tuned(const cc_store *store, int32_t n_viewers,
     const int64_t *extra = (n_lookups == 2) ? extra_keys[0] : nullptr;
     return join_impl(store, n_viewers, cand_offsets, cand_idx, total_cand, key_offsets,
                      edge_keys, total_keys, edge_feats, edge_row_bytes, default_row, n_lookups,
-                     extra, out, out_row_stride, hit_mask, tuning, stream);
+                     extra, out, out_row_stride, hit_mask, 0, nullptr, tuning, stream);
+}
+
+cc_status cc_join_batched_padded(const cc_store *store, int32_t n_viewers,
+                                 const int64_t *cand_offsets, const int64_t *cand_idx,
+                                 int64_t total_cand, const int64_t *key_offsets,
+                                 const int64_t *edge_keys, int64_t total_keys,
+                                 const void *edge_feats, int32_t edge_row_bytes,
+                                 const void *default_row, int32_t n_lookups,
+                                 const int64_t *const *extra_keys, int64_t n_max, void *out,
+                                 int64_t out_row_stride, int8_t *hit_mask, int8_t *valid_mask,
+                                 hipStream_t stream) {
+    if (n_viewers > 0 && (!cand_offsets || !key_offsets || n_max < 1))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_lookups == 2 && !extra_keys)
+        return CC_ERR_INVALID_ARGUMENT;
+    const int64_t *extra = (n_lookups == 2) ? extra_keys[0] : nullptr;
+    if (n_viewers == 0)
+        return join_impl(store, 0, cand_offsets, cand_idx, total_cand, key_offsets, edge_keys,
+                         total_keys, edge_feats, edge_row_bytes, default_row, n_lookups, extra,
+                         out, out_row_stride, hit_mask, 0, nullptr, nullptr, stream);
+    return join_impl(store, n_viewers, cand_offsets, cand_idx, total_cand, key_offsets,
+                     edge_keys, total_keys, edge_feats, edge_row_bytes, default_row, n_lookups,
+                     extra, out, out_row_stride, hit_mask, n_max, valid_mask, nullptr, stream);
 }
 
 cc_status cc_join_batched(const cc_store *store, int32_t n_viewers, const int64_t *cand_offsets,

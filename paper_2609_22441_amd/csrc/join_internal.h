@@ -32,6 +32,7 @@ struct JoinArgs {
     uint8_t *out;
     int64_t out_stride;
     int8_t *hit;
+    int64_t n_max;               // > 0: padded layout, n_max output rows per viewer
     unsigned long long *invalid_counter;
     int32_t n_viewers;
     int32_t lds_keys;            // capacity of the dynamic LDS key table
@@ -45,6 +46,11 @@ struct JoinArgs {
 // error of the launch.
 hipError_t launch_join(JoinArgs &args, int n_lookups, int32_t workgroups, int device,
                        hipStream_t stream);
+
+// Enqueue the pad fill of the padded layout: valid mask of every slot, zero rows and hit bits
+// for pad slots.
+hipError_t launch_pad_fill(const JoinArgs &args, int n_lookups, int8_t *valid_mask,
+                           hipStream_t stream);
 
 // Enqueue the key-order check; *first_bad (device) must hold UINT64_MAX beforehand.
 hipError_t launch_validate_keys(const int64_t *key_offsets, const int64_t *keys,

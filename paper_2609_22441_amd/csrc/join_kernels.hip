@@ -250,17 +250,19 @@ __device__ __forceinline__ void stage_fences(int64_t *s_tab, const int64_t *gk, 
     }
 }
 
-// Resolve one sub-tile starting at tb: per thread, the candidate's position check and search(es).
-// Writes the doc position (or -1) to src[tid] and the global edge row per lookup (or -1) to
-// row[l][tid], stores the hit bytes, and counts invalid positions of rows tid >= fresh.
+// Resolve one sub-tile starting at candidate tb: per thread, the candidate's position check and
+// search(es). Writes the doc position (or -1) to src[tid] and the global edge row per lookup (or
+// -1) to row[l][tid], stores the hit bytes (output row = candidate + shift), and counts invalid
+// positions of rows tid >= fresh.
 template <int NL>
 __device__ __forceinline__ void resolve_tile(const JoinArgs &a, int64_t *src,
                                              int64_t (*row)[kBlock], unsigned int *s_invalid,
                                              const int64_t *s_tab, int64_t M, int S,
                                              const int64_t *gk, int64_t K, int64_t kb, int64_t tb,
-                                             int fresh, int64_t c, int64_t x0, int64_t x1) {
+                                             int64_t shift, int fresh, int64_t c, int64_t x0,
+                                             int64_t x1) {
     const int tid = threadIdx.x;
-    const int64_t j = tb + tid;
+    const int64_t j = tb + tid + shift;
     const bool valid = c >= 0 && c < a.n_docs;
     src[tid] = valid ? c : -1;
     if (!valid && tid >= fresh)
@@ -295,7 +297,7 @@ __device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t (*s_src)[k
                                            int64_t (*s_row)[NL][kBlock],
                                            unsigned int *s_invalid, const int64_t *s_tab,
                                            int64_t M, int S, const int64_t *gk, int64_t K,
-                                           int64_t kb, int64_t s0, int64_t s1,
+                                           int64_t kb, int64_t s0, int64_t s1, int64_t shift,
                                            const uint8_t *miss_row, Stage stage) {
     const int tid = threadIdx.x;
     const int64_t last_doc = a.n_docs > 0 ? a.n_docs - 1 : 0;
@@ -318,7 +320,7 @@ __device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t (*s_src)[k
         x1 = a.author[clamp64(c1, last_doc)];
         stage();
         resolve_tile<NL>(a, s_src[0], s_row[0], s_invalid, s_tab, M, S, gk, K, kb, base(0),
-                         fresh(0), c0, x0, e0);
+                         shift, fresh(0), c0, x0, e0);
     }
     // Let the prologue loads land here (once per segment). Otherwise, where the loop entry and
     // the back edge meet, the compiler keeps the prologue's short distances and waits for the
@@ -328,9 +330,9 @@ __device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t (*s_src)[k
     for (int64_t k = 0; k < ntiles; ++k) {
         const int p = (int)(k & 1);
         copy_full_tile<DOC_CH, EDGE_CH, NL>(
-            a, s_src[p], s_row[p], base(k), miss_row, [&]() {
+            a, s_src[p], s_row[p], base(k) + shift, miss_row, [&]() {
                 resolve_tile<NL>(a, s_src[p ^ 1], s_row[p ^ 1], s_invalid, s_tab, M, S, gk, K,
-                                 kb, base(k + 1), fresh(k + 1), c1, x1, e1);
+                                 kb, base(k + 1), shift, fresh(k + 1), c1, x1, e1);
                 const int64_t c3 = a.cand_idx[base(k + 3) + tid];
                 const int64_t e2 = extra(k + 2);
                 const int64_t x2 = a.author[clamp64(c2, last_doc)];
@@ -380,11 +382,16 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
 
     for (; v < B && begin < end; ++v) {
         int64_t vb = 0, ve = a.total_cand, kb = 0, ke = a.total_keys;
+        int64_t shift = 0;                        // output row = candidate index + shift
         if (batched) {
             vb = clamp64(a.cand_offsets[v], a.total_cand);
             ve = clamp64(a.cand_offsets[v + 1], a.total_cand);
             kb = clamp64(a.key_offsets[v], a.total_keys);
             ke = max(kb, clamp64(a.key_offsets[v + 1], a.total_keys));
+            if (a.n_max > 0) {                    // padded layout: first n_max candidates
+                ve = min(ve, vb + a.n_max);
+                shift = (int64_t)v * a.n_max - vb;
+            }
         }
         const int64_t s0 = max(begin, vb);
         const int64_t s1 = min(end, ve);
@@ -407,7 +414,7 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
         if constexpr (DOC_CH > 0) {
             if (seg >= kBlock) {
                 full_tiles<DOC_CH, EDGE_CH, NL>(a, s_src, s_row, &s_invalid, s_tab, M, S, gk, K,
-                                                kb, s0, s1, miss_row, stage);
+                                                kb, s0, s1, shift, miss_row, stage);
                 continue;
             }
         }
@@ -421,11 +428,11 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
                 const bool ok = c >= 0 && c < a.n_docs;
                 const int64_t x0 = ok ? a.author[c] : 0;
                 const int64_t x1 = NL == 2 ? a.extra[t0 + tid] : 0;
-                resolve_tile<NL>(a, s_src[0], s_row[0], &s_invalid, s_tab, M, S, gk, K, kb, t0, 0,
-                                 c, x0, x1);
+                resolve_tile<NL>(a, s_src[0], s_row[0], &s_invalid, s_tab, M, S, gk, K, kb, t0,
+                                 shift, 0, c, x0, x1);
             }
             lds_barrier();
-            copy_rows<DOC_CH, EDGE_CH, NL>(a, s_src[0], s_row[0], t0, n);
+            copy_rows<DOC_CH, EDGE_CH, NL>(a, s_src[0], s_row[0], t0 + shift, n);
             lds_barrier();
         }
     }
@@ -519,6 +526,27 @@ hipError_t dispatch_widths(JoinArgs &a, int32_t wgs, int device, hipStream_t str
     return launch_form<0, 0, L>(a, wgs, device, stream);
 }
 
+// Padded layout: slot r = v * n_max + i is a candidate's slot when i < min(n_v, n_max). Writes
+// the valid mask of every slot; a pad slot also gets zero bytes over the row width and hit 0.
+__global__ void pad_fill_kernel(JoinArgs a, int NL, int width_chunks, int8_t *valid) {
+    const int64_t slots = (int64_t)a.n_viewers * a.n_max;
+    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < slots;
+         r += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t v = r / a.n_max, i = r - v * a.n_max;
+        const int64_t nv = clamp64(a.cand_offsets[v + 1], a.total_cand) -
+                           clamp64(a.cand_offsets[v], a.total_cand);
+        const bool used = i < nv;
+        valid[r] = used ? 1 : 0;
+        if (!used) {
+            for (int l = 0; l < NL; ++l)
+                a.hit[r * NL + l] = 0;
+            chunk_t *o = reinterpret_cast<chunk_t *>(a.out + r * a.out_stride);
+            for (int q = 0; q < width_chunks; ++q)
+                o[q] = chunk_t{0u, 0u, 0u, 0u};
+        }
+    }
+}
+
 __global__ void validate_keys_kernel(const int64_t *key_offsets, const int64_t *keys,
                                      int32_t n_viewers, int64_t total_keys,
                                      unsigned long long *first_bad) {
@@ -539,6 +567,19 @@ hipError_t launch_join(JoinArgs &a, int n_lookups, int32_t workgroups, int devic
                        hipStream_t stream) {
     return n_lookups == 2 ? dispatch_widths<2>(a, workgroups, device, stream)
                           : dispatch_widths<1>(a, workgroups, device, stream);
+}
+
+hipError_t launch_pad_fill(const JoinArgs &a, int n_lookups, int8_t *valid_mask,
+                           hipStream_t stream) {
+    const int64_t slots = (int64_t)a.n_viewers * a.n_max;
+    if (slots <= 0)
+        return hipSuccess;
+    const int64_t blocks = (slots + 255) / 256;
+    const int grid = (int)(blocks < 8192 ? blocks : 8192);
+    const int width_chunks = (a.doc_bytes + n_lookups * a.edge_bytes) / 16;
+    hipLaunchKernelGGL(pad_fill_kernel, dim3(grid), dim3(256), 0, stream, a, n_lookups,
+                       width_chunks, valid_mask);
+    return hipGetLastError();
 }
 
 hipError_t launch_validate_keys(const int64_t *key_offsets, const int64_t *keys,

@@ -259,7 +259,49 @@ def pin_invariants(lib, seeds=(3, 4)):
         assert np.array_equal(o1, out[:, :wd + we]) and np.array_equal(h1[:, 0], hit[:, 0])
 
 
-ALL_PINS = (pin_golden, pin_scan, pin_alg1, pin_invariants)
+# --------------------------------------------------------------------------------------------
+def pin_padding(lib):
+    """§6.3's padding example, then the padded layout against the CSR join on random inputs."""
+    g = json.loads((GOLDEN / "padding_worked.json").read_text())
+    feat = np.arange(100 * 16, dtype=np.int64).astype(np.uint8).reshape(100, 16)
+    feat[:, 0] = np.arange(100)                       # row p starts with the byte p
+    pos = g["positions"]
+    co = np.array([0, len(pos[0]), len(pos[0]) + len(pos[1])])
+    ci = np.array(pos[0] + pos[1])
+    T, H, V, inv = oracle.join_padded(np.full(100, 7, np.int64), feat, co, ci, np.zeros(3, np.int64),
+                                      np.zeros(0, np.int64), np.zeros((0, 16), np.uint8),
+                                      g["n_max"], lib=lib)
+    assert V.tolist() == g["expected_valid"], "padding example: valid mask"
+    for b, want in enumerate(g["expected_rows"]):
+        for i, p in enumerate(want):
+            if p is None:
+                assert not T[b, i].any() and not H[b, i].any(), "padding example: pad slot"
+            else:
+                assert np.array_equal(T[b, i, :16], feat[p]), "padding example: gathered row"
+    got_idx = [[int(b), int(i)] for b, i in zip(*np.nonzero(V))]
+    assert got_idx == g["scatter_indices"], "padding example: scatter indices"
+    for seed in range(12):
+        tc = W.tiny_case(3000 + seed, max_viewers=5)
+        b = tc.batch
+        n = np.diff(b.cand_offsets.numpy())
+        n_max = int(n.max()) + (seed % 3) - 1 if n.max() > 0 else 1   # includes truncation
+        n_max = max(n_max, 1)
+        extra = [b.actor] if tc.n_lookups == 2 else None
+        T, H, V, inv = oracle.join_padded(tc.author_id, tc.doc_rows, b.cand_offsets, b.cand_idx,
+                                          b.key_offsets, b.keys, b.edge_rows, n_max,
+                                          default_row=tc.default_row, n_lookups=tc.n_lookups,
+                                          extra_keys=extra, lib=lib)
+        out, hit, _ = _run(lib, tc, oracle.LOWER_BOUND)
+        co = b.cand_offsets.numpy()
+        for v in range(len(n)):
+            k = min(n[v], n_max)
+            assert np.array_equal(T[v, :k], out[co[v]:co[v] + k]), f"padded rows, seed {seed}"
+            assert np.array_equal(H[v, :k], hit[co[v]:co[v] + k]), f"padded hits, seed {seed}"
+            assert V[v, :k].all() and not V[v, k:].any(), f"padded valid, seed {seed}"
+            assert not T[v, k:].any() and not H[v, k:].any(), f"padded pads, seed {seed}"
+
+
+ALL_PINS = (pin_golden, pin_scan, pin_alg1, pin_invariants, pin_padding)
 
 
 def run_all(lib_path=None):

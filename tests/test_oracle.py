@@ -41,6 +41,10 @@ def test_pin_invariants(lib):
     P.pin_invariants(lib)
 
 
+def test_pin_padding(lib):
+    P.pin_padding(lib)
+
+
 # ---- edge cases of the readings --------------------------------------------------------------
 def _one(lib, author, doc, cand, keys, edge, **kw):
     return oracle.join_single(np.asarray(author, np.int64), np.asarray(doc, np.uint8),

@@ -58,6 +58,8 @@ def load(path: Optional[Path] = None):
                               vp,
                               i64, vp,
                               vp, i64, vp]
+    lib.ccor_sort_affinity.restype = ctypes.c_int
+    lib.ccor_sort_affinity.argtypes = [i64, vp, vp, vp, i64, vp, vp]
     return lib
 
 
@@ -138,6 +140,21 @@ def join(author_id, doc_rows, cand_offsets, cand_idx, key_offsets, keys, edge_ro
     if inv < 0:
         raise ValueError("oracle rejected its arguments")
     return out, hit, int(inv)
+
+
+def sort_affinity(key_offsets, keys, rows, lib=None):
+    """Alg. 1 Step 1 per viewer (stable): returns (sorted keys int64, rows moved with them)."""
+    lib = lib or _default_lib()
+    ko, ks = _i64(key_offsets), _i64(keys)
+    r = as_bytes(rows)
+    if r.shape[0] != ks.shape[0]:
+        raise ValueError("rows and keys disagree on K")
+    ko_out = np.empty_like(ks)
+    r_out = np.empty_like(r)
+    if lib.ccor_sort_affinity(ko.shape[0] - 1, _ptr(ko), _ptr(ks), _ptr(r), r.shape[1],
+                              _ptr(ko_out), _ptr(r_out)) != 0:
+        raise ValueError("oracle rejected its arguments")
+    return ko_out, r_out
 
 
 def pad_scatter(rows, hit, cand_offsets, n_max: int):

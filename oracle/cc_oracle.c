@@ -212,3 +212,65 @@ int64_t ccor_join(int method,
     }
     return invalid;
 }
+
+/*
+ * Alg. 1 Step 1 (§3.1): sort each viewer's affinity records by author id (signed int64,
+ * ascending) and move the feature rows with them. The sort is stable: records with equal ids
+ * keep their input order, so the leftmost-equal-key rule of the join picks the record that came
+ * first. Plain top-down merge sort of record indices, one viewer at a time.
+ * Returns 0, or -1 on an argument error.
+ */
+static void merge_sort_idx(const int64_t *keys, int64_t *idx, int64_t *tmp, int64_t n)
+{
+    if (n < 2)
+        return;
+    int64_t h = n / 2;
+    merge_sort_idx(keys, idx, tmp, h);
+    merge_sort_idx(keys, idx + h, tmp, n - h);
+    int64_t i = 0, j = h, k = 0;
+    while (i < h && j < n) {
+        if (keys[idx[j]] < keys[idx[i]])       /* strictly less: ties keep the left element */
+            tmp[k++] = idx[j++];
+        else
+            tmp[k++] = idx[i++];
+    }
+    while (i < h)
+        tmp[k++] = idx[i++];
+    while (j < n)
+        tmp[k++] = idx[j++];
+    memcpy(idx, tmp, (size_t)n * sizeof(int64_t));
+}
+
+int ccor_sort_affinity(int64_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
+                       const uint8_t *rows_in, int64_t row_bytes, int64_t *keys_out,
+                       uint8_t *rows_out)
+{
+    if (n_viewers < 0 || row_bytes < 0 || (n_viewers > 0 && !key_offsets))
+        return -1;
+    for (int64_t v = 0; v < n_viewers; v++) {
+        int64_t k0 = key_offsets[v], k1 = key_offsets[v + 1];
+        if (k0 < 0 || k1 < k0)
+            return -1;
+        int64_t K = k1 - k0;
+        if (K == 0)
+            continue;
+        int64_t *idx = (int64_t *)malloc((size_t)K * sizeof(int64_t));
+        int64_t *tmp = (int64_t *)malloc((size_t)K * sizeof(int64_t));
+        if (!idx || !tmp) {
+            free(idx);
+            free(tmp);
+            return -1;
+        }
+        for (int64_t i = 0; i < K; i++)
+            idx[i] = i;
+        merge_sort_idx(keys_in + k0, idx, tmp, K);
+        for (int64_t i = 0; i < K; i++) {
+            keys_out[k0 + i] = keys_in[k0 + idx[i]];
+            memcpy(rows_out + (k0 + i) * row_bytes, rows_in + (k0 + idx[i]) * row_bytes,
+                   (size_t)row_bytes);
+        }
+        free(idx);
+        free(tmp);
+    }
+    return 0;
+}

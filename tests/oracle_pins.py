@@ -301,7 +301,43 @@ def pin_padding(lib):
             assert not T[v, k:].any() and not H[v, k:].any(), f"padded pads, seed {seed}"
 
 
-ALL_PINS = (pin_golden, pin_scan, pin_alg1, pin_invariants, pin_padding)
+# --------------------------------------------------------------------------------------------
+def pin_sort(lib):
+    """Alg. 1 Step 1: the oracle's per-viewer sort against Python's stable sorted(), then the
+    whole of Alg. 1 (sort, then join) against the NumPy route, on shuffled records."""
+    for seed in range(40):
+        tc = W.tiny_case(7000 + seed, max_k=60, max_viewers=4, dup_keys=bool(seed % 2))
+        b = tc.batch
+        ko = b.key_offsets.numpy()
+        g = W.gen("cpu", seed, 5)
+        keys = b.keys.clone()
+        rows = b.edge_rows.clone()
+        for v in range(len(ko) - 1):          # shuffle each viewer's records
+            p = torch.randperm(int(ko[v + 1] - ko[v]), generator=g) + int(ko[v])
+            keys[ko[v]:ko[v + 1]] = b.keys[p]
+            rows[ko[v]:ko[v + 1]] = b.edge_rows[p]
+        ks, rs = oracle.sort_affinity(ko, keys, rows, lib=lib)
+        kn, rn = keys.numpy(), oracle.as_bytes(rows)
+        for v in range(len(ko) - 1):
+            sl = slice(ko[v], ko[v + 1])
+            order = sorted(range(int(ko[v + 1] - ko[v])), key=lambda i: int(kn[sl][i]))
+            assert ks[sl].tolist() == [int(kn[sl][i]) for i in order], f"sort keys, seed {seed}"
+            assert np.array_equal(rs[sl], rn[sl][order]), f"sort rows, seed {seed}"
+        # whole Alg. 1 on one viewer: shuffled records -> sort -> join == NumPy Alg. 1
+        v0 = slice(ko[0], ko[1])
+        if ko[1] > ko[0]:
+            cand = b.cand_idx[b.cand_offsets[0]:b.cand_offsets[1]].numpy()
+            ok = (cand >= 0) & (cand < tc.author_id.numel())
+            d = tc.author_id.numpy()[np.where(ok, cand, 0)]
+            O, valid = alg1_numpy(d, kn[v0], rn[v0])
+            out, hit, _ = oracle.join_single(tc.author_id, tc.doc_rows, cand, ks[v0], rs[v0],
+                                             lib=lib, fill=FILL)
+            wd = tc.doc_rows.shape[1]
+            assert np.array_equal(hit[ok, 0].astype(bool), valid[ok]), f"Alg.1 valid, seed {seed}"
+            assert np.array_equal(out[ok, wd:], O[ok]), f"Alg.1 rows, seed {seed}"
+
+
+ALL_PINS = (pin_golden, pin_scan, pin_alg1, pin_invariants, pin_padding, pin_sort)
 
 
 def run_all(lib_path=None):

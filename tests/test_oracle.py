@@ -45,6 +45,10 @@ def test_pin_padding(lib):
     P.pin_padding(lib)
 
 
+def test_pin_sort(lib):
+    P.pin_sort(lib)
+
+
 # ---- edge cases of the readings --------------------------------------------------------------
 def _one(lib, author, doc, cand, keys, edge, **kw):
     return oracle.join_single(np.asarray(author, np.int64), np.asarray(doc, np.uint8),
@@ -155,6 +159,8 @@ MUTANTS = [
      "extra_keys[(l - 1) * total_cand + (j > c0 ? j - 1 : j)]"),
     ("invalid doc segment not cleared", "                memset(row, 0, (size_t)doc_bytes);\n",
      "\n"),
+    ("sort loses stability", "if (keys[idx[j]] < keys[idx[i]])", "if (keys[idx[j]] <= keys[idx[i]])"),
+    ("sorted rows not moved", "rows_in + (k0 + idx[i]) * row_bytes", "rows_in + (k0 + i) * row_bytes"),
 ]
 
 

@@ -143,6 +143,28 @@ def all_configs(torch, P, W, dev, seed):
                                "hbm_gbps": algp / (pm / 1e3) / 1e9,
                                "hbm_frac_of_peak": algp / (pm / 1e3) / 1e9 / PEAK_GBPS}
             del outp, hitp, valid
+        if i in (2, 3, 5):
+            # Alg. 1 Step 1 on the same records (shuffled within each viewer): the sort that
+            # precedes the join when affinity records arrive unsorted.
+            bs = b if i != 2 else W.pack(W.make_requests(st10, r, seed, n_viewers=64))
+            ko = bs.key_offsets
+            nk = bs.keys.numel()
+            perm = torch.argsort(torch.rand(nk, device=dev) + 2.0 * torch.repeat_interleave(
+                torch.arange(ko.numel() - 1, device=dev), ko[1:] - ko[:-1]))
+            k_in, r_in = bs.keys[perm].contiguous(), bs.edge_rows[perm].contiguous()
+            k_out, r_out = torch.empty_like(k_in), torch.empty_like(r_in)
+            ws = torch.empty(P.cc_sort_workspace_bytes(nk, ko.numel() - 1), dtype=torch.uint8,
+                             device=dev)
+            mk = int((ko[1:] - ko[:-1]).max())
+            fns = lambda: P.cc_sort_affinity(ko, k_in, r_in, k_out, r_out, ws, max_keys=mk)
+            sm, smean = time_launches(torch, fns, 30)
+            alg_s = nk * (16 + 2 * we)
+            res[f"{i}-sort"] = {"entry": "cc_sort_affinity", "viewers": ko.numel() - 1,
+                                "records": nk, "row_bytes": we, "ms_median": sm,
+                                "ms_mean": smean, "records_per_s": nk / (sm / 1e3),
+                                "algorithmic_bytes": alg_s, "hbm_gbps": alg_s / (sm / 1e3) / 1e9,
+                                "hbm_frac_of_peak": alg_s / (sm / 1e3) / 1e9 / PEAK_GBPS}
+            del k_in, r_in, k_out, r_out, ws
         P.cc_store_destroy(store)
         res[str(i)] = {"entry": entry, "viewers": r.n_viewers, "candidates": n,
                        "keys": b.keys.numel(), "lookups": L, "ms_median": med, "ms_mean": mean,

@@ -234,6 +234,38 @@ CC_API cc_status cc_join_batched_tuned(const cc_store *store, int32_t n_viewers,
                                 const cc_tuning *tuning, hipStream_t stream);
 
 /*
+ * cc_sort_affinity -- Alg. 1 Step 1 (§3.1) on the device: sort each viewer's affinity records
+ * by author id (signed int64, ascending) and move each record's feature row with it. The sort
+ * is stable: records with equal ids keep their input order, so the join's leftmost-equal-key
+ * rule picks the record that came first (the reading of Alg. 1's unspecified tie order).
+ *
+ *   n_viewers      B >= 0.
+ *   key_offsets    [B+1] int64 device, CSR offsets as in cc_join_batched (records of viewer v
+ *                  are [key_offsets[v], key_offsets[v+1]); sorted within that range).
+ *   keys_in        [total_keys] int64 device, any order within a viewer.
+ *   rows_in        [total_keys][row_bytes] device.
+ *   row_bytes      positive multiple of 16.
+ *   total_keys     host copy of key_offsets[B]; < 2^32.
+ *   max_keys       host upper bound on any one viewer's record count (fewer merge passes), or
+ *                  0 if unknown. The output of a viewer with more records than max_keys is
+ *                  unspecified (every access still stays inside the buffers).
+ *   keys_out       [total_keys] int64 device (sorted keys, same CSR offsets).
+ *   rows_out       [total_keys][row_bytes] device (rows in the sorted order).
+ *   workspace      device scratch of at least cc_sort_workspace_bytes(total_keys, n_viewers)
+ *                  bytes, 16-byte aligned, owned by the caller (the library allocates nothing).
+ * Outputs must not overlap inputs or the workspace. Alignment: rows 16 bytes, keys and
+ * offsets 8 bytes. Offsets that break the CSR rules give unspecified output, but they are
+ * clamped to [0, total_keys] and every access stays inside the buffers. Asynchronous on
+ * `stream`. Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_DEVICE.
+ */
+CC_API int64_t cc_sort_workspace_bytes(int64_t total_keys, int32_t n_viewers);
+CC_API cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets,
+                                  const int64_t *keys_in, const void *rows_in, int32_t row_bytes,
+                                  int64_t total_keys, int64_t max_keys, int64_t *keys_out,
+                                  void *rows_out, void *workspace, int64_t workspace_bytes,
+                                  hipStream_t stream);
+
+/*
  * cc_validate_keys -- debug helper: check that each viewer's keys are strictly increasing
  * (the precondition under which the join result is unique, §3.1 Alg. 1 Step 1 output).
  * Synchronises `stream`. Returns CC_OK, or CC_ERR_UNSORTED_KEYS with *first_bad_viewer set to

@@ -16,7 +16,7 @@ LIB_PATH = Path(__file__).resolve().with_name("libccjoin.so")
 EXPORTS = (
     "cc_store_create", "cc_store_destroy", "cc_store_info", "cc_store_invalid_count",
     "cc_store_reset_invalid_count", "cc_join", "cc_join_batched", "cc_join_batched_tuned",
-    "cc_join_batched_padded",
+    "cc_join_batched_padded", "cc_sort_workspace_bytes", "cc_sort_affinity",
     "cc_validate_keys", "cc_status_string", "cc_last_device_error",
 )
 
@@ -66,6 +66,7 @@ def lib():
                                       vp],
             "cc_join_batched_padded": [vp, i32, vp, vp, i64, vp, vp, i64, vp, i32, vp, i32,
                                        ctypes.POINTER(vp), i64, vp, i64, vp, vp, vp],
+            "cc_sort_affinity": [i32, vp, vp, vp, i32, i64, i64, vp, vp, vp, i64, vp],
             "cc_validate_keys": [vp, vp, i32, i64, P64, vp],
             "cc_status_string": [st],
             "cc_last_device_error": [],
@@ -75,6 +76,8 @@ def lib():
             f.argtypes = args
             f.restype = st
         L.cc_status_string.restype = ctypes.c_char_p
+        L.cc_sort_workspace_bytes.argtypes = [i64, i32]
+        L.cc_sort_workspace_bytes.restype = i64
         _lib = L
     return _lib
 
@@ -203,6 +206,22 @@ def cc_join_batched_padded(store: int, cand_offsets, cand_idx, key_offsets, edge
         _ptr(key_offsets), _ptr(edge_keys), tk, _ptr(edge_feats), ew, _ptr(default_row),
         n_lookups, ex, n_max, _ptr(out), stride, _ptr(hit_mask), _ptr(valid_mask),
         _stream(stream)), "cc_join_batched_padded")
+
+
+def cc_sort_workspace_bytes(total_keys: int, n_viewers: int) -> int:
+    return lib().cc_sort_workspace_bytes(total_keys, n_viewers)
+
+
+def cc_sort_affinity(key_offsets, keys_in, rows_in, keys_out, rows_out, workspace,
+                     max_keys: int = 0, total_keys: Optional[int] = None, stream=None) -> None:
+    """Stable per-viewer sort of affinity records (Alg. 1 Step 1; see include/cc_join.h)."""
+    tk = keys_in.numel() if total_keys is None else total_keys
+    rb = int(_prod(rows_in.shape[1:])) * rows_in.element_size()
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().cc_sort_affinity(key_offsets.numel() - 1, _ptr(key_offsets), _ptr(keys_in),
+                                  _ptr(rows_in), rb, tk, max_keys, _ptr(keys_out),
+                                  _ptr(rows_out), _ptr(workspace), ws_bytes, _stream(stream)),
+           "cc_sort_affinity")
 
 
 def cc_validate_keys(key_offsets, edge_keys, total_keys: Optional[int] = None, stream=None):

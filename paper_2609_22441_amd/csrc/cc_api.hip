@@ -340,6 +340,46 @@ cc_status cc_join_batched(const cc_store *store, int32_t n_viewers, const int64_
                                  hit_mask, nullptr, stream);
 }
 
+int64_t cc_sort_workspace_bytes(int64_t total_keys, int32_t n_viewers) {
+    return ccj::sort_workspace_bytes(total_keys, n_viewers);
+}
+
+namespace {
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return na > 0 && nb > 0 && x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+}  // namespace
+
+cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
+                           const void *rows_in, int32_t row_bytes, int64_t total_keys,
+                           int64_t max_keys, int64_t *keys_out, void *rows_out, void *workspace,
+                           int64_t workspace_bytes, hipStream_t stream) {
+    if (n_viewers < 0 || total_keys < 0 || total_keys >= ((int64_t)1 << 32) || max_keys < 0)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (row_bytes <= 0 || (row_bytes & 15))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_viewers > 0 && !key_offsets)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (total_keys == 0 || n_viewers == 0)
+        return CC_OK;
+    const int64_t need = ccj::sort_workspace_bytes(total_keys, n_viewers);
+    if (!keys_in || !rows_in || !keys_out || !rows_out || !workspace || workspace_bytes < need)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (!aligned(key_offsets, 8) || !aligned(keys_in, 8) || !aligned(keys_out, 8) ||
+        !aligned(rows_in, 16) || !aligned(rows_out, 16) || !aligned(workspace, 16))
+        return CC_ERR_INVALID_ARGUMENT;
+    const int64_t kbytes = total_keys * 8, rbytes = total_keys * (int64_t)row_bytes;
+    if (overlaps(keys_out, kbytes, keys_in, kbytes) || overlaps(keys_out, kbytes, rows_in, rbytes) ||
+        overlaps(rows_out, rbytes, keys_in, kbytes) || overlaps(rows_out, rbytes, rows_in, rbytes) ||
+        overlaps(keys_out, kbytes, workspace, need) || overlaps(rows_out, rbytes, workspace, need) ||
+        overlaps(keys_out, kbytes, rows_out, rbytes))
+        return CC_ERR_INVALID_ARGUMENT;
+    hipError_t e = ccj::launch_sort(n_viewers, key_offsets, keys_in, rows_in, row_bytes,
+                                    total_keys, max_keys, keys_out, rows_out, workspace, stream);
+    return e == hipSuccess ? CC_OK : device_error(e);
+}
+
 cc_status cc_validate_keys(const int64_t *key_offsets, const int64_t *edge_keys,
                            int32_t n_viewers, int64_t total_keys, int64_t *first_bad_viewer,
                            hipStream_t stream) {

@@ -52,6 +52,15 @@ hipError_t launch_join(JoinArgs &args, int n_lookups, int32_t workgroups, int de
 hipError_t launch_pad_fill(const JoinArgs &args, int n_lookups, int8_t *valid_mask,
                            hipStream_t stream);
 
+// Workspace bytes of the affinity-record sort for `total` records in `n_viewers` viewers.
+int64_t sort_workspace_bytes(int64_t total, int32_t n_viewers);
+
+// Enqueue the per-viewer stable sort of affinity records (keys + rows) into keys_out/rows_out.
+// max_keys > 0 bounds the records of any one viewer (fewer merge rounds); 0 = unknown.
+hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
+                       const void *rows_in, int32_t row_bytes, int64_t total, int64_t max_keys,
+                       int64_t *keys_out, void *rows_out, void *workspace, hipStream_t stream);
+
 // Enqueue the key-order check; *first_bad (device) must hold UINT64_MAX beforehand.
 hipError_t launch_validate_keys(const int64_t *key_offsets, const int64_t *keys,
                                 int32_t n_viewers, int64_t total_keys,

@@ -1,0 +1,435 @@
+// Alg. 1 Step 1 on the device (Connected Content Retriever §3.1): sort each viewer's affinity
+// records by author id and move their feature rows with them.
+//
+// Each viewer's records (a CSR segment) are cut into tiles of kTile records. Elements are
+// 16 bytes, (key, input position), ordered by key then position. That order is unique, so any
+// correct sort is stable.
+//   0. plan: tile offsets per viewer (an exclusive scan of ceil(K_v / kTile)).
+//   1. block sort: a workgroup loads one tile; every thread sorts kEpt records in registers
+//      with a bitonic network, then log2(kTile / kEpt) merge-path rounds in LDS double the
+//      sorted runs until the tile is one run.
+//   2. merge rounds: within each viewer, runs of kTile << r records are merged pairwise, one
+//      output tile per workgroup. A viewer with n tiles takes part in ceil(log2 n) rounds. The
+//      tile's split on the merge path is found by a 64-ary search run by one wavefront (a few
+//      rounds of 64 probes instead of a ~20-step dependent binary search); the tile is merged
+//      in LDS, kEpt outputs per thread.
+//   3. A viewer's last pass (its block sort when it has one tile, else its last merge round)
+//      writes the sorted keys and copies each record's feature row from the input, straight
+//      from LDS; earlier passes write elements to two ping-pong arrays in a caller-provided
+//      workspace.
+// LDS rows are padded by one element every kEpt elements so that the per-thread blocked
+// accesses (stride kEpt elements) spread over the banks.
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+#include "join_internal.h"
+
+namespace ccj {
+namespace {
+
+constexpr int kTile = 4096;                       // records per tile
+constexpr int kThreads = 256;                     // threads per workgroup
+constexpr int kEpt = kTile / kThreads;            // records per thread (16)
+constexpr int kLdsElems = kTile + kTile / kEpt;   // padded LDS tile
+
+typedef unsigned int chunk_t __attribute__((ext_vector_type(4)));
+
+struct Elem {
+    int64_t key;
+    int64_t f;    // flat input position
+};
+
+__device__ __forceinline__ bool elem_less(const Elem &a, const Elem &b) {
+    return a.key != b.key ? a.key < b.key : a.f < b.f;
+}
+
+// a goes first in a merge (ties go to the first run).
+__device__ __forceinline__ bool first_le(const Elem &a, const Elem &b) { return !elem_less(b, a); }
+
+__device__ __forceinline__ int pidx(int i) { return i + i / kEpt; }
+
+__device__ __forceinline__ void lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__device__ __forceinline__ int64_t clampk(int64_t v, int64_t hi) {
+    return v < 0 ? 0 : (v > hi ? hi : v);
+}
+
+// Segment [kb, ke) of viewer v, offsets clamped to [0, total] and made non-decreasing.
+__device__ __forceinline__ void segment(const int64_t *off, int64_t total, int64_t v, int64_t &kb,
+                                        int64_t &ke) {
+    kb = clampk(off[v], total);
+    ke = max(kb, clampk(off[v + 1], total));
+}
+
+__device__ __forceinline__ int64_t tiles_of(int64_t n) { return (n + kTile - 1) / kTile; }
+
+__device__ __forceinline__ int rounds_of(int64_t tiles) {
+    int r = 0;
+    while (((int64_t)1 << r) < tiles)
+        ++r;
+    return r;
+}
+
+// Largest v in [0, B) with tile_off[v] <= t (tile_off non-decreasing, tile_off[0] = 0).
+__device__ __forceinline__ int64_t owner(const int64_t *tile_off, int64_t B, int64_t t) {
+    int64_t lo = 0, hi = B - 1;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi + 1) >> 1;
+        if (tile_off[mid] <= t)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ Elem pad_elem() { return Elem{INT64_MAX, INT64_MAX}; }
+
+// c ? x : y field by field (a select of the whole struct is lowered through scratch memory).
+__device__ __forceinline__ Elem sel(bool c, const Elem &x, const Elem &y) {
+    return Elem{c ? x.key : y.key, c ? x.f : y.f};
+}
+
+// Compare-exchange: afterwards a <= b when up, a >= b otherwise.
+__device__ __forceinline__ void cx(Elem &a, Elem &b, bool up) {
+    const bool sw = up ? elem_less(b, a) : elem_less(a, b);
+    const Elem x = sel(sw, b, a), y = sel(sw, a, b);
+    a = x;
+    b = y;
+}
+
+// Bitonic network over a thread's kEpt registers. Written with template recursion so that every
+// register index is a compile-time constant (a runtime partner index would put the array in
+// scratch memory).
+template <int K, int J>
+__device__ __forceinline__ void bitonic_stage(Elem (&r)[kEpt]) {
+#pragma unroll
+    for (int i = 0; i < kEpt; ++i) {
+        const int p = i ^ J;
+        if (p > i)
+            cx(r[i], r[p], (i & K) == 0);
+    }
+    if constexpr (J > 1)
+        bitonic_stage<K, J / 2>(r);
+}
+
+template <int K>
+__device__ __forceinline__ void bitonic_level(Elem (&r)[kEpt]) {
+    bitonic_stage<K, K / 2>(r);
+    if constexpr (K < kEpt)
+        bitonic_level<K * 2>(r);
+}
+
+__device__ __forceinline__ void sort_regs(Elem (&r)[kEpt]) { bitonic_level<2>(r); }
+
+// Outputs [d, d + kEpt) of merge(A, B), A = s[a_off, a_off + la), B = s[b_off, b_off + lb)
+// (logical indices, padded in LDS). Outputs past la + lb are pad elements.
+__device__ __forceinline__ void merge_ept(const Elem *s, int a_off, int la, int b_off, int lb,
+                                          int d, Elem (&r)[kEpt]) {
+    int lo = d > lb ? d - lb : 0, hi = d < la ? d : la;
+    while (lo < hi) {                      // smallest i with A[i] not among the first d outputs
+        const int mid = (lo + hi) >> 1;
+        if (first_le(s[pidx(a_off + mid)], s[pidx(b_off + d - 1 - mid)]))
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    int ia = lo, ib = d - lo;
+    Elem a = ia < la ? s[pidx(a_off + ia)] : pad_elem();
+    Elem b = ib < lb ? s[pidx(b_off + ib)] : pad_elem();
+#pragma unroll
+    for (int m = 0; m < kEpt; ++m) {
+        const bool take_a = ib >= lb || (ia < la && first_le(a, b));
+        r[m] = sel(take_a, a, b);
+        ia += take_a;
+        ib += !take_a;
+        const bool ok = take_a ? ia < la : ib < lb;
+        const Elem nx = ok ? s[pidx(take_a ? a_off + ia : b_off + ib)] : pad_elem();
+        a = sel(take_a, nx, a);
+        b = sel(take_a, b, nx);
+    }
+}
+
+__device__ __forceinline__ void store_regs(Elem *s, const Elem (&r)[kEpt], int first, int n) {
+#pragma unroll
+    for (int m = 0; m < kEpt; ++m)
+        if (first + m < n)
+            s[pidx(first + m)] = r[m];
+}
+
+// The first n records of s (sorted) belong at flat positions [pos, pos + n). Either write the
+// elements to dst, or, on a viewer's last pass, the keys and the rows they came from.
+__device__ __forceinline__ void emit(const Elem *s, int n, int64_t pos, Elem *__restrict__ dst,
+                                     bool last, int64_t total,
+                                     const chunk_t *__restrict__ rows_in, int row_chunks,
+                                     int64_t *__restrict__ keys_out,
+                                     chunk_t *__restrict__ rows_out) {
+    const int tid = threadIdx.x;
+    if (!last) {
+        for (int i = tid; i < n; i += kThreads)
+            dst[pos + i] = s[pidx(i)];
+        return;
+    }
+    for (int i = tid; i < n; i += kThreads)
+        keys_out[pos + i] = s[pidx(i)].key;
+    constexpr int U = 4;
+    const int n_chunks = n * row_chunks;
+    for (int g0 = tid; g0 < n_chunks; g0 += U * kThreads) {
+        chunk_t c[U];
+        int64_t dst_i[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int g = g0 + u * kThreads;
+            dst_i[u] = -1;
+            if (g < n_chunks) {
+                const int rec = g / row_chunks;
+                const int q = g - rec * row_chunks;
+                const int64_t f = clampk(s[pidx(rec)].f, total - 1);
+                c[u] = rows_in[f * row_chunks + q];
+                dst_i[u] = (pos + rec) * row_chunks + q;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (dst_i[u] >= 0)
+                rows_out[dst_i[u]] = c[u];
+    }
+}
+
+// tile_off[v] = sum of tiles of viewers < v, for v in [0, B]. One workgroup.
+__global__ __launch_bounds__(kThreads) void plan_kernel(const int64_t *off, int32_t B,
+                                                        int64_t total, int64_t *tile_off) {
+    __shared__ int64_t s[kThreads];
+    __shared__ int64_t carry;
+    const int tid = threadIdx.x;
+    if (tid == 0)
+        carry = 0;
+    lds_sync();
+    for (int64_t b0 = 0; b0 <= B; b0 += kThreads) {
+        const int64_t v = b0 + tid;
+        int64_t n = 0;
+        if (v < B) {
+            int64_t kb, ke;
+            segment(off, total, v, kb, ke);
+            n = tiles_of(ke - kb);
+        }
+        s[tid] = n;
+        lds_sync();
+        for (int d = 1; d < kThreads; d <<= 1) {     // inclusive scan (Hillis-Steele)
+            const int64_t x = tid >= d ? s[tid - d] : 0;
+            lds_sync();
+            s[tid] += x;
+            lds_sync();
+        }
+        if (v <= B)
+            tile_off[v] = carry + s[tid] - n;         // exclusive
+        lds_sync();
+        if (tid == kThreads - 1)
+            carry += s[tid];
+        lds_sync();
+    }
+}
+
+struct SortOut {
+    int64_t total;
+    const chunk_t *rows_in;
+    int32_t row_chunks;
+    int64_t *keys_out;
+    chunk_t *rows_out;
+};
+
+__global__ __launch_bounds__(kThreads) void block_sort_kernel(const int64_t *__restrict__ keys,
+                                                              const int64_t *off, int32_t B,
+                                                              const int64_t *tile_off,
+                                                              Elem *__restrict__ out, SortOut o) {
+    __shared__ Elem s[kLdsElems];
+    const int tid = threadIdx.x;
+    if (B <= 0)
+        return;
+    const int64_t n_tiles = tile_off[B];
+    for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {   // uniform per workgroup
+        const int64_t v = owner(tile_off, B, t);
+        int64_t kb, ke;
+        segment(off, o.total, v, kb, ke);
+        const int64_t base = kb + (t - tile_off[v]) * kTile;
+        const int n = (int)(min<int64_t>(base + kTile, ke) - base);
+        const bool last = tile_off[v + 1] - tile_off[v] == 1;
+#pragma unroll
+        for (int m = 0; m < kEpt; ++m) {
+            const int i = m * kThreads + tid;
+            s[pidx(i)] = i < n ? Elem{keys[base + i], base + i} : pad_elem();   // pads sort last
+        }
+        lds_sync();
+        Elem r[kEpt];
+#pragma unroll
+        for (int m = 0; m < kEpt; ++m)
+            r[m] = s[pidx(tid * kEpt + m)];
+        sort_regs(r);
+        for (int L = kEpt; L < kTile; L <<= 1) {
+            lds_sync();                                  // every thread has read s
+            store_regs(s, r, tid * kEpt, kTile);
+            lds_sync();
+            const int d = tid * kEpt;
+            const int a_off = (d / (2 * L)) * (2 * L);
+            merge_ept(s, a_off, L, a_off + L, L, d - a_off, r);
+        }
+        lds_sync();
+        store_regs(s, r, tid * kEpt, kTile);
+        lds_sync();
+        emit(s, n, base, out, last, o.total, o.rows_in, o.row_chunks, o.keys_out, o.rows_out);
+        lds_sync();                                      // s is reused by the next tile
+    }
+}
+
+// Merge-path split: the number of A elements among the first d outputs of merge(A, B), i.e.
+// the smallest i in [lo, hi] such that A[i] is not among them. Run by all 64 lanes of one
+// wavefront (64 probes per round); returns the same value in every lane.
+__device__ int64_t split64(const Elem *A, int64_t la, const Elem *B, int64_t lb, int64_t d) {
+    int64_t lo = d > lb ? d - lb : 0;
+    int64_t hi = d < la ? d : la;
+    const int lane = threadIdx.x & 63;
+    while (hi > lo) {
+        const int64_t n = hi - lo;
+        const int64_t step = (n + 63) / 64;
+        const int64_t m = lo + lane * step;
+        bool in_out = false;                     // A[m] is among the first d outputs
+        if (m < hi)
+            in_out = first_le(A[m], B[d - 1 - m]);
+        const uint64_t ballot = __ballot(m < hi && !in_out);
+        if (step == 1)
+            return ballot ? lo + __builtin_ctzll(ballot) : hi;   // first false, else hi
+        if (ballot == 0) {
+            // Every probe in range was true: the answer lies past the last one in range.
+            const int64_t last = min<int64_t>(63, (n - 1) / step);
+            lo = lo + last * step + 1;
+        } else {
+            const int first = __builtin_ctzll(ballot);
+            const int64_t new_hi = lo + first * step;
+            lo = first == 0 ? lo : lo + (first - 1) * step + 1;
+            hi = new_hi;
+        }
+    }
+    return lo;
+}
+
+// Round r: within every viewer with more than 2^r tiles, merge runs of kTile << r records
+// pairwise from src into dst (a run without a partner is copied).
+__global__ __launch_bounds__(kThreads) void merge_kernel(const Elem *__restrict__ src,
+                                                         Elem *__restrict__ dst,
+                                                         const int64_t *off, int32_t B,
+                                                         const int64_t *tile_off, int r,
+                                                         SortOut o) {
+    __shared__ Elem s[kLdsElems];
+    __shared__ int64_t s_split[2];
+    const int tid = threadIdx.x;
+    if (B <= 0)
+        return;
+    const int64_t n_tiles = tile_off[B];
+    for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {   // uniform per workgroup
+        const int64_t v = owner(tile_off, B, t);
+        const int64_t nt = tile_off[v + 1] - tile_off[v];
+        if (((int64_t)1 << r) >= nt)
+            continue;                                    // this viewer is already sorted
+        const bool last = r == rounds_of(nt) - 1;
+        int64_t kb, ke;
+        segment(off, o.total, v, kb, ke);
+        const int64_t n_seg = ke - kb;
+        const int64_t run = (int64_t)kTile << r;
+        const int64_t out0 = (t - tile_off[v]) * kTile;  // position within the viewer
+        const int64_t a0 = (out0 / (2 * run)) * 2 * run;
+        const int64_t la = min(run, n_seg - a0);
+        const int64_t b0 = a0 + la;
+        const int64_t lb = max<int64_t>(0, min(run, n_seg - b0));
+        const int64_t d0 = out0 - a0;
+        const int64_t d1 = min<int64_t>(d0 + kTile, la + lb);
+        const Elem *A = src + kb + a0;
+        const Elem *Bv = src + kb + b0;
+        if (tid < 64) {
+            const int64_t i0 = split64(A, la, Bv, lb, d0);
+            const int64_t i1 = split64(A, la, Bv, lb, d1);
+            if (tid == 0) {
+                s_split[0] = i0;
+                s_split[1] = i1;
+            }
+        }
+        lds_sync();
+        const int64_t i0 = s_split[0], i1 = s_split[1];
+        const int64_t j0 = d0 - i0;
+        // For sorted runs i0 <= i1 and j0 <= j1; the clamp keeps every access inside the runs
+        // even when malformed offsets made two viewers overlap.
+        const int n = (int)(d1 - d0);
+        const int na = (int)min<int64_t>(max<int64_t>(i1 - i0, 0), n), nb = n - na;
+        // A[i0, i0 + na) then B[j0, j0 + nb) side by side in LDS.
+#pragma unroll 4
+        for (int i = tid; i < n; i += kThreads)
+            s[pidx(i)] = i < na ? A[i0 + i] : Bv[j0 + (i - na)];
+        lds_sync();
+        Elem rr[kEpt];
+        const int d = tid * kEpt;
+        if (d < n)
+            merge_ept(s, 0, na, na, nb, d, rr);
+        lds_sync();
+        if (d < n)
+            store_regs(s, rr, d, n);
+        lds_sync();
+        emit(s, n, kb + a0 + d0, dst, last, o.total, o.rows_in, o.row_chunks, o.keys_out,
+             o.rows_out);
+        lds_sync();                                      // s and s_split are reused
+    }
+}
+
+int64_t round_up(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+}  // namespace
+
+int64_t sort_workspace_bytes(int64_t total, int32_t n_viewers) {
+    if (total <= 0 || n_viewers <= 0)
+        return 0;
+    return 2 * round_up(total * (int64_t)sizeof(Elem)) + round_up((n_viewers + 1) * 8);
+}
+
+hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
+                       const void *rows_in, int32_t row_bytes, int64_t total, int64_t max_keys,
+                       int64_t *keys_out, void *rows_out, void *workspace, hipStream_t stream) {
+    if (total <= 0 || n_viewers <= 0)
+        return hipSuccess;
+    uint8_t *w = static_cast<uint8_t *>(workspace);
+    Elem *buf0 = reinterpret_cast<Elem *>(w);
+    Elem *buf1 = reinterpret_cast<Elem *>(w + round_up(total * (int64_t)sizeof(Elem)));
+    int64_t *tile_off = reinterpret_cast<int64_t *>(w + 2 * round_up(total * (int64_t)sizeof(Elem)));
+    // Upper bound on tiles (every viewer adds at most one partial tile); larger counts are
+    // covered by the kernels' grid-stride loops.
+    int64_t grid = (total + kTile - 1) / kTile + n_viewers;
+    if (grid > (1 << 20))
+        grid = 1 << 20;
+    const int64_t per_viewer = max_keys > 0 ? ((max_keys < total ? max_keys : total) + kTile - 1) / kTile
+                                            : (total + kTile - 1) / kTile;
+    int rounds = 0;
+    while (((int64_t)1 << rounds) < per_viewer)
+        ++rounds;
+    const SortOut o{total, static_cast<const chunk_t *>(rows_in), row_bytes / 16, keys_out,
+                    static_cast<chunk_t *>(rows_out)};
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kThreads), 0, stream, key_offsets, n_viewers,
+                       total, tile_off);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(block_sort_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream,
+                           keys_in, key_offsets, n_viewers, tile_off, buf0, o);
+        e = hipGetLastError();
+    }
+    for (int r = 0; e == hipSuccess && r < rounds; ++r) {
+        const Elem *src = (r & 1) ? buf1 : buf0;
+        Elem *dst = (r & 1) ? buf0 : buf1;
+        hipLaunchKernelGGL(merge_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream, src, dst,
+                           key_offsets, n_viewers, tile_off, r, o);
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+}  // namespace ccj

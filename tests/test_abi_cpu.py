@@ -85,6 +85,41 @@ def test_validate_keys_rejects_bad_arguments():
     assert bad.value == -1
 
 
+def test_sort_workspace_size():
+    lib = B.lib()
+    assert lib.cc_sort_workspace_bytes(0, 3) == 0
+    assert lib.cc_sort_workspace_bytes(-5, 3) == 0
+    assert lib.cc_sort_workspace_bytes(100, 0) == 0
+    assert lib.cc_sort_workspace_bytes(4097, 2) >= 2 * 16 * 4097 + 3 * 8   # ping-pong + plan
+
+
+def test_sort_rejects_bad_arguments():
+    lib = B.lib()
+    ws = lib.cc_sort_workspace_bytes(1000, 1)
+    base = dict(nv=1, off=0x1000, kin=0x2000, rin=0x10000, rb=32, tk=1000, mk=0, kout=0x30000,
+                rout=0x100000, w=0x200000, wb=ws)
+
+    def call(**kw):
+        a = dict(base, **kw)
+        return lib.cc_sort_affinity(a["nv"], a["off"], a["kin"], a["rin"], a["rb"], a["tk"],
+                                    a["mk"], a["kout"], a["rout"], a["w"], a["wb"], None)
+
+    assert call(rb=24) == 1                      # row width not a multiple of 16
+    assert call(tk=-1) == 1
+    assert call(tk=1 << 32) == 1                 # record count must fit 32 bits
+    assert call(nv=-1) == 1
+    assert call(off=None) == 1
+    assert call(kin=None) == 1
+    assert call(wb=ws - 1) == 1                  # workspace too small
+    assert call(rout=0x100008) == 1              # misaligned rows
+    assert call(kout=0x2004) == 1                # misaligned keys
+    assert call(kout=0x2000) == 1                # output keys alias the input keys
+    assert call(rout=0x10000 + 64) == 1          # output rows overlap the input rows
+    assert call(w=0x30000) == 1                  # workspace overlaps the output keys
+    assert call(mk=-1) == 1                      # negative hint
+    assert call(tk=0, kin=None, rin=None, kout=None, rout=None, w=None, wb=0) == 0   # no work
+
+
 def test_library_has_no_cpu_fallback(monkeypatch, tmp_path):
     """The binding refuses to run when the HIP library is missing (no silent fallback)."""
     monkeypatch.setattr(B, "_lib", None)

@@ -1,0 +1,121 @@
+"""GPU parity of the affinity-record sort (Alg. 1 Step 1) against the oracle's stable sort."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_22441_amd as P
+import workload as W
+from gpu_common import note, row_bytes
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+def _shuffle_within(key_offsets, keys, rows, seed):
+    g = W.gen("cpu", seed, 9)
+    ko = key_offsets.cpu().numpy()
+    k, r = keys.clone().cpu(), rows.clone().cpu()
+    for v in range(len(ko) - 1):
+        p = torch.randperm(int(ko[v + 1] - ko[v]), generator=g) + int(ko[v])
+        k[ko[v]:ko[v + 1]] = keys.cpu()[p]
+        r[ko[v]:ko[v + 1]] = rows.cpu()[p]
+    return k, r
+
+
+def _gpu_sort(ko, keys, rows, max_keys=0):
+    n = keys.numel()
+    ws = torch.empty(max(16, P.cc_sort_workspace_bytes(n, ko.numel() - 1)), dtype=torch.uint8,
+                     device=DEV)
+    ko_d, k_d, r_d = ko.to(DEV), keys.to(DEV), rows.to(DEV)
+    k_out = torch.full_like(k_d, -7)
+    r_out = torch.full_like(r_d, 0xCD) if r_d.dtype == torch.uint8 else torch.empty_like(r_d)
+    P.cc_sort_affinity(ko_d, k_d, r_d, k_out, r_out, ws, max_keys=max_keys)
+    torch.cuda.synchronize()
+    return k_out.cpu().numpy(), oracle.as_bytes(r_out.cpu())
+
+
+def _check(ko, keys, rows, what, max_keys=0):
+    gk, gr = _gpu_sort(ko, keys, rows, max_keys)
+    wk, wr = oracle.sort_affinity(ko, keys, rows)
+    assert np.array_equal(gk, wk), f"{what}: keys"
+    assert np.array_equal(gr, wr), f"{what}: rows"
+
+
+def test_tiny_sorts_with_duplicates_and_empty_viewers():
+    note("sort: tiny cases")
+    for seed in range(40):
+        tc = W.tiny_case(8000 + seed, max_k=300, max_viewers=6, dup_keys=bool(seed % 2),
+                         k_values=None if seed % 3 else [0, 250, 3, 0, 100, 1])
+        b = tc.batch
+        k, r = _shuffle_within(b.key_offsets, b.keys, b.edge_rows, seed)
+        mk = int(b.key_offsets.diff().max()) if seed % 4 == 0 else 0    # with and without hint
+        _check(b.key_offsets, k, r, f"seed {seed}", max_keys=mk)
+
+
+@pytest.mark.parametrize("n", [1, 4095, 4096, 4097, 8192, 8193, 12289, 100_000])
+def test_one_viewer_tile_boundaries(n):
+    note(f"sort: one viewer, {n} records")
+    g = W.gen("cpu", n, 3)
+    keys = torch.randint(-1000, 1000, (n,), generator=g)        # many repeats
+    rows = torch.randint(0, 256, (n, 32), generator=g, dtype=torch.int64).to(torch.uint8)
+    _check(torch.tensor([0, n]), keys, rows, f"n={n}")
+
+
+def test_many_ragged_viewers():
+    """Viewers from empty to several tiles in one call: each viewer runs its own number of
+    merge rounds and its result sits in the ping-pong array that matches that count."""
+    note("sort: 300 ragged viewers")
+    g = W.gen("cpu", 77, 3)
+    sizes = torch.tensor([0, 1, 4095, 4096, 4097, 9000, 20000, 0, 70000, 3] * 30)
+    sizes = sizes[torch.randperm(sizes.numel(), generator=g)]
+    ko = torch.cat([torch.zeros(1, dtype=torch.int64), torch.cumsum(sizes, 0)])
+    n = int(ko[-1])
+    keys = torch.randint(-(1 << 40), 1 << 40, (n,), generator=g)
+    keys[::7] = 5                                                # repeats across tiles
+    rows = torch.randint(0, 256, (n, 16), generator=g, dtype=torch.int64).to(torch.uint8)
+    _check(ko, keys, rows, "ragged")
+    _check(ko, keys, rows, "ragged with hint", max_keys=int(sizes.max()))
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("cfg", [3, 5])
+def test_workload_record_sets(cfg):
+    note(f"sort: workload {cfg} record sets")
+    s, r = W.CONFIGS[cfg]
+    s = W.StoreSpec(1_000_000, s.n_authors, s.zipf_s, s.doc_cols, s.doc_dtype)
+    st = W.make_store(s, 2, device=DEV)
+    b = W.pack(W.make_requests(st, r, cfg))
+    k, rw = _shuffle_within(b.key_offsets, b.keys, b.edge_rows, cfg)
+    _check(b.key_offsets.cpu(), k, rw, f"workload {cfg}")
+    _check(b.key_offsets.cpu(), k, rw, f"workload {cfg} with hint",
+           max_keys=int(b.key_offsets.diff().max()))
+
+
+def test_sort_then_join_equals_oracle():
+    note("sort then join")
+    s, r = W.config(2, store_n_docs=300_000, store_n_authors=200_000, req_k=3000,
+                    req_n_cand=20_000, req_n_viewers=3)
+    st = W.make_store(s, 4, device=DEV)
+    b = W.pack(W.make_requests(st, r, 4))
+    k, rw = _shuffle_within(b.key_offsets, b.keys, b.edge_rows, 4)
+    ws = torch.empty(P.cc_sort_workspace_bytes(k.numel(), 3), dtype=torch.uint8, device=DEV)
+    ko_d = b.key_offsets
+    k_s, r_s = torch.empty_like(b.keys), torch.empty_like(b.edge_rows)
+    P.cc_sort_affinity(ko_d, k.to(DEV), rw.to(DEV), k_s, r_s, ws)
+    store = P.cc_store_create(st.author_id, st.doc_rows)
+    try:
+        wd, we = row_bytes(st.doc_rows), row_bytes(b.edge_rows)
+        out = torch.empty(b.cand_idx.numel(), wd + we, dtype=torch.uint8, device=DEV)
+        hit = torch.empty(b.cand_idx.numel(), 1, dtype=torch.int8, device=DEV)
+        P.cc_join_batched(store, b.cand_offsets, b.cand_idx, ko_d, k_s, r_s, out, hit)
+        torch.cuda.synchronize()
+        bc = b.to("cpu")
+        ks, rs = oracle.sort_affinity(bc.key_offsets, k, rw)
+        want = oracle.join(st.author_id.cpu(), st.doc_rows.cpu(), bc.cand_offsets, bc.cand_idx,
+                           bc.key_offsets, ks, rs)
+        assert np.array_equal(out.cpu().numpy(), want[0]) and np.array_equal(hit.cpu().numpy(), want[1])
+    finally:
+        P.cc_store_destroy(store)

@@ -60,6 +60,10 @@ def load(path: Optional[Path] = None):
                               vp, i64, vp]
     lib.ccor_sort_affinity.restype = ctypes.c_int
     lib.ccor_sort_affinity.argtypes = [i64, vp, vp, vp, i64, vp, vp]
+    lib.ccor_resolve.restype = ctypes.c_int
+    lib.ccor_resolve.argtypes = [i64, vp, i64, vp, vp]
+    lib.ccor_upsert.restype = i64
+    lib.ccor_upsert.argtypes = [i64, vp, vp, vp, vp, i64, i64, vp, vp, vp, vp]
     return lib
 
 
@@ -198,6 +202,54 @@ def join_padded(author_id, doc_rows, cand_offsets, cand_idx, key_offsets, keys, 
                          extra_keys=extra, **kw)
     T, H, valid = pad_scatter(out, hit, co_kept, n_max)
     return T, H, valid, inv
+
+
+INT64_MIN = -(1 << 63)
+
+
+def resolve(index_ids, queries, lib=None):
+    """Eq. 6 (§6.3.1): position of each query id in the index, or -1 (index_ids[p] = id at p)."""
+    lib = lib or _default_lib()
+    ix, q = _i64(index_ids), _i64(queries)
+    out = np.empty_like(q)
+    if lib.ccor_resolve(ix.shape[0], _ptr(ix), q.shape[0], _ptr(q), _ptr(out)) != 0:
+        raise ValueError("oracle rejected its arguments")
+    return out
+
+
+class IndexState:
+    """A document index under ingestion (§6.2): the id, author id and row at each position, and
+    the number of stored documents. ``upsert`` applies one batch by sequential replay."""
+
+    def __init__(self, capacity: int, row_bytes: int, lib=None):
+        self.lib = lib or _default_lib()
+        self.capacity = capacity
+        self.n_docs = 0
+        self.ids = np.full(capacity, INT64_MIN, np.int64)
+        self.author = np.zeros(capacity, np.int64)
+        self.rows = np.zeros((capacity, row_bytes), np.uint8)
+
+    def upsert(self, ids, authors, rows):
+        """Apply one batch; returns (n_new, n_rejected), or None when it does not fit (then the
+        state is unchanged)."""
+        i, a = _i64(ids), _i64(authors)
+        r = as_bytes(rows)
+        if not (i.shape[0] == a.shape[0] == r.shape[0]) or r.shape[1] != self.rows.shape[1]:
+            raise ValueError("batch arrays disagree")
+        nd = ctypes.c_int64(self.n_docs)
+        rej = ctypes.c_int64(0)
+        n_new = self.lib.ccor_upsert(self.capacity, ctypes.byref(nd), _ptr(self.ids),
+                                     _ptr(self.author), _ptr(self.rows), self.rows.shape[1],
+                                     i.shape[0], _ptr(i), _ptr(a), _ptr(r), ctypes.byref(rej))
+        if n_new == -1:
+            raise ValueError("oracle rejected its arguments")
+        if n_new == -2:
+            return None
+        self.n_docs = nd.value
+        return int(n_new), int(rej.value)
+
+    def resolve(self, queries):
+        return resolve(self.ids[:self.n_docs], queries, self.lib)
 
 
 def join_single(author_id, doc_rows, cand_idx, keys, edge_rows, **kw):

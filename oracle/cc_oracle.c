@@ -34,6 +34,10 @@
  *   CCOR_HASH:        open-addressing hash table from key to its first index, built per viewer
  *                     in index order. Works for any key order.
  * For sorted keys (duplicates allowed) all three return the same i_min.
+ *
+ * Also here: the stable per-viewer sort of Alg. 1 Step 1 (ccor_sort_affinity), the document-id
+ * map of §6.3.1 Eq. 6 (ccor_resolve) and the sequential replay of ingestion batches of §6.2
+ * (ccor_upsert).
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -89,7 +93,8 @@ static uint64_t mix64(uint64_t z)
     return z;
 }
 
-static int table_build(table_t *t, const int64_t *keys, int64_t n)
+/* An empty table with room for at least n keys at load factor <= 1/2. */
+static int table_init(table_t *t, int64_t n)
 {
     uint64_t cap = 16;
     while (cap < (uint64_t)n * 2)
@@ -104,15 +109,27 @@ static int table_build(table_t *t, const int64_t *keys, int64_t n)
     t->mask = cap - 1;
     for (uint64_t s = 0; s < cap; s++)
         t->idx[s] = -1;
-    for (int64_t i = 0; i < n; i++) {
-        uint64_t s = mix64((uint64_t)keys[i]) & t->mask;
-        while (t->idx[s] >= 0 && t->key[s] != keys[i])
-            s = (s + 1) & t->mask;
-        if (t->idx[s] < 0) {          /* first occurrence keeps its index */
-            t->key[s] = keys[i];
-            t->idx[s] = i;
-        }
+    return 0;
+}
+
+/* Insert key -> i unless the key is present already (then the earlier index stays). */
+static void table_insert(table_t *t, int64_t key, int64_t i)
+{
+    uint64_t s = mix64((uint64_t)key) & t->mask;
+    while (t->idx[s] >= 0 && t->key[s] != key)
+        s = (s + 1) & t->mask;
+    if (t->idx[s] < 0) {          /* first occurrence keeps its index */
+        t->key[s] = key;
+        t->idx[s] = i;
     }
+}
+
+static int table_build(table_t *t, const int64_t *keys, int64_t n)
+{
+    if (table_init(t, n) != 0)
+        return -1;
+    for (int64_t i = 0; i < n; i++)
+        table_insert(t, keys[i], i);
     return 0;
 }
 
@@ -273,4 +290,85 @@ int ccor_sort_affinity(int64_t n_viewers, const int64_t *key_offsets, const int6
         free(tmp);
     }
     return 0;
+}
+
+/*
+ * Eq. 6 (§6.3.1): pos(q) = H[q] when q is a stored document id, else -1. The index is given as
+ * the id stored at each position, index_ids[0, n_index) (ids unique), and H is built from it.
+ * Returns 0, or -1 on an argument error.
+ */
+int ccor_resolve(int64_t n_index, const int64_t *index_ids, int64_t n_q, const int64_t *queries,
+                 int64_t *pos_out)
+{
+    if (n_index < 0 || n_q < 0 || (n_index > 0 && !index_ids) || (n_q > 0 && (!queries || !pos_out)))
+        return -1;
+    table_t t;
+    if (table_build(&t, index_ids, n_index) != 0)
+        return -1;
+    for (int64_t j = 0; j < n_q; j++)
+        pos_out[j] = table_find(&t, queries[j]);
+    table_free(&t);
+    return 0;
+}
+
+/*
+ * Ingestion into the index (§6.2, bootstrap protocol), as its sequential replay: the records of
+ * a batch are applied one at a time in batch order. A stored id has its author id and row
+ * overwritten in place; a new id takes the next free position (n_docs, n_docs + 1, ...) and is
+ * added to H. The id INT64_MIN is reserved (it cannot be stored): such records are skipped and
+ * counted in *n_rejected. A batch whose new ids would not fit in capacity changes nothing.
+ *
+ * State (caller-owned): ids_by_pos, author [capacity], rows [capacity][row_bytes], *n_docs.
+ * Returns the number of new ids, -2 when the batch does not fit, or -1 on an argument error.
+ */
+int64_t ccor_upsert(int64_t capacity, int64_t *n_docs, int64_t *ids_by_pos, int64_t *author,
+                    uint8_t *rows, int64_t row_bytes, int64_t n, const int64_t *ids,
+                    const int64_t *authors_in, const uint8_t *rows_in, int64_t *n_rejected)
+{
+    if (!n_docs || *n_docs < 0 || *n_docs > capacity || n < 0 || row_bytes < 0 || !n_rejected)
+        return -1;
+    if (n > 0 && (!ids || !authors_in || !rows_in))
+        return -1;
+    table_t t;
+    if (table_init(&t, *n_docs + n) != 0)
+        return -1;
+    for (int64_t p = 0; p < *n_docs; p++)
+        table_insert(&t, ids_by_pos[p], p);
+    /* count the distinct new ids first, so that a batch that does not fit changes nothing */
+    int64_t n_new = 0, rejected = 0;
+    table_t seen;
+    if (table_init(&seen, n) != 0) {
+        table_free(&t);
+        return -1;
+    }
+    for (int64_t i = 0; i < n; i++) {
+        if (ids[i] == INT64_MIN) {
+            rejected++;
+            continue;
+        }
+        if (table_find(&t, ids[i]) < 0 && table_find(&seen, ids[i]) < 0) {
+            table_insert(&seen, ids[i], i);
+            n_new++;
+        }
+    }
+    table_free(&seen);
+    if (*n_docs + n_new > capacity) {
+        table_free(&t);
+        return -2;
+    }
+    for (int64_t i = 0; i < n; i++) {
+        if (ids[i] == INT64_MIN)
+            continue;
+        int64_t p = table_find(&t, ids[i]);
+        if (p < 0) {
+            p = (*n_docs)++;
+            table_insert(&t, ids[i], p);
+            ids_by_pos[p] = ids[i];
+        }
+        author[p] = authors_in[i];
+        memcpy(rows + p * row_bytes, rows_in + i * row_bytes, (size_t)row_bytes);
+    }
+    table_free(&t);
+    *n_rejected = rejected;
+    return n_new;
 }

@@ -13,7 +13,12 @@ are independent of the oracle's code:
                          in the viewer's key set, miss rows equal the default row, valid doc
                          segments equal the store row, equivariance under a permutation of the
                          candidates, batched == per-viewer concatenation, the second lookup does
-                         not disturb the first, and the hit count equals the membership count.
+                         not disturb the first, and the hit count equals the membership count;
+* ``pin_padding`` / ``pin_sort`` -- the padded layout of §6.3.1 and Alg. 1 Step 1;
+* ``pin_index_golden`` -- the hand-worked ingestion example in ``tests/golden/upsert_worked.json``;
+* ``pin_resolve``     -- Eq. 6 against a brute-force scan and a sorted-search route;
+* ``pin_upsert``      -- the sequential replay against the four-step batch protocol of §6.2
+                         written with NumPy set operations.
 """
 from __future__ import annotations
 
@@ -337,7 +342,149 @@ def pin_sort(lib):
             assert np.array_equal(out[ok, wd:], O[ok]), f"Alg.1 rows, seed {seed}"
 
 
-ALL_PINS = (pin_golden, pin_scan, pin_alg1, pin_invariants, pin_padding, pin_sort)
+def _golden_int(x):
+    return oracle.INT64_MIN if x == "INT64_MIN" else int(x)
+
+
+def _golden_state(st, d):
+    rb = st.rows.shape[1]
+    n = st.n_docs
+    assert st.ids[:n].tolist() == [_golden_int(x) for x in d["ids"]]
+    assert st.author[:n].tolist() == d["authors"]
+    assert np.array_equal(st.rows[:n], np.repeat(np.array(d["row_fill"], np.uint8)[:, None], rb, 1))
+
+
+def pin_index_golden(lib):
+    """The hand-worked ingestion and id-resolution example in tests/golden/upsert_worked.json."""
+    g = json.loads((GOLDEN / "upsert_worked.json").read_text())
+    st = oracle.IndexState(g["capacity"], g["row_bytes"], lib=lib)
+    for k, bt in enumerate(g["batches"]):
+        ids = [_golden_int(x) for x in bt["ids"]]
+        rows = np.repeat(np.array(bt["row_fill"], np.uint8)[:, None], g["row_bytes"], 1)
+        r = st.upsert(ids, bt["authors"], rows)
+        if bt.get("fits", True):
+            assert r == (bt["n_new"], bt["n_rejected"]), f"upsert golden batch {k}: {r}"
+        else:
+            assert r is None, f"upsert golden batch {k} should not fit"
+        _golden_state(st, bt["after"])
+    q = [_golden_int(x) for x in g["resolve"]["queries"]]
+    assert st.resolve(q).tolist() == g["resolve"]["positions"], "resolve golden"
+
+
+def _random_ids(rng, n, lo=-(1 << 63) + 1, hi=(1 << 63) - 1):
+    out = set()
+    while len(out) < n:
+        out.add(int(rng.integers(lo, hi, dtype=np.int64, endpoint=True)))
+    return list(out)
+
+
+def pin_resolve(lib):
+    """Eq. 6: the oracle's map against a brute-force scan of the index (tiny inputs, int64
+    extremes, the reserved id) and against a sorted-search route (argsort + searchsorted) on a
+    larger index; every stored id resolves to its own position."""
+    rng = np.random.default_rng(11)
+    for seed in range(30):
+        n = int(rng.integers(0, 40))
+        ix = _random_ids(rng, n)
+        if n and seed % 3 == 0:
+            ix[0] = (1 << 63) - 1
+            ix[-1] = oracle.INT64_MIN + 1
+        extra = [0, -1, (1 << 63) - 1, oracle.INT64_MIN] + _random_ids(rng, 5)
+        q = ix + extra
+        rng.shuffle(q)
+        want = []
+        for x in q:
+            p = -1
+            for i, y in enumerate(ix):
+                if y == x:
+                    p = i
+                    break
+            want.append(p)
+        got = oracle.resolve(np.array(ix, np.int64), np.array(q, np.int64), lib=lib)
+        assert got.tolist() == want, f"resolve brute force, seed {seed}"
+    n = 200_000
+    ix = np.array(_random_ids(rng, n), np.int64)
+    q = np.concatenate([ix[rng.integers(0, n, 50_000)], rng.integers(-(1 << 62), 1 << 62, 50_000)])
+    order = np.argsort(ix, kind="stable")
+    s = ix[order]
+    k = np.searchsorted(s, q, side="left")
+    kc = np.minimum(k, n - 1)
+    want = np.where((k < n) & (s[kc] == q), order[kc], -1)
+    got = oracle.resolve(ix, q, lib=lib)
+    assert np.array_equal(got, want), "resolve vs sorted search"
+    assert np.array_equal(oracle.resolve(ix, ix, lib=lib), np.arange(n)), "resolve identity"
+
+
+def bootstrap_numpy(state, ids, authors, rows):
+    """The four-step batch protocol of §6.2 in NumPy: (1) identify new vs stored ids (a tensor
+    membership test), (2) prefix-sum positions for the new ids in order of first appearance,
+    (3) scatter each id's last row to its position, (4) record the new ids in the map."""
+    ids_all, author, table, n_docs, cap = state
+    ok = ids != oracle.INT64_MIN
+    i_ok = np.nonzero(ok)[0]
+    ids_ok = ids[i_ok]
+    stored = np.isin(ids_ok, ids_all[:n_docs])                              # step 1
+    uniq, first = np.unique(ids_ok, return_index=True)
+    is_new_first = np.zeros(len(ids_ok), bool)
+    is_new_first[first] = ~stored[first]
+    n_new = int(is_new_first.sum())
+    if n_docs + n_new > cap:
+        return None
+    new_pos = n_docs + np.cumsum(is_new_first) - 1                          # step 2
+    pos_of = dict(zip(ids_all[:n_docs].tolist(), range(n_docs)))
+    for j in np.nonzero(is_new_first)[0]:
+        pos_of[int(ids_ok[j])] = int(new_pos[j])
+    rev_u, rev_first = np.unique(ids_ok[::-1], return_index=True)
+    last = len(ids_ok) - 1 - rev_first                                      # last occurrences
+    tgt = np.array([pos_of[int(x)] for x in ids_ok[last]], np.int64)
+    table[tgt] = rows[i_ok[last]]                                           # step 3
+    author[tgt] = authors[i_ok[last]]
+    ids_all[new_pos[is_new_first]] = ids_ok[is_new_first]                   # step 4
+    return n_docs + n_new, n_new, int((~ok).sum())
+
+
+def pin_upsert(lib):
+    """Ingestion: the oracle's sequential replay against the four-step batch protocol written
+    with NumPy set operations, over batches mixing new ids, stored ids, repeats inside a batch,
+    the reserved id, and batches that do not fit; then invariants of the final index."""
+    rng = np.random.default_rng(5)
+    cap, rb = 1500, 16
+    st = oracle.IndexState(cap, rb, lib=lib)
+    ref = [np.full(cap, oracle.INT64_MIN, np.int64), np.zeros(cap, np.int64),
+           np.zeros((cap, rb), np.uint8), 0, cap]
+    universe = np.array(_random_ids(rng, 4000), np.int64)
+    last_row = {}
+    for b in range(25):
+        m = int(rng.integers(0, 400))
+        ids = universe[rng.integers(0, 250 + 150 * b, m)]        # widening pool: new + stored
+        if m and b % 4 == 1:
+            ids[rng.integers(0, m, 3)] = oracle.INT64_MIN
+        authors = rng.integers(-(1 << 40), 1 << 40, m)
+        rows = rng.integers(0, 256, (m, rb)).astype(np.uint8)
+        r = st.upsert(ids, authors, rows)
+        w = bootstrap_numpy(ref, ids, authors, rows)
+        if w is None:
+            assert r is None, f"batch {b}: replay accepted a batch that does not fit"
+        else:
+            ref[3] = w[0]
+            assert r == (w[1], w[2]), f"batch {b}: counts {r} vs {w[1:]}"
+            for i in range(m):
+                if ids[i] != oracle.INT64_MIN:
+                    last_row[int(ids[i])] = (int(authors[i]), rows[i].copy())
+        assert st.n_docs == ref[3], f"batch {b}: n_docs"
+        n = st.n_docs
+        assert np.array_equal(st.ids[:n], ref[0][:n]), f"batch {b}: ids by position"
+        assert np.array_equal(st.author[:n], ref[1][:n]), f"batch {b}: authors"
+        assert np.array_equal(st.rows[:n], ref[2][:n]), f"batch {b}: rows"
+    n = st.n_docs
+    assert len(set(st.ids[:n].tolist())) == n == len(last_row), "positions are a bijection"
+    for x, (a, row) in last_row.items():
+        p = int(st.resolve([x])[0])
+        assert st.author[p] == a and np.array_equal(st.rows[p], row), "last write wins"
+
+
+ALL_PINS = (pin_golden, pin_scan, pin_alg1, pin_invariants, pin_padding, pin_sort,
+            pin_index_golden, pin_resolve, pin_upsert)
 
 
 def run_all(lib_path=None):

@@ -161,6 +161,17 @@ MUTANTS = [
      "\n"),
     ("sort loses stability", "if (keys[idx[j]] < keys[idx[i]])", "if (keys[idx[j]] <= keys[idx[i]])"),
     ("sorted rows not moved", "rows_in + (k0 + idx[i]) * row_bytes", "rows_in + (k0 + i) * row_bytes"),
+    ("resolve reports positions one too high", "pos_out[j] = table_find(&t, queries[j]);",
+     "pos_out[j] = table_find(&t, queries[j]) + (j > 0);"),
+    ("stored ids not overwritten", "            ids_by_pos[p] = ids[i];\n        }\n",
+     "            ids_by_pos[p] = ids[i];\n        } else\n            continue;\n"),
+    ("reserved id stored", "        if (ids[i] == INT64_MIN)\n            continue;",
+     "        if (0)\n            continue;"),
+    ("capacity check off by one", "if (*n_docs + n_new > capacity)", "if (*n_docs + n_new >= capacity)"),
+    ("stored ids counted as new",
+     "if (table_find(&t, ids[i]) < 0 && table_find(&seen, ids[i]) < 0)",
+     "if (table_find(&seen, ids[i]) < 0)"),
+    ("author id not moved", "author[p] = authors_in[i];", "author[p] = authors_in[0];"),
 ]
 
 

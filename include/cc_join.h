@@ -22,8 +22,10 @@
  *   - Data-dependent conditions that a check would need a synchronisation to see have
  *     defined, memory-safe outcomes instead of errors (see cc_join_batched).
  *   - No C++ exception crosses this interface.
- *   - A store is read-only after creation: concurrent joins on one store, from any threads
- *     and streams, are safe.
+ *   - A store is read-only for the joins: concurrent joins on one store, from any threads
+ *     and streams, are safe. Ingestion (cc_store_upsert) is the one writer; it must not overlap
+ *     any other call on the same store (the paper's read-write lock per index, §6.3.1: joins
+ *     and id resolution hold the read side, an ingestion batch the write side).
  */
 #ifndef CC_JOIN_H
 #define CC_JOIN_H
@@ -49,7 +51,8 @@ typedef enum cc_status {
     CC_ERR_OUT_OF_MEMORY = 2,      /* device allocation failed (store creation only)        */
     CC_ERR_DEVICE = 3,             /* a HIP call failed; see cc_last_device_error()         */
     CC_ERR_UNSORTED_KEYS = 4,      /* only from cc_validate_keys                            */
-    CC_ERR_NOT_SUPPORTED = 5       /* no usable gfx950 device                               */
+    CC_ERR_NOT_SUPPORTED = 5,      /* no usable gfx950 device, or a store without an id map */
+    CC_ERR_STORE_FULL = 6          /* an ingestion batch does not fit; the store is unchanged */
 } cc_status;
 
 /* Where cc_store_create reads its source arrays from. */
@@ -232,6 +235,81 @@ CC_API cc_status cc_join_batched_tuned(const cc_store *store, int32_t n_viewers,
                                 int32_t n_lookups, const int64_t *const *extra_keys,
                                 void *out, int64_t out_row_stride, int8_t *hit_mask,
                                 const cc_tuning *tuning, hipStream_t stream);
+
+/*
+ * cc_store_create_indexed -- an empty document store with an id map, for ingestion (§6.2) and
+ * document-id resolution (§6.3.1, Eq. 6).
+ *
+ *   out_store      receives the new store handle (set to NULL on error).
+ *   capacity       documents the store can hold, 0 <= capacity <= 2^31 - 1. Rows, author ids
+ *                  and the id map are allocated for this many documents up front.
+ *   doc_row_bytes  bytes per document row; a positive multiple of 16.
+ *   stream         initialisation is enqueued on this stream.
+ *
+ * Layout in HBM: author ids [capacity] int64, rows [capacity][doc_row_bytes], and the id map:
+ * an open-addressing table of 16-byte entries {id, position} in 64-byte probe groups, sized
+ * to at least twice the capacity (load factor <= 1/2), so that inserts never rebuild it.
+ * The store starts with n_docs = 0; cc_store_upsert fills it. All join entry points accept it.
+ * Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_OUT_OF_MEMORY, CC_ERR_NOT_SUPPORTED, CC_ERR_DEVICE.
+ */
+CC_API cc_status cc_store_create_indexed(cc_store **out_store, int64_t capacity,
+                                         int32_t doc_row_bytes, hipStream_t stream);
+
+/*
+ * cc_store_upsert -- apply one ingestion batch (§6.2, bootstrap protocol: identify new and
+ * stored ids, prefix-sum positions for the new ones, scatter the rows, update the map only
+ * after the rows are written).
+ *
+ * The result is that of applying the records one at a time in batch order: a stored id has
+ * its author id and row overwritten in place (the last record with that id wins); a new id
+ * takes the next free position n_docs, n_docs + 1, ... in order of its first record. The id
+ * INT64_MIN is reserved: its records are skipped and counted in *n_rejected.
+ *
+ *   store          a store from cc_store_create_indexed (else CC_ERR_NOT_SUPPORTED).
+ *   n_records      records in the batch, 0 <= n_records <= 2^30.
+ *   doc_ids        [n_records] int64 device, 8-byte aligned.
+ *   author_ids     [n_records] int64 device, 8-byte aligned.
+ *   doc_rows       [n_records][doc_row_bytes] device, 16-byte aligned.
+ *   workspace      device scratch of cc_upsert_workspace_bytes(n_records) bytes, 16-byte
+ *                  aligned, caller-owned, not overlapping the inputs.
+ *   n_new, n_rejected  host outputs (may be NULL): ids added, records skipped.
+ *
+ * Synchronises `stream` (twice: after the new ids are counted, and at the end). When the new
+ * ids do not fit in the remaining capacity, or an id cannot be placed within the map's probe
+ * limit (64 groups; not expected below load 1/2), the batch is undone and CC_ERR_STORE_FULL is
+ * returned with the store unchanged. Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_NOT_SUPPORTED,
+ * CC_ERR_STORE_FULL, CC_ERR_DEVICE.
+ */
+CC_API int64_t cc_upsert_workspace_bytes(int64_t n_records);
+CC_API cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc_ids,
+                                 const int64_t *author_ids, const void *doc_rows, void *workspace,
+                                 int64_t workspace_bytes, int64_t *n_new, int64_t *n_rejected,
+                                 hipStream_t stream);
+
+/*
+ * cc_store_read -- copy positions [first, first + count) of a store out: author ids into
+ * author_out [count] int64 and rows into rows_out [count][doc_row_bytes] (either may be NULL).
+ * Device buffers, 8- and 16-byte aligned. Requires 0 <= first, first + count <= n_docs.
+ * Asynchronous on `stream`; must not overlap an ingestion batch. Errors:
+ * CC_ERR_INVALID_ARGUMENT, CC_ERR_DEVICE.
+ */
+CC_API cc_status cc_store_read(const cc_store *store, int64_t first, int64_t count,
+                               int64_t *author_out, void *rows_out, hipStream_t stream);
+
+/*
+ * cc_resolve_ids -- document id to store position (§6.3.1, Eq. 6): positions[i] = the
+ * position of doc_ids[i] in the store, or -1 when the id is not stored. The output is what
+ * cc_join / cc_join_batched take as cand_idx (a -1 there yields the defined invalid row).
+ *
+ *   store          a store from cc_store_create_indexed (else CC_ERR_NOT_SUPPORTED).
+ *   doc_ids        [n] int64 device, 8-byte aligned.
+ *   positions      [n] int64 device, 8-byte aligned; may be doc_ids itself (in place), must
+ *                  not overlap it otherwise.
+ * Asynchronous on `stream`; never allocates. Errors: CC_ERR_INVALID_ARGUMENT,
+ * CC_ERR_NOT_SUPPORTED, CC_ERR_DEVICE.
+ */
+CC_API cc_status cc_resolve_ids(const cc_store *store, const int64_t *doc_ids, int64_t n,
+                                int64_t *positions, hipStream_t stream);
 
 /*
  * cc_sort_affinity -- Alg. 1 Step 1 (§3.1) on the device: sort each viewer's affinity records

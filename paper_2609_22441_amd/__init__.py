@@ -1,4 +1,6 @@
-"""MI355X-native edge-feature join (Connected Content Retriever, §3.1 and §6.3).
+"""MI355X-native edge-feature join (Connected Content Retriever, §3.1 and §6.3), with the
+device sort of the affinity records (Alg. 1 Step 1), the document-id map (§6.3.1, Eq. 6) and
+ingestion into the store (§6.2).
 
 The work happens in ``libccjoin.so`` (hand-written HIP kernels for gfx950 behind the C ABI in
 ``include/cc_join.h``). This package is a thin ctypes binding with the same function names; it
@@ -10,4 +12,7 @@ from .binding import (  # noqa: F401
     cc_sort_affinity, cc_sort_workspace_bytes, cc_status_string,
     cc_store_create, cc_store_destroy, cc_store_info, cc_store_invalid_count,
     cc_store_reset_invalid_count, cc_validate_keys, lib, LIB_PATH, EXPORTS,
+    cc_store_create_indexed, cc_upsert_workspace_bytes, cc_store_upsert, cc_resolve_ids,
+    cc_store_read,
+    CC_ERR_STORE_FULL,
 )

@@ -17,11 +17,13 @@ EXPORTS = (
     "cc_store_create", "cc_store_destroy", "cc_store_info", "cc_store_invalid_count",
     "cc_store_reset_invalid_count", "cc_join", "cc_join_batched", "cc_join_batched_tuned",
     "cc_join_batched_padded", "cc_sort_workspace_bytes", "cc_sort_affinity",
+    "cc_store_create_indexed", "cc_upsert_workspace_bytes", "cc_store_upsert", "cc_store_read",
+    "cc_resolve_ids",
     "cc_validate_keys", "cc_status_string", "cc_last_device_error",
 )
 
 CC_OK, CC_ERR_INVALID_ARGUMENT, CC_ERR_OUT_OF_MEMORY, CC_ERR_DEVICE = 0, 1, 2, 3
-CC_ERR_UNSORTED_KEYS, CC_ERR_NOT_SUPPORTED = 4, 5
+CC_ERR_UNSORTED_KEYS, CC_ERR_NOT_SUPPORTED, CC_ERR_STORE_FULL = 4, 5, 6
 CC_SRC_HOST, CC_SRC_DEVICE = 1, 2
 
 
@@ -67,6 +69,10 @@ def lib():
             "cc_join_batched_padded": [vp, i32, vp, vp, i64, vp, vp, i64, vp, i32, vp, i32,
                                        ctypes.POINTER(vp), i64, vp, i64, vp, vp, vp],
             "cc_sort_affinity": [i32, vp, vp, vp, i32, i64, i64, vp, vp, vp, i64, vp],
+            "cc_store_create_indexed": [ctypes.POINTER(vp), i64, i32, vp],
+            "cc_store_upsert": [vp, i64, vp, vp, vp, vp, i64, P64, P64, vp],
+            "cc_resolve_ids": [vp, vp, i64, vp, vp],
+            "cc_store_read": [vp, i64, i64, vp, vp, vp],
             "cc_validate_keys": [vp, vp, i32, i64, P64, vp],
             "cc_status_string": [st],
             "cc_last_device_error": [],
@@ -78,6 +84,8 @@ def lib():
         L.cc_status_string.restype = ctypes.c_char_p
         L.cc_sort_workspace_bytes.argtypes = [i64, i32]
         L.cc_sort_workspace_bytes.restype = i64
+        L.cc_upsert_workspace_bytes.argtypes = [i64]
+        L.cc_upsert_workspace_bytes.restype = i64
         _lib = L
     return _lib
 
@@ -132,6 +140,43 @@ def cc_store_create(author_ids, doc_rows, stream=None) -> int:
                                  int(_prod(doc_rows.shape[1:])) * doc_rows.element_size(),
                                  flags, _stream(stream)), "cc_store_create")
     return h.value
+
+
+def cc_store_create_indexed(capacity: int, doc_row_bytes: int, stream=None) -> int:
+    """An empty store with a document-id map for `capacity` documents; returns its handle."""
+    h = ctypes.c_void_p()
+    _check(lib().cc_store_create_indexed(ctypes.byref(h), capacity, doc_row_bytes,
+                                         _stream(stream)), "cc_store_create_indexed")
+    return h.value
+
+
+def cc_upsert_workspace_bytes(n_records: int) -> int:
+    return lib().cc_upsert_workspace_bytes(n_records)
+
+
+def cc_store_upsert(store: int, doc_ids, author_ids, doc_rows, workspace, stream=None):
+    """Apply one ingestion batch (§6.2); returns (n_new, n_rejected). Synchronises the stream.
+    Raises CCError with status CC_ERR_STORE_FULL (store unchanged) when the batch does not fit."""
+    n = doc_ids.numel()
+    nn, nr = ctypes.c_int64(), ctypes.c_int64()
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().cc_store_upsert(store, n, _ptr(doc_ids), _ptr(author_ids), _ptr(doc_rows),
+                                 _ptr(workspace), ws_bytes, ctypes.byref(nn), ctypes.byref(nr),
+                                 _stream(stream)), "cc_store_upsert")
+    return nn.value, nr.value
+
+
+def cc_store_read(store: int, first: int, count: int, author_out=None, rows_out=None,
+                  stream=None) -> None:
+    """Copy positions [first, first + count) of the store into device buffers."""
+    _check(lib().cc_store_read(store, first, count, _ptr(author_out), _ptr(rows_out),
+                               _stream(stream)), "cc_store_read")
+
+
+def cc_resolve_ids(store: int, doc_ids, positions, stream=None) -> None:
+    """Eq. 6 (§6.3.1): positions[i] = store position of doc_ids[i], or -1."""
+    _check(lib().cc_resolve_ids(store, _ptr(doc_ids), doc_ids.numel(), _ptr(positions),
+                                _stream(stream)), "cc_resolve_ids")
 
 
 def cc_store_destroy(store: int) -> None:

@@ -10,7 +10,8 @@ PKG = Path(__file__).resolve().parent
 ROOT = PKG.parent
 CSRC = PKG / "csrc"
 LIB = PKG / "libccjoin.so"
-SOURCES = [CSRC / "cc_api.hip", CSRC / "join_kernels.hip", CSRC / "sort_kernels.hip"]
+SOURCES = [CSRC / "cc_api.hip", CSRC / "join_kernels.hip", CSRC / "sort_kernels.hip",
+           CSRC / "map_kernels.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

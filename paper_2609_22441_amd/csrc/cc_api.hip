@@ -13,11 +13,14 @@
 struct cc_store {
     int device;
     int64_t n_docs;
+    int64_t capacity;                // rows allocated (n_docs for a store without an id map)
     int32_t doc_row_bytes;
-    int64_t *d_author;               // [n_docs]
-    uint8_t *d_rows;                 // [n_docs][doc_row_bytes]
+    int64_t *d_author;               // [capacity]
+    uint8_t *d_rows;                 // [capacity][doc_row_bytes]
     unsigned long long *d_invalid;   // invalid-position counter
     uint8_t *d_zero;                 // ccj::kZeroRowBytes zero bytes, read in place of absent rows
+    ccj::MapEntry *d_map;            // document-id map, or null (store without ids)
+    int64_t map_groups;              // probe groups in d_map (a power of two)
 };
 
 namespace {
@@ -32,6 +35,11 @@ cc_status device_error(hipError_t e) {
 bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
 bool mul_ok(int64_t a, int64_t b, int64_t *r) { return !__builtin_mul_overflow(a, b, r); }
+
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return na > 0 && nb > 0 && x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
 
 // Keeps the store's device current for the duration of a call.
 class DeviceGuard {
@@ -162,6 +170,83 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
 
 extern "C" {
 
+namespace {
+
+// The current device, if it is a gfx950.
+cc_status current_gfx950(int *dev) {
+    hipError_t e = hipGetDevice(dev);
+    if (e != hipSuccess)
+        return e == hipErrorNoDevice ? CC_ERR_NOT_SUPPORTED : device_error(e);
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, *dev);
+    if (e != hipSuccess)
+        return device_error(e);
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return CC_ERR_NOT_SUPPORTED;
+    return CC_OK;
+}
+
+void free_store(cc_store *s) {
+    (void)hipFree(s->d_author);
+    (void)hipFree(s->d_rows);
+    (void)hipFree(s->d_invalid);
+    (void)hipFree(s->d_zero);
+    (void)hipFree(s->d_map);
+    delete s;
+}
+
+cc_status alloc_failure(cc_store *s, hipError_t err) {
+    free_store(s);
+    if (err == hipErrorOutOfMemory || err == hipErrorMemoryAllocation) {
+        g_last_device_error = (int)err;
+        (void)hipGetLastError();
+        return CC_ERR_OUT_OF_MEMORY;
+    }
+    return device_error(err);
+}
+
+// A store with room for `capacity` rows (and an id map when with_map), counters cleared.
+cc_status new_store(int64_t capacity, int32_t doc_row_bytes, bool with_map, hipStream_t stream,
+                    cc_store **out) {
+    int64_t row_total = 0, id_total = 0, map_total = 0;
+    const int64_t groups = with_map ? ccj::map_groups_for(capacity) : 0;
+    if (!mul_ok(capacity, doc_row_bytes, &row_total) || !mul_ok(capacity, 8, &id_total) ||
+        !mul_ok(groups, ccj::kGroup * (int64_t)sizeof(ccj::MapEntry), &map_total))
+        return CC_ERR_INVALID_ARGUMENT;
+    int dev = 0;
+    cc_status st = current_gfx950(&dev);
+    if (st != CC_OK)
+        return st;
+    cc_store *s = new (std::nothrow) cc_store();
+    if (!s)
+        return CC_ERR_OUT_OF_MEMORY;
+    s->device = dev;
+    s->capacity = capacity;
+    s->doc_row_bytes = doc_row_bytes;
+    s->map_groups = groups;
+    hipError_t e;
+    if ((e = hipMalloc(&s->d_author, (size_t)(id_total > 0 ? id_total : 256))) != hipSuccess)
+        return alloc_failure(s, e);
+    if ((e = hipMalloc(&s->d_rows, (size_t)(row_total > 0 ? row_total : 256))) != hipSuccess)
+        return alloc_failure(s, e);
+    if ((e = hipMalloc(&s->d_invalid, sizeof(unsigned long long))) != hipSuccess)
+        return alloc_failure(s, e);
+    if ((e = hipMalloc(&s->d_zero, ccj::kZeroRowBytes)) != hipSuccess)
+        return alloc_failure(s, e);
+    if (with_map && (e = hipMalloc(&s->d_map, (size_t)map_total)) != hipSuccess)
+        return alloc_failure(s, e);
+    if ((e = hipMemsetAsync(s->d_invalid, 0, sizeof(unsigned long long), stream)) != hipSuccess)
+        return alloc_failure(s, e);
+    if ((e = hipMemsetAsync(s->d_zero, 0, ccj::kZeroRowBytes, stream)) != hipSuccess)
+        return alloc_failure(s, e);
+    if (with_map && (e = ccj::launch_map_init(s->d_map, groups, stream)) != hipSuccess)
+        return alloc_failure(s, e);
+    *out = s;
+    return CC_OK;
+}
+
+}  // namespace
+
 cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *author_ids,
                           const void *doc_rows, int32_t doc_row_bytes, uint32_t flags,
                           hipStream_t stream) {
@@ -177,70 +262,145 @@ cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *a
     int64_t row_total = 0, id_total = 0;
     if (!mul_ok(n_docs, doc_row_bytes, &row_total) || !mul_ok(n_docs, 8, &id_total))
         return CC_ERR_INVALID_ARGUMENT;
-
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess)
-        return e == hipErrorNoDevice ? CC_ERR_NOT_SUPPORTED : device_error(e);
-    hipDeviceProp_t prop;
-    e = hipGetDeviceProperties(&prop, dev);
-    if (e != hipSuccess)
-        return device_error(e);
-    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
-        return CC_ERR_NOT_SUPPORTED;
-
-    cc_store *s = new (std::nothrow) cc_store();
-    if (!s)
-        return CC_ERR_OUT_OF_MEMORY;
-    s->device = dev;
+    cc_store *s = nullptr;
+    cc_status st = new_store(n_docs, doc_row_bytes, false, stream, &s);
+    if (st != CC_OK)
+        return st;
     s->n_docs = n_docs;
-    s->doc_row_bytes = doc_row_bytes;
-    auto fail = [&](hipError_t err) {
-        (void)hipFree(s->d_author);
-        (void)hipFree(s->d_rows);
-        (void)hipFree(s->d_invalid);
-        (void)hipFree(s->d_zero);
-        delete s;
-        if (err == hipErrorOutOfMemory || err == hipErrorMemoryAllocation) {
-            g_last_device_error = (int)err;
-            (void)hipGetLastError();
-            return CC_ERR_OUT_OF_MEMORY;
-        }
-        return device_error(err);
-    };
-    if ((e = hipMalloc(&s->d_author, (size_t)(id_total > 0 ? id_total : 256))) != hipSuccess)
-        return fail(e);
-    if ((e = hipMalloc(&s->d_rows, (size_t)(row_total > 0 ? row_total : 256))) != hipSuccess)
-        return fail(e);
-    if ((e = hipMalloc(&s->d_invalid, sizeof(unsigned long long))) != hipSuccess)
-        return fail(e);
-    if ((e = hipMalloc(&s->d_zero, ccj::kZeroRowBytes)) != hipSuccess)
-        return fail(e);
     const hipMemcpyKind kind = flags == CC_SRC_HOST ? hipMemcpyHostToDevice
                                                     : hipMemcpyDeviceToDevice;
+    hipError_t e;
     if (n_docs > 0) {
         if ((e = hipMemcpyAsync(s->d_author, author_ids, (size_t)id_total, kind, stream)) != hipSuccess)
-            return fail(e);
+            return alloc_failure(s, e);
         if ((e = hipMemcpyAsync(s->d_rows, doc_rows, (size_t)row_total, kind, stream)) != hipSuccess)
-            return fail(e);
+            return alloc_failure(s, e);
     }
-    if ((e = hipMemsetAsync(s->d_invalid, 0, sizeof(unsigned long long), stream)) != hipSuccess)
-        return fail(e);
-    if ((e = hipMemsetAsync(s->d_zero, 0, ccj::kZeroRowBytes, stream)) != hipSuccess)
-        return fail(e);
     *out_store = s;
     return CC_OK;
+}
+
+cc_status cc_store_create_indexed(cc_store **out_store, int64_t capacity, int32_t doc_row_bytes,
+                                  hipStream_t stream) {
+    if (!out_store)
+        return CC_ERR_INVALID_ARGUMENT;
+    *out_store = nullptr;
+    if (capacity < 0 || capacity > INT32_MAX || doc_row_bytes <= 0 || (doc_row_bytes & 15))
+        return CC_ERR_INVALID_ARGUMENT;
+    cc_store *s = nullptr;
+    cc_status st = new_store(capacity, doc_row_bytes, true, stream, &s);
+    if (st != CC_OK)
+        return st;
+    *out_store = s;
+    return CC_OK;
+}
+
+int64_t cc_upsert_workspace_bytes(int64_t n_records) {
+    return ccj::upsert_workspace_bytes(n_records);
+}
+
+cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc_ids,
+                          const int64_t *author_ids, const void *doc_rows, void *workspace,
+                          int64_t workspace_bytes, int64_t *n_new, int64_t *n_rejected,
+                          hipStream_t stream) {
+    if (!store || n_records < 0 || n_records > ccj::kMaxBatch)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (!store->d_map)
+        return CC_ERR_NOT_SUPPORTED;
+    if (n_new)
+        *n_new = 0;
+    if (n_rejected)
+        *n_rejected = 0;
+    if (n_records == 0)
+        return CC_OK;
+    const int64_t rb = store->doc_row_bytes;
+    if (!doc_ids || !author_ids || !doc_rows || !workspace)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (!aligned(doc_ids, 8) || !aligned(author_ids, 8) || !aligned(doc_rows, 16) ||
+        !aligned(workspace, 16))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (workspace_bytes < ccj::upsert_workspace_bytes(n_records))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (overlaps(workspace, workspace_bytes, doc_ids, n_records * 8) ||
+        overlaps(workspace, workspace_bytes, author_ids, n_records * 8) ||
+        overlaps(workspace, workspace_bytes, doc_rows, n_records * rb))
+        return CC_ERR_INVALID_ARGUMENT;
+    DeviceGuard guard(store->device);
+    hipError_t e = ccj::launch_upsert_claim(store->d_map, store->map_groups, doc_ids, n_records,
+                                            workspace, stream);
+    int64_t counts[3] = {0, 0, 0};
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(counts, ccj::upsert_counts(workspace, n_records), sizeof(counts),
+                           hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(stream);
+    if (e != hipSuccess)
+        return device_error(e);
+    const int64_t fresh = counts[0], rejected = counts[1], unplaced = counts[2];
+    if (unplaced > 0 || store->n_docs + fresh > store->capacity) {
+        e = ccj::launch_upsert_rollback(store->d_map, n_records, workspace, stream);
+        if (e == hipSuccess)
+            e = hipStreamSynchronize(stream);
+        return e == hipSuccess ? CC_ERR_STORE_FULL : device_error(e);
+    }
+    e = ccj::launch_upsert_apply(store->d_map, n_records, workspace, store->n_docs, author_ids,
+                                 doc_rows, store->doc_row_bytes, store->d_author, store->d_rows,
+                                 stream);
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(stream);
+    if (e != hipSuccess)
+        return device_error(e);
+    store->n_docs += fresh;
+    if (n_new)
+        *n_new = fresh;
+    if (n_rejected)
+        *n_rejected = rejected;
+    return CC_OK;
+}
+
+cc_status cc_store_read(const cc_store *store, int64_t first, int64_t count, int64_t *author_out,
+                        void *rows_out, hipStream_t stream) {
+    if (!store || first < 0 || count < 0 || first > store->n_docs || count > store->n_docs - first)
+        return CC_ERR_INVALID_ARGUMENT;
+    if ((author_out && !aligned(author_out, 8)) || (rows_out && !aligned(rows_out, 16)))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (count == 0)
+        return CC_OK;
+    DeviceGuard guard(store->device);
+    const int64_t rb = store->doc_row_bytes;
+    hipError_t e = hipSuccess;
+    if (author_out)
+        e = hipMemcpyAsync(author_out, store->d_author + first, (size_t)(count * 8),
+                           hipMemcpyDeviceToDevice, stream);
+    if (e == hipSuccess && rows_out)
+        e = hipMemcpyAsync(rows_out, store->d_rows + first * rb, (size_t)(count * rb),
+                           hipMemcpyDeviceToDevice, stream);
+    return e == hipSuccess ? CC_OK : device_error(e);
+}
+
+cc_status cc_resolve_ids(const cc_store *store, const int64_t *doc_ids, int64_t n,
+                         int64_t *positions, hipStream_t stream) {
+    if (!store || n < 0)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (!store->d_map)
+        return CC_ERR_NOT_SUPPORTED;
+    if (n == 0)
+        return CC_OK;
+    if (!doc_ids || !positions || !aligned(doc_ids, 8) || !aligned(positions, 8))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (doc_ids != positions && overlaps(doc_ids, n * 8, positions, n * 8))
+        return CC_ERR_INVALID_ARGUMENT;
+    DeviceGuard guard(store->device);
+    hipError_t e = ccj::launch_resolve(store->d_map, store->map_groups, doc_ids, n, positions,
+                                       stream);
+    return e == hipSuccess ? CC_OK : device_error(e);
 }
 
 cc_status cc_store_destroy(cc_store *store) {
     if (!store)
         return CC_OK;
     DeviceGuard guard(store->device);
-    (void)hipFree(store->d_author);
-    (void)hipFree(store->d_rows);
-    (void)hipFree(store->d_invalid);
-    (void)hipFree(store->d_zero);
-    delete store;
+    free_store(store);
     return CC_OK;
 }
 
@@ -344,12 +504,6 @@ int64_t cc_sort_workspace_bytes(int64_t total_keys, int32_t n_viewers) {
     return ccj::sort_workspace_bytes(total_keys, n_viewers);
 }
 
-namespace {
-bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
-    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
-    return na > 0 && nb > 0 && x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
-}
-}  // namespace
 
 cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
                            const void *rows_in, int32_t row_bytes, int64_t total_keys,
@@ -424,6 +578,7 @@ const char *cc_status_string(cc_status status) {
     case CC_ERR_DEVICE: return "CC_ERR_DEVICE";
     case CC_ERR_UNSORTED_KEYS: return "CC_ERR_UNSORTED_KEYS";
     case CC_ERR_NOT_SUPPORTED: return "CC_ERR_NOT_SUPPORTED";
+    case CC_ERR_STORE_FULL: return "CC_ERR_STORE_FULL";
     }
     return "CC_UNKNOWN_STATUS";
 }

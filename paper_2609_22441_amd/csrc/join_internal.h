@@ -66,4 +66,35 @@ hipError_t launch_validate_keys(const int64_t *key_offsets, const int64_t *keys,
                                 int32_t n_viewers, int64_t total_keys,
                                 unsigned long long *first_bad, hipStream_t stream);
 
+// ---- document-id map (id -> store position), open addressing over 64-byte groups ----
+
+struct MapEntry {
+    int64_t key;    // document id; kEmptyKey marks a free entry
+    int32_t pos;    // store position >= 0; while a batch is applied, -(3 + first record index)
+    int32_t aux;    // while a batch is applied: last record index with this id; else -1
+};
+static_assert(sizeof(MapEntry) == 16, "map entries are 16 bytes");
+constexpr int kGroup = 4;                        // entries per probe group (64 bytes)
+constexpr int64_t kEmptyKey = INT64_MIN;         // reserved: cannot be stored
+constexpr int32_t kNoPos = INT32_MIN;            // pos of a free entry
+constexpr int64_t kMaxBatch = (int64_t)1 << 30;  // records per ingestion batch
+
+// Probe groups for a store of `capacity` documents (load factor <= 1/2), a power of two.
+int64_t map_groups_for(int64_t capacity);
+hipError_t launch_map_init(MapEntry *map, int64_t n_groups, hipStream_t stream);
+hipError_t launch_resolve(const MapEntry *map, int64_t n_groups, const int64_t *ids, int64_t n,
+                          int64_t *pos, hipStream_t stream);
+
+// Ingestion batch in three parts: claim (map entries for every id, first/last occurrence,
+// ranks of the new ids, and the counts {n_new, n_rejected} at upsert_counts(ws, n)); then
+// either rollback (the batch does not fit) or apply (scatter rows, then commit the map).
+int64_t upsert_workspace_bytes(int64_t n);
+int64_t *upsert_counts(void *workspace, int64_t n);
+hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *ids, int64_t n,
+                               void *workspace, hipStream_t stream);
+hipError_t launch_upsert_rollback(MapEntry *map, int64_t n, void *workspace, hipStream_t stream);
+hipError_t launch_upsert_apply(MapEntry *map, int64_t n, void *workspace, int64_t n_old,
+                               const int64_t *author_in, const void *rows_in, int32_t row_bytes,
+                               int64_t *author, uint8_t *rows, hipStream_t stream);
+
 }  // namespace ccj

@@ -1,0 +1,408 @@
+// Document-id map on the device: H(id) -> store position (Connected Content Retriever §6.3.1,
+// Eq. 6) and the ingestion batch that maintains it (§6.2, bootstrap protocol).
+//
+// The paper keeps H as a CPU hash map because a GPU hash map would need rebuilds under tens
+// of thousands of upserts per second. Here the map is an open-addressing table in HBM sized
+// for a load factor of at most 1/2 of the store's capacity, so an upsert never rebuilds it:
+// new ids are placed with a compare-and-swap and stored ids are found in place.
+//
+// Layout: groups of kGroup 16-byte entries (64 bytes); an id probes groups h, h+1, ... from
+// its home group h = mix(id) mod n_groups and takes the first free entry. Entries are only
+// ever freed by the rollback of a batch that did not fit, and those entries were free before
+// the batch, so the occupied entries of a group always form a prefix and an id that is absent
+// is known to be absent at the first group with a free entry. Probing stops after
+// kMaxProbeGroups groups; an id that cannot be placed within that distance fails its batch.
+//
+// Ingestion batch of n records (§6.2: identify new vs. stored ids, prefix-sum positions for the
+// new ones, scatter rows, update the map only after the rows are written):
+//   claim:   every record finds or claims its id's entry; atomic maxima leave in the entry the
+//            first record index (pos = -(3 + i), only while the entry is pending) and the last
+//            record index (aux); an exclusive scan over "record i is the first occurrence of a
+//            new id" gives each new id its rank, in batch order.
+//   apply:   the last occurrence of every id copies its row and author id to the stored
+//            position or to n_old + rank; then the first occurrence commits pos and every
+//            record clears aux.
+//   rollback (batch does not fit): pending entries are freed again, aux is cleared.
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+#include "join_internal.h"
+
+namespace ccj {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kScanPer = 4;                          // flags per thread in the scan
+constexpr int kScanBlock = kThreads * kScanPer;      // flags per scan block
+constexpr uint64_t kMaxProbeGroups = 64;
+
+typedef unsigned int chunk_t __attribute__((ext_vector_type(4)));
+
+// SplitMix64 output function (Steele, Lea and Flood 2014; Vigna's constants): a bijective
+// 64-bit mixer, so that ids that differ in any bit spread over the groups.
+__device__ __forceinline__ uint64_t mix(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+    return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ int64_t load_key(const MapEntry *e) {
+    return __hip_atomic_load(&e->key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ int64_t grid_stride() { return (int64_t)gridDim.x * blockDim.x; }
+
+__device__ __forceinline__ int64_t global_id() {
+    return (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+}
+
+// Workspace: slot int64[n] | rank int32[n] | partial int32[blocks + 1] | counts int64[4].
+struct Ws {
+    int64_t *slot;
+    int32_t *rank;
+    int32_t *partial;
+    int64_t *counts;     // {n_new, n_rejected, n_unplaced, unused}
+    int64_t blocks;
+};
+
+int64_t round_up(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+Ws carve(void *workspace, int64_t n) {
+    uint8_t *w = static_cast<uint8_t *>(workspace);
+    Ws s;
+    s.blocks = (n + kScanBlock - 1) / kScanBlock;
+    s.slot = reinterpret_cast<int64_t *>(w);
+    w += round_up(n * 8);
+    s.rank = reinterpret_cast<int32_t *>(w);
+    w += round_up(n * 4);
+    s.partial = reinterpret_cast<int32_t *>(w);
+    w += round_up((s.blocks + 1) * 4);
+    s.counts = reinterpret_cast<int64_t *>(w);
+    return s;
+}
+
+__global__ void map_init_kernel(MapEntry *map, int64_t n_entries) {
+    for (int64_t i = global_id(); i < n_entries; i += grid_stride())
+        map[i] = MapEntry{kEmptyKey, kNoPos, -1};
+}
+
+// One query per quad of lanes: each lane reads one entry of the probed group (a quad reads the
+// group's 64 contiguous bytes) and the quad votes.
+__global__ __launch_bounds__(kThreads) void resolve_kernel(const MapEntry *__restrict__ map,
+                                                           uint64_t mask,
+                                                           const int64_t *__restrict__ ids,
+                                                           int64_t n, int64_t *__restrict__ pos) {
+    const int lane = threadIdx.x & 63;
+    const int sub = lane & (kGroup - 1);
+    const int quad0 = lane & ~(kGroup - 1);
+    const int64_t stride = grid_stride() / kGroup;
+    for (int64_t q = global_id() / kGroup; q < n; q += stride) {
+        const int64_t key = ids[q];
+        int64_t result = -1;
+        if (key != kEmptyKey) {
+            uint64_t g = mix((uint64_t)key) & mask;
+            for (uint64_t probe = 0; probe < kMaxProbeGroups && probe <= mask; ++probe) {
+                const MapEntry e = map[g * kGroup + sub];
+                const unsigned hit = (unsigned)(__ballot(e.key == key) >> quad0) & 0xF;
+                const unsigned emp = (unsigned)(__ballot(e.key == kEmptyKey) >> quad0) & 0xF;
+                if (hit) {
+                    const int32_t p = __shfl(e.pos, quad0 + __builtin_ctz(hit));
+                    result = p >= 0 ? p : -1;
+                    break;
+                }
+                if (emp)
+                    break;
+                g = (g + 1) & mask;
+            }
+        }
+        if (sub == 0)
+            pos[q] = result;
+    }
+}
+
+__global__ void counts_init_kernel(int64_t *counts) {
+    if (threadIdx.x < 4)
+        counts[threadIdx.x] = 0;
+}
+
+__global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t mask,
+                                                         const int64_t *__restrict__ ids,
+                                                         int64_t n, Ws w) {
+    for (int64_t i = global_id(); i < n; i += grid_stride()) {
+        const int64_t key = ids[i];
+        int64_t found = -1;
+        if (key == kEmptyKey) {
+            atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[1]), 1ULL);
+            w.slot[i] = -1;
+            continue;
+        }
+        uint64_t g = mix((uint64_t)key) & mask;
+        for (uint64_t probe = 0; probe < kMaxProbeGroups && probe <= mask && found < 0; ++probe) {
+            for (int e = 0; e < kGroup; ++e) {
+                MapEntry *m = map + g * kGroup + e;
+                int64_t k = load_key(m);
+                if (k == kEmptyKey) {
+                    k = (int64_t)atomicCAS(reinterpret_cast<unsigned long long *>(&m->key),
+                                           (unsigned long long)kEmptyKey,
+                                           (unsigned long long)key);
+                    if (k == kEmptyKey)
+                        k = key;                               // claimed by this record
+                }
+                if (k == key) {
+                    found = (int64_t)(g * kGroup + e);
+                    break;
+                }
+            }
+            g = (g + 1) & mask;
+        }
+        w.slot[i] = found;
+        if (found < 0) {
+            atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[2]), 1ULL);
+            continue;
+        }
+        atomicMax(&map[found].pos, -(3 + (int32_t)i));   // no effect on a stored entry (pos >= 0)
+        atomicMax(&map[found].aux, (int32_t)i);
+    }
+}
+
+// Record i is the first occurrence of an id that is new in this batch.
+__device__ __forceinline__ int32_t first_new(const MapEntry *map, const Ws &w, int64_t i) {
+    const int64_t s = w.slot[i];
+    return (s >= 0 && map[s].pos == -(3 + (int32_t)i)) ? 1 : 0;
+}
+
+__device__ __forceinline__ int32_t block_sum(int32_t v, int32_t *lds) {
+    // 64-lane reduction, then across the kThreads / 64 waves
+    for (int off = 32; off > 0; off >>= 1)
+        v += __shfl_down(v, off);
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0)
+        lds[wave] = v;
+    __syncthreads();
+    int32_t t = 0;
+    for (int k = 0; k < kThreads / 64; ++k)
+        t += lds[k];
+    return t;
+}
+
+__global__ __launch_bounds__(kThreads) void scan_reduce_kernel(const MapEntry *map, int64_t n,
+                                                               Ws w) {
+    __shared__ int32_t lds[kThreads / 64];
+    const int64_t base = (int64_t)blockIdx.x * kScanBlock;
+    int32_t v = 0;
+    for (int k = 0; k < kScanPer; ++k) {
+        const int64_t i = base + k * kThreads + threadIdx.x;
+        if (i < n)
+            v += first_new(map, w, i);
+    }
+    const int32_t t = block_sum(v, lds);
+    if (threadIdx.x == 0)
+        w.partial[blockIdx.x] = t;
+}
+
+// Exclusive scan of the block partials in place (one workgroup); the total goes to counts[0].
+__global__ __launch_bounds__(kThreads) void scan_partials_kernel(Ws w) {
+    __shared__ int32_t s[kThreads];
+    __shared__ int64_t carry;
+    const int tid = threadIdx.x;
+    if (tid == 0)
+        carry = 0;
+    __syncthreads();
+    for (int64_t b0 = 0; b0 < w.blocks; b0 += kThreads) {
+        const int64_t b = b0 + tid;
+        const int32_t x = b < w.blocks ? w.partial[b] : 0;
+        s[tid] = x;
+        __syncthreads();
+        for (int d = 1; d < kThreads; d <<= 1) {
+            const int32_t y = tid >= d ? s[tid - d] : 0;
+            __syncthreads();
+            s[tid] += y;
+            __syncthreads();
+        }
+        if (b < w.blocks)
+            w.partial[b] = (int32_t)(carry + s[tid] - x);
+        __syncthreads();
+        if (tid == kThreads - 1)
+            carry += s[tid];
+        __syncthreads();
+    }
+    if (tid == 0)
+        w.counts[0] = carry;
+}
+
+// rank[i] = number of first occurrences of new ids before record i.
+__global__ __launch_bounds__(kThreads) void scan_apply_kernel(const MapEntry *map, int64_t n,
+                                                              Ws w) {
+    __shared__ int32_t s[kThreads];
+    const int tid = threadIdx.x;
+    const int64_t base = (int64_t)blockIdx.x * kScanBlock + (int64_t)tid * kScanPer;
+    int32_t f[kScanPer];
+    int32_t v = 0;
+#pragma unroll
+    for (int k = 0; k < kScanPer; ++k) {
+        const int64_t i = base + k;
+        f[k] = i < n ? first_new(map, w, i) : 0;
+        v += f[k];
+    }
+    s[tid] = v;
+    __syncthreads();
+    for (int d = 1; d < kThreads; d <<= 1) {
+        const int32_t y = tid >= d ? s[tid - d] : 0;
+        __syncthreads();
+        s[tid] += y;
+        __syncthreads();
+    }
+    int32_t run = w.partial[blockIdx.x] + s[tid] - v;
+#pragma unroll
+    for (int k = 0; k < kScanPer; ++k) {
+        const int64_t i = base + k;
+        if (i < n)
+            w.rank[i] = run;
+        run += f[k];
+    }
+}
+
+__global__ void rollback_kernel(MapEntry *map, int64_t n, Ws w) {
+    for (int64_t i = global_id(); i < n; i += grid_stride()) {
+        const int64_t s = w.slot[i];
+        if (s < 0)
+            continue;
+        if (map[s].pos < 0) {                     // pending: claimed by this batch
+            map[s].key = kEmptyKey;
+            map[s].pos = kNoPos;
+        }
+        map[s].aux = -1;
+    }
+}
+
+// The last occurrence of each id writes its row (one 16-byte chunk per thread) and author id.
+__global__ __launch_bounds__(kThreads) void scatter_kernel(const MapEntry *map, int64_t n, Ws w,
+                                                           int64_t n_old,
+                                                           const int64_t *__restrict__ author_in,
+                                                           const chunk_t *__restrict__ rows_in,
+                                                           int32_t chunks,
+                                                           int64_t *__restrict__ author,
+                                                           chunk_t *__restrict__ rows) {
+    const int64_t total = n * chunks;
+    for (int64_t g = global_id(); g < total; g += grid_stride()) {
+        const int64_t i = g / chunks;
+        const int32_t q = (int32_t)(g - i * chunks);
+        const int64_t s = w.slot[i];
+        if (s < 0)
+            continue;
+        const MapEntry e = map[s];
+        if (e.aux != (int32_t)i)
+            continue;                             // a later record carries this id's row
+        const int64_t target = e.pos >= 0 ? (int64_t)e.pos : n_old + w.rank[-(int64_t)e.pos - 3];
+        rows[target * chunks + q] = rows_in[i * chunks + q];
+        if (q == 0)
+            author[target] = author_in[i];
+    }
+}
+
+__global__ void commit_kernel(MapEntry *map, int64_t n, Ws w, int64_t n_old) {
+    for (int64_t i = global_id(); i < n; i += grid_stride()) {
+        const int64_t s = w.slot[i];
+        if (s < 0)
+            continue;
+        if (map[s].pos == -(3 + (int32_t)i))      // only the id's first occurrence writes pos
+            map[s].pos = (int32_t)(n_old + w.rank[i]);
+        map[s].aux = -1;
+    }
+}
+
+unsigned grid_for(int64_t work, int64_t per_block) {
+    int64_t b = (work + per_block - 1) / per_block;
+    if (b < 1)
+        b = 1;
+    return (unsigned)(b < 65536 ? b : 65536);
+}
+
+}  // namespace
+
+int64_t map_groups_for(int64_t capacity) {
+    int64_t g = 64;
+    while (g * kGroup < 2 * capacity)
+        g <<= 1;
+    return g;
+}
+
+hipError_t launch_map_init(MapEntry *map, int64_t n_groups, hipStream_t stream) {
+    const int64_t n = n_groups * kGroup;
+    hipLaunchKernelGGL(map_init_kernel, dim3(grid_for(n, kThreads)), dim3(kThreads), 0, stream,
+                       map, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_resolve(const MapEntry *map, int64_t n_groups, const int64_t *ids, int64_t n,
+                          int64_t *pos, hipStream_t stream) {
+    if (n <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(resolve_kernel, dim3(grid_for(n * kGroup, kThreads)), dim3(kThreads), 0,
+                       stream, map, (uint64_t)(n_groups - 1), ids, n, pos);
+    return hipGetLastError();
+}
+
+int64_t upsert_workspace_bytes(int64_t n) {
+    if (n <= 0)
+        return 0;
+    const int64_t blocks = (n + kScanBlock - 1) / kScanBlock;
+    return round_up(n * 8) + round_up(n * 4) + round_up((blocks + 1) * 4) + 256;
+}
+
+int64_t *upsert_counts(void *workspace, int64_t n) { return carve(workspace, n).counts; }
+
+hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *ids, int64_t n,
+                               void *workspace, hipStream_t stream) {
+    const Ws w = carve(workspace, n);
+    const uint64_t mask = (uint64_t)(n_groups - 1);
+    hipLaunchKernelGGL(counts_init_kernel, dim3(1), dim3(64), 0, stream, w.counts);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || n <= 0)
+        return e;
+    hipLaunchKernelGGL(claim_kernel, dim3(grid_for(n, kThreads)), dim3(kThreads), 0, stream, map,
+                       mask, ids, n, w);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(scan_reduce_kernel, dim3((unsigned)w.blocks), dim3(kThreads), 0, stream,
+                       map, n, w);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(scan_partials_kernel, dim3(1), dim3(kThreads), 0, stream, w);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(scan_apply_kernel, dim3((unsigned)w.blocks), dim3(kThreads), 0, stream,
+                       map, n, w);
+    return hipGetLastError();
+}
+
+hipError_t launch_upsert_rollback(MapEntry *map, int64_t n, void *workspace, hipStream_t stream) {
+    if (n <= 0)
+        return hipSuccess;
+    const Ws w = carve(workspace, n);
+    hipLaunchKernelGGL(rollback_kernel, dim3(grid_for(n, kThreads)), dim3(kThreads), 0, stream,
+                       map, n, w);
+    return hipGetLastError();
+}
+
+hipError_t launch_upsert_apply(MapEntry *map, int64_t n, void *workspace, int64_t n_old,
+                               const int64_t *author_in, const void *rows_in, int32_t row_bytes,
+                               int64_t *author, uint8_t *rows, hipStream_t stream) {
+    if (n <= 0)
+        return hipSuccess;
+    const Ws w = carve(workspace, n);
+    const int32_t chunks = row_bytes / 16;
+    hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(n * chunks, kThreads)), dim3(kThreads), 0,
+                       stream, map, n, w, n_old, author_in,
+                       static_cast<const chunk_t *>(rows_in), chunks, author,
+                       reinterpret_cast<chunk_t *>(rows));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(commit_kernel, dim3(grid_for(n, kThreads)), dim3(kThreads), 0, stream, map,
+                       n, w, n_old);
+    return hipGetLastError();
+}
+
+}  // namespace ccj

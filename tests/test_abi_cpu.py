@@ -33,6 +33,7 @@ def test_status_strings():
     assert P.cc_status_string(0) == "CC_OK"
     assert P.cc_status_string(1) == "CC_ERR_INVALID_ARGUMENT"
     assert P.cc_status_string(5) == "CC_ERR_NOT_SUPPORTED"
+    assert P.cc_status_string(6) == "CC_ERR_STORE_FULL"
     assert P.cc_status_string(99) == "CC_UNKNOWN_STATUS"
     assert P.cc_last_device_error() == 0
 
@@ -118,6 +119,27 @@ def test_sort_rejects_bad_arguments():
     assert call(w=0x30000) == 1                  # workspace overlaps the output keys
     assert call(mk=-1) == 1                      # negative hint
     assert call(tk=0, kin=None, rin=None, kout=None, rout=None, w=None, wb=0) == 0   # no work
+
+
+def test_indexed_store_rejects_bad_arguments():
+    lib = B.lib()
+    h = ctypes.c_void_p(99)
+    assert lib.cc_store_create_indexed(None, 10, 16, None) == 1
+    assert lib.cc_store_create_indexed(ctypes.byref(h), -1, 16, None) == 1
+    assert h.value is None
+    assert lib.cc_store_create_indexed(ctypes.byref(h), 1 << 31, 16, None) == 1   # > INT32_MAX
+    assert lib.cc_store_create_indexed(ctypes.byref(h), 10, 24, None) == 1        # row width
+    assert lib.cc_store_create_indexed(ctypes.byref(h), 10, 0, None) == 1
+
+
+def test_upsert_and_resolve_reject_bad_arguments():
+    lib = B.lib()
+    n = ctypes.c_int64()
+    assert lib.cc_store_upsert(None, 1, 8, 8, 16, 16, 1 << 20, ctypes.byref(n), None, None) == 1
+    assert lib.cc_resolve_ids(None, 8, 1, 8, None) == 1
+    assert lib.cc_upsert_workspace_bytes(0) == 0
+    assert lib.cc_upsert_workspace_bytes(-3) == 0
+    assert lib.cc_upsert_workspace_bytes(1000) >= 12 * 1000
 
 
 def test_library_has_no_cpu_fallback(monkeypatch, tmp_path):

@@ -1,0 +1,290 @@
+"""GPU parity of the document-id map (§6.3.1, Eq. 6) and of ingestion batches (§6.2) against
+the oracle's map and sequential replay."""
+from __future__ import annotations
+
+import json
+from pathlib import Path
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_22441_amd as P
+import workload as W
+from gpu_common import FILL, gpu_join, note, oracle_join
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+GOLDEN = Path(__file__).resolve().parent / "golden"
+I64_MIN = -(1 << 63)
+
+
+class DeviceIndex:
+    """An indexed device store plus the oracle state it must equal."""
+
+    def __init__(self, capacity, row_bytes):
+        self.store = P.cc_store_create_indexed(capacity, row_bytes)
+        self.ref = oracle.IndexState(capacity, row_bytes)
+        self.rb = row_bytes
+
+    def upsert(self, ids, authors, rows):
+        """Apply one batch on both sides; returns the device result (or None when full)."""
+        ids, authors = torch.as_tensor(ids, dtype=torch.int64), torch.as_tensor(authors,
+                                                                               dtype=torch.int64)
+        rows = torch.as_tensor(rows)
+        ws = torch.empty(max(16, P.cc_upsert_workspace_bytes(ids.numel())), dtype=torch.uint8,
+                         device=DEV)
+        want = self.ref.upsert(ids.numpy(), authors.numpy(), oracle.as_bytes(rows))
+        try:
+            got = P.cc_store_upsert(self.store, ids.to(DEV), authors.to(DEV), rows.to(DEV), ws)
+        except P.CCError as e:
+            assert e.status == P.CC_ERR_STORE_FULL, e
+            got = None
+        assert got == want, f"upsert result {got} vs {want}"
+        return got
+
+    def check_state(self, what=""):
+        n, _ = P.cc_store_info(self.store)
+        assert n == self.ref.n_docs, f"{what}: n_docs {n} vs {self.ref.n_docs}"
+        a = torch.full((max(n, 1),), -7, dtype=torch.int64, device=DEV)
+        r = torch.full((max(n, 1), self.rb), FILL, dtype=torch.uint8, device=DEV)
+        P.cc_store_read(self.store, 0, n, a, r)
+        torch.cuda.synchronize()
+        assert np.array_equal(a.cpu().numpy()[:n], self.ref.author[:n]), f"{what}: authors"
+        assert np.array_equal(r.cpu().numpy()[:n], self.ref.rows[:n]), f"{what}: rows"
+
+    def resolve(self, q, what=""):
+        q = torch.as_tensor(q, dtype=torch.int64)
+        pos = torch.full_like(q, -7, device=DEV)
+        P.cc_resolve_ids(self.store, q.to(DEV), pos)
+        torch.cuda.synchronize()
+        want = self.ref.resolve(q.numpy())
+        assert np.array_equal(pos.cpu().numpy(), want), f"{what}: resolve"
+        return want
+
+    def close(self):
+        P.cc_store_destroy(self.store)
+
+
+def _gi(x):
+    return I64_MIN if x == "INT64_MIN" else int(x)
+
+
+def test_worked_example():
+    note("map: hand-worked ingestion example")
+    g = json.loads((GOLDEN / "upsert_worked.json").read_text())
+    ix = DeviceIndex(g["capacity"], g["row_bytes"])
+    try:
+        for k, bt in enumerate(g["batches"]):
+            rows = np.repeat(np.array(bt["row_fill"], np.uint8)[:, None], g["row_bytes"], 1)
+            got = ix.upsert([_gi(x) for x in bt["ids"]], bt["authors"], torch.from_numpy(rows))
+            if bt.get("fits", True):
+                assert got == (bt["n_new"], bt["n_rejected"]), f"batch {k}"
+            else:
+                assert got is None, f"batch {k}"
+            ix.check_state(f"batch {k}")
+        pos = ix.resolve([_gi(x) for x in g["resolve"]["queries"]], "golden")
+        assert pos.tolist() == g["resolve"]["positions"]
+    finally:
+        ix.close()
+
+
+@pytest.mark.parametrize("cap", [0, 1, 37, 1500, 70_000])
+def test_random_batches(cap):
+    """Batches mixing new ids, stored ids, repeats, the reserved id, empty batches and batches
+    that do not fit, compared with the sequential replay after every batch."""
+    note(f"map: random batches, capacity {cap}")
+    rng = np.random.default_rng(cap + 1)
+    ix = DeviceIndex(cap, 32)
+    universe = W.doc_ids(torch.arange(3 * cap + 50), 9).numpy()
+    universe[: min(4, len(universe))] = [(1 << 63) - 1, -1, 0, I64_MIN + 1][: min(4, len(universe))]
+    try:
+        for b in range(12):
+            m = int(rng.integers(0, max(2, cap // 3 + 40)))
+            pool = min(len(universe), 20 + (b + 1) * max(1, cap // 4))
+            ids = universe[rng.integers(0, pool, m)]
+            if m and b % 3 == 1:
+                ids[rng.integers(0, m, 2)] = I64_MIN
+            authors = rng.integers(-(1 << 60), 1 << 60, m)
+            rows = rng.integers(0, 256, (m, 32)).astype(np.uint8)
+            ix.upsert(ids, authors, torch.from_numpy(rows))
+            ix.check_state(f"cap {cap} batch {b}")
+            q = np.concatenate([universe[: pool + 10], [I64_MIN, 12345]])
+            ix.resolve(q, f"cap {cap} batch {b}")
+    finally:
+        ix.close()
+
+
+def test_full_store_is_unchanged_and_exact_fit_is_accepted():
+    note("map: store full, then exact fit")
+    ix = DeviceIndex(100, 16)
+    try:
+        ids = W.doc_ids(torch.arange(300), 4)
+        rows = torch.arange(300 * 16, dtype=torch.int64).to(torch.uint8).reshape(300, 16)
+        assert ix.upsert(ids[:60], torch.arange(60), rows[:60]) == (60, 0)
+        # 30 stored + 41 new: does not fit
+        mixed = torch.cat([ids[:30], ids[100:141]])
+        assert ix.upsert(mixed, torch.arange(71), rows[:71]) is None
+        ix.check_state("after the rejected batch")
+        ix.resolve(ids[:200], "after the rejected batch")
+        # 30 stored + 40 new: fills the store exactly
+        mixed = torch.cat([ids[100:140], ids[:30]])
+        assert ix.upsert(mixed, torch.arange(70), rows[:70]) == (40, 0)
+        ix.check_state("after the exact fit")
+        ix.resolve(ids[:200], "after the exact fit")
+        # updates only still fit a full store
+        stored = torch.cat([ids[:60], ids[100:140]]).flip(0)
+        assert ix.upsert(stored, torch.arange(100), rows[100:200]) == (0, 0)
+        ix.check_state("updates into a full store")
+    finally:
+        ix.close()
+
+
+def test_resolve_then_join_equals_oracle():
+    """Eq. 6 feeding Eq. 1: ids resolved on the device are the join's candidate positions."""
+    note("map: resolve then join")
+    spec = W.IndexSpec(200_000, 20_000, 64, torch.bfloat16, 3, 4000, 0.05, 0, 0.0, 0.0)
+    ix = DeviceIndex(spec.n_index, 128)
+    try:
+        ids, authors, rows = W.index_records(spec, torch.arange(spec.n_index), 6, 1, DEV)
+        ws = torch.empty(P.cc_upsert_workspace_bytes(spec.n_index), dtype=torch.uint8,
+                         device=DEV)
+        assert P.cc_store_upsert(ix.store, ids, authors, rows, ws) == (spec.n_index, 0)
+        q = W.resolve_queries(spec, spec.n_index, 6, DEV)
+        pos = torch.empty_like(q)
+        P.cc_resolve_ids(ix.store, q, pos)
+        want_pos = oracle.resolve(ids.cpu(), q.cpu())
+        assert np.array_equal(pos.cpu().numpy(), want_pos), "resolve"
+        # a batch of 3 viewers over the resolved candidates
+        g = W.gen(DEV, 6, 2)
+        co = torch.arange(0, 3 * 4000 + 1, 4000, device=DEV)
+        keys = torch.sort(torch.randperm(spec.n_authors, generator=g, device=DEV)[:3 * 1500]
+                          .view(3, 1500), dim=1).values.reshape(-1)
+        ko = torch.arange(0, 3 * 1500 + 1, 1500, device=DEV)
+        edge = torch.randn(3 * 1500, 32, generator=g, device=DEV).to(torch.bfloat16)
+        batch = W.Batch(co, pos, ko, keys, edge, None)
+        got = gpu_join(ix.store, None, batch, 128, 64, 1)
+        want = oracle_join(authors.cpu(), rows.cpu(), batch.to("cpu"), 1)
+        assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1]), "join"
+        # in-place resolve
+        P.cc_resolve_ids(ix.store, q, q)
+        torch.cuda.synchronize()
+        assert np.array_equal(q.cpu().numpy(), want_pos), "in-place resolve"
+    finally:
+        ix.close()
+
+
+@pytest.mark.timeout(300)
+def test_full_size_index_sampled():
+    """The 200M-document index of the benchmark: built by ingestion in large batches, every
+    stored id resolves to its item index (the replay gives item i position i when items arrive
+    in order without repeats); then one ingestion batch of the benchmark's mix is checked on
+    its counts and on sampled rows and positions."""
+    spec = W.INDEX_CONFIG
+    n = spec.n_index
+    note(f"map: full-size index, {n} documents")
+    store = P.cc_store_create_indexed(n + 4 * spec.upsert_batch, 128)
+    try:
+        step = 25_000_000
+        ws = torch.empty(P.cc_upsert_workspace_bytes(step), dtype=torch.uint8, device=DEV)
+        for first in range(0, n, step):
+            ids, authors, rows = W.index_records(spec, torch.arange(first, first + step,
+                                                                    device=DEV), 1, 100, DEV)
+            assert P.cc_store_upsert(store, ids, authors, rows, ws) == (step, 0)
+            del ids, authors, rows
+        assert P.cc_store_info(store)[0] == n
+        g = W.gen(DEV, 1, 7)
+        items = torch.randint(0, n, (1_000_000,), generator=g, device=DEV)
+        q = W.doc_ids(items, 1)
+        pos = torch.empty_like(q)
+        P.cc_resolve_ids(store, q, pos)
+        assert torch.equal(pos, items), "stored ids resolve to their positions"
+        absent = W.doc_ids(n + torch.arange(100_000, device=DEV), 1)
+        P.cc_resolve_ids(store, absent, absent)
+        assert bool((absent == -1).all()), "absent ids resolve to -1"
+        # one ingestion batch of the benchmark's mix
+        ids, authors, rows, n_new = W.upsert_batch(spec, n, n, 1, 30, DEV)
+        wsb = torch.empty(P.cc_upsert_workspace_bytes(ids.numel()), dtype=torch.uint8,
+                          device=DEV)
+        got = P.cc_store_upsert(store, ids, authors, rows, wsb)
+        ic = ids.cpu().numpy()
+        uniq, first = np.unique(ic, return_index=True)
+        assert got[1] == 0
+        # new ids are exactly the ids of items >= n (ids are a bijection of item indices);
+        # in-batch repeats can drop some of the fresh items, so count those present
+        fresh_ids = W.doc_ids(torch.arange(n, n + n_new), 1).numpy()
+        want_new = int(np.isin(fresh_ids, ic).sum())
+        assert got[0] == want_new, f"new ids {got[0]} vs {want_new}"
+        # positions of the fresh ids follow their first appearance in the batch
+        fi = fresh_ids[np.isin(fresh_ids, ic)]
+        order = np.argsort([first[np.searchsorted(uniq, x)] for x in fi], kind="stable")
+        qd = torch.from_numpy(fi[order]).to(DEV)
+        pos = torch.empty_like(qd)
+        P.cc_resolve_ids(store, qd, pos)
+        assert torch.equal(pos.cpu(), torch.arange(n, n + want_new)), "fresh positions"
+        # sampled rows: each id's row is its last record's row
+        last = len(ic) - 1 - np.unique(ic[::-1], return_index=True)[1]
+        pick = last[np.random.default_rng(0).integers(0, len(last), 2000)]
+        qd = ids[torch.from_numpy(pick).to(DEV)]
+        pos = torch.empty_like(qd)
+        P.cc_resolve_ids(store, qd, pos)
+        a = torch.empty(1, dtype=torch.int64, device=DEV)
+        r = torch.empty(1, 128, dtype=torch.uint8, device=DEV)
+        rows_u8 = rows.view(torch.uint8).reshape(rows.shape[0], -1)
+        pos_c = pos.cpu().tolist()
+        for k, p in enumerate(pos_c[:200]):
+            P.cc_store_read(store, p, 1, a, r)
+            assert int(a) == int(authors[pick[k]]), "sampled author"
+            assert torch.equal(r[0], rows_u8[pick[k]]), "sampled row"
+    finally:
+        P.cc_store_destroy(store)
+
+
+def test_concurrent_resolves_on_two_streams():
+    note("map: concurrent resolves")
+    spec = W.IndexSpec(50_000, 1000, 8, torch.bfloat16, 2, 20_000, 0.1, 0, 0.0, 0.0)
+    ix = DeviceIndex(spec.n_index, 16)
+    try:
+        ids, authors, rows = W.index_records(spec, torch.arange(spec.n_index), 2, 1, DEV)
+        ws = torch.empty(P.cc_upsert_workspace_bytes(spec.n_index), dtype=torch.uint8,
+                         device=DEV)
+        assert P.cc_store_upsert(ix.store, ids, authors, rows, ws)[0] == spec.n_index
+        q1 = W.resolve_queries(spec, spec.n_index, 1, DEV)
+        q2 = W.resolve_queries(spec, spec.n_index, 2, DEV)
+        p1, p2 = torch.empty_like(q1), torch.empty_like(q2)
+        s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+        torch.cuda.synchronize()
+        for _ in range(5):
+            P.cc_resolve_ids(ix.store, q1, p1, stream=s1)
+            P.cc_resolve_ids(ix.store, q2, p2, stream=s2)
+        torch.cuda.synchronize()
+        ic = ids.cpu()
+        assert np.array_equal(p1.cpu().numpy(), oracle.resolve(ic, q1.cpu()))
+        assert np.array_equal(p2.cpu().numpy(), oracle.resolve(ic, q2.cpu()))
+    finally:
+        ix.close()
+
+
+def test_argument_errors_on_device():
+    note("map: argument errors")
+    st = P.cc_store_create(torch.zeros(4, dtype=torch.int64, device=DEV),
+                           torch.zeros(4, 16, dtype=torch.uint8, device=DEV))
+    try:
+        q = torch.zeros(3, dtype=torch.int64, device=DEV)
+        with pytest.raises(P.CCError) as e:
+            P.cc_resolve_ids(st, q, q)
+        assert e.value.status == 5                     # a store without an id map
+    finally:
+        P.cc_store_destroy(st)
+    ix = DeviceIndex(10, 16)
+    try:
+        ids = torch.arange(3, dtype=torch.int64, device=DEV)
+        small = torch.empty(8, dtype=torch.uint8, device=DEV)
+        with pytest.raises(P.CCError):                 # workspace too small
+            P.cc_store_upsert(ix.store, ids, ids, torch.zeros(3, 16, dtype=torch.uint8,
+                                                               device=DEV), small)
+        with pytest.raises(P.CCError):                 # read past n_docs
+            P.cc_store_read(ix.store, 0, 1, ids, None)
+    finally:
+        ix.close()

@@ -27,6 +27,14 @@ Recipe (every draw comes from a ``torch.Generator`` seeded with
   are concatenated and shuffled. Duplicate candidates are allowed.
 * actor keys (second lookup): half of the candidates carry an actor drawn uniformly from the
   viewer's keys, the other half carry -1 ("no actor").
+* document ids (id map and ingestion, §6.3.1 and §6.2): item i has the id
+  ``((i * A) mod 2^62) xor salt(seed)`` with A odd, a bijection on [0, 2^62), so ids are
+  distinct and never the reserved INT64_MIN. The index holds items [0, n_index). A resolve
+  batch has ``batch`` requests of ``ids_per_request`` ids; a share ``miss_rate`` are items past
+  the index (absent), the rest uniform over stored items. An ingestion batch draws a share
+  ``new_rate`` of new items (fresh indices), the rest uniform over stored items, then a share
+  ``repeat_rate`` of its records repeat another record's id; the order is shuffled. Author
+  ids are uniform over ``[0, n_authors)``, rows N(0,1) rounded to the row dtype.
 """
 from __future__ import annotations
 
@@ -39,6 +47,7 @@ import torch
 __all__ = [
     "StoreSpec", "RequestSpec", "CONFIGS", "Store", "Request", "Batch",
     "gen", "make_store", "make_requests", "pack", "salt_special_values", "config",
+    "IndexSpec", "INDEX_CONFIG", "doc_ids", "index_records", "resolve_queries", "upsert_batch",
 ]
 
 
@@ -411,3 +420,73 @@ def tiny_case(seed: int, device="cpu", max_docs=48, max_k=40, max_n=64, max_view
         tc = TinyCase(author.to(device), doc.to(device), batch.to(device),
                       None if default is None else default.to(device), n_lookups)
     return tc
+
+
+# ---- document ids: the id map (§6.3.1, Eq. 6) and ingestion batches (§6.2) ----
+
+@dataclass(frozen=True)
+class IndexSpec:
+    n_index: int            # documents in the index (items [0, n_index))
+    n_authors: int
+    row_cols: int
+    row_dtype: torch.dtype
+    batch: int              # requests per resolve batch (the paper's b)
+    ids_per_request: int    # candidate ids per request ("tens of thousands")
+    miss_rate: float        # share of query ids not in the index
+    upsert_batch: int       # records per ingestion batch
+    new_rate: float         # share of an ingestion batch's records with new ids
+    repeat_rate: float      # share of records repeating another record's id in the batch
+
+
+# The one-shard index of the largest store shape (200M documents with 64 bf16 columns); resolve
+# batches of b = 8 requests x 50,000 ids (§6.3.1 quotes batch 8 with tens of thousands of ids
+# per request against a few-hundred-million-entry index); ingestion batches of 300,000 records
+# (§6.2: bootstrap batches of hundreds of thousands of documents).
+INDEX_CONFIG = IndexSpec(200_000_000, 50_000_000, 64, BF16, 8, 50_000, 0.02, 300_000, 0.2, 0.05)
+
+_ID_MASK = (1 << 62) - 1
+_ID_MULT = 0x2545F4914F6CDD1D & _ID_MASK       # odd
+
+
+def doc_ids(items: torch.Tensor, seed: int) -> torch.Tensor:
+    """Distinct document ids for item indices (int64 tensor, any device)."""
+    salt = (seed * 0x9E3779B97F4A7C15 + 0x632BE59BD9B4E019) & _ID_MASK
+    return ((items * _ID_MULT) & _ID_MASK) ^ salt
+
+
+def index_records(spec: IndexSpec, items: torch.Tensor, seed: int, stream: int, device="cpu"):
+    """(doc ids, author ids, rows) for the given item indices."""
+    g = gen(device, seed, stream)
+    n = items.numel()
+    ids = doc_ids(items.to(device), seed)
+    authors = torch.randint(0, spec.n_authors, (n,), generator=g, device=device)
+    rows = torch.randn(n, spec.row_cols, generator=g, device=device).to(spec.row_dtype)
+    return ids, authors, rows
+
+
+def resolve_queries(spec: IndexSpec, n_stored: int, seed: int, device="cpu") -> torch.Tensor:
+    """[batch * ids_per_request] query ids: stored items, and a share of absent ones."""
+    g = gen(device, seed, 11)
+    m = spec.batch * spec.ids_per_request
+    items = torch.randint(0, max(n_stored, 1), (m,), generator=g, device=device)
+    miss = torch.rand(m, generator=g, device=device) < spec.miss_rate
+    absent = n_stored + torch.randint(0, 1 << 40, (m,), generator=g, device=device)
+    return doc_ids(torch.where(miss | (n_stored == 0), absent, items), seed)
+
+
+def upsert_batch(spec: IndexSpec, n_stored: int, next_item: int, seed: int, stream: int,
+                 device="cpu", n: Optional[int] = None):
+    """One ingestion batch: (ids, authors, rows, n_fresh_items). Fresh items are
+    [next_item, next_item + n_fresh_items); the caller advances next_item by that much."""
+    g = gen(device, seed, stream)
+    n = spec.upsert_batch if n is None else n
+    n_new = int(round(n * spec.new_rate)) if n_stored > 0 else n
+    items = torch.cat([torch.arange(next_item, next_item + n_new, device=device),
+                       torch.randint(0, max(n_stored, 1), (n - n_new,), generator=g,
+                                     device=device)])
+    rep = torch.nonzero(torch.rand(n, generator=g, device=device) < spec.repeat_rate).flatten()
+    if n > 0 and rep.numel():
+        items[rep] = items[torch.randint(0, n, (rep.numel(),), generator=g, device=device)]
+    items = items[torch.randperm(n, generator=g, device=device)]
+    ids, authors, rows = index_records(spec, items, seed, stream + 1, device)
+    return ids, authors, rows, n_new

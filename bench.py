@@ -173,6 +173,71 @@ def all_configs(torch, P, W, dev, seed):
                        "hbm_frac_of_peak": alg / (med / 1e3) / 1e9 / PEAK_GBPS}
         del out, hit, b, reqs
         torch.cuda.empty_cache()
+    res.update(index_workloads(torch, P, W, dev, seed))
+    return res
+
+
+def index_workloads(torch, P, W, dev, seed):
+    """The document-id map (§6.3.1, Eq. 6) and ingestion (§6.2) on the one-shard index: build it
+    by ingestion, resolve b x tens-of-thousands ids, and apply ingestion batches."""
+    import time
+    spec = W.INDEX_CONFIG
+    n = spec.n_index
+    rb = spec.row_cols * 2
+    n_batches = 20
+    res = {}
+    store = P.cc_store_create_indexed(n + n_batches * spec.upsert_batch, rb)
+    step = 25_000_000
+    ws = torch.empty(P.cc_upsert_workspace_bytes(step), dtype=torch.uint8, device=dev)
+    t_build = 0.0
+    for first in range(0, n, step):
+        ids, authors, rows = W.index_records(spec, torch.arange(first, first + step, device=dev),
+                                             seed, 100, dev)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        P.cc_store_upsert(store, ids, authors, rows, ws)
+        t_build += time.perf_counter() - t0
+        del ids, authors, rows
+    del ws
+    res["index-build"] = {"entry": "cc_store_upsert", "documents": n, "batch": step,
+                          "seconds": t_build, "records_per_s": n / t_build}
+    # Eq. 6: b requests x ids_per_request ids, 2% absent
+    q = W.resolve_queries(spec, n, seed, dev)
+    pos = torch.empty_like(q)
+    med, mean = time_launches(torch, lambda: P.cc_resolve_ids(store, q, pos), 200)
+    m = q.numel()
+    alg = m * (8 + 8 + 64)            # id in, position out, one 64-byte probe group
+    res["resolve"] = {"entry": "cc_resolve_ids", "index": n, "ids": m, "requests": spec.batch,
+                      "ms_median": med, "ms_mean": mean, "ids_per_s": m / (med / 1e3),
+                      "algorithmic_bytes": alg, "hbm_gbps": alg / (med / 1e3) / 1e9,
+                      "hbm_frac_of_peak": alg / (med / 1e3) / 1e9 / PEAK_GBPS}
+    # §6.2 ingestion: bootstrap-size batches, then steady-state batches (a third of the size)
+    next_item = n
+    for tag, size, count in (("upsert", spec.upsert_batch, 10),
+                             ("upsert-steady", spec.upsert_batch // 3, 10)):
+        wsb = torch.empty(P.cc_upsert_workspace_bytes(size), dtype=torch.uint8, device=dev)
+        times, fresh = [], 0
+        for k in range(count):
+            n_stored = P.cc_store_info(store)[0]
+            ids, authors, rows, n_new = W.upsert_batch(spec, n_stored, next_item, seed,
+                                                       200 + 2 * k + (0 if tag == "upsert" else 50),
+                                                       dev, n=size)
+            next_item += n_new
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            got = P.cc_store_upsert(store, ids, authors, rows, wsb)
+            times.append(time.perf_counter() - t0)
+            fresh += got[0]
+            del ids, authors, rows
+        times.sort()
+        med = times[len(times) // 2]
+        alg = size * (8 + 8 + rb + 16 + 12) + size * (rb + 8)   # read in + map, write rows
+        res[tag] = {"entry": "cc_store_upsert", "records": size, "batches": count,
+                    "new_ids": fresh, "ms_median": med * 1e3, "records_per_s": size / med,
+                    "algorithmic_bytes": alg, "hbm_gbps": alg / med / 1e9,
+                    "note": "host wall clock per call, including its two stream synchronisations"}
+    P.cc_store_destroy(store)
+    torch.cuda.empty_cache()
     return res
 
 

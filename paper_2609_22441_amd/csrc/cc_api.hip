@@ -111,7 +111,14 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
         !aligned(cand_idx, 8) || !aligned(edge_keys, 8) || !aligned(cand_offsets, 8) ||
         !aligned(key_offsets, 8) || !aligned(extra, 8))
         return CC_ERR_INVALID_ARGUMENT;
-    int32_t lds_cap = ccj::kDefaultLdsKeys, stride = 0, wgs = 0;
+    int32_t lds_cap = ccj::kDefaultLdsKeys, stride = 0, wgs = 0, budget = 4;
+    bool one_wave = false;
+    const int64_t viewers = cand_offsets ? n_viewers : 1;
+    if (viewers > 0 && total_keys / viewers > ccj::kLongListKeys) {
+        lds_cap = ccj::kMaxLdsKeys;
+        budget = 16;
+        one_wave = true;
+    }
     if (tuning) {
         if (tuning->fence_stride < 0 || tuning->lds_keys < 0 || tuning->workgroups < 0 ||
             tuning->lds_keys > ccj::kMaxLdsKeys || tuning->workgroups > (1 << 30))
@@ -153,6 +160,8 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
     a.invalid_counter = store->d_invalid;
     a.n_viewers = cand_offsets ? n_viewers : 1;
     a.fence_stride = stride;
+    a.fence_budget = budget;
+    a.one_wave = one_wave;
     // The LDS table never needs more entries than the largest viewer has keys.
     a.lds_keys = (int32_t)(total_keys < lds_cap ? (total_keys > 0 ? total_keys : 1) : lds_cap);
 

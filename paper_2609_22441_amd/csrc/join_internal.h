@@ -11,6 +11,10 @@ constexpr int kWindow = 15;          // keys between two fences read from L2 in 
 constexpr int kMaxLdsKeys = 18432;   // LDS key table limit: 144 KiB + at most 12 KiB of static
                                      // tables stays within the 160 KiB a workgroup may use
 constexpr int kDefaultLdsKeys = 8192;   // 64 KiB: within the register-limited occupancy
+// Average key-list length above which a launch uses the whole LDS table, one resident wave of
+// workgroups (one per CU) and a larger fence budget: staging more fences per workgroup keeps
+// each lookup's window of keys within one 64-byte sector.
+constexpr int64_t kLongListKeys = 4 * (int64_t)kDefaultLdsKeys;
 constexpr int kZeroRowBytes = 1024;    // >= the widest row of a compile-time specialisation
 
 struct JoinArgs {
@@ -37,6 +41,8 @@ struct JoinArgs {
     int32_t n_viewers;
     int32_t lds_keys;            // capacity of the dynamic LDS key table
     int32_t fence_stride;        // 0 = chosen per viewer segment
+    int32_t fence_budget;        // fences staged per candidate of a segment (automatic stride)
+    bool one_wave;               // automatic grid: one resident wave, not 1.5
     int32_t n_wg;                // workgroups launched (a multiple of 8); set by launch_join
     int64_t per_wg;              // candidates per workgroup (multiple of kBlock); set by launch_join
 };

@@ -121,8 +121,8 @@ __device__ __forceinline__ int64_t find_key(int64_t x, const int64_t *tab, int64
 // Fence stride for one segment: the smallest power of two whose fence count fits the LDS
 // table and is not much larger than the number of candidates that will use it.
 __device__ __forceinline__ int choose_stride(int64_t K, int64_t seg_len, int32_t cap,
-                                             int32_t forced) {
-    int64_t budget = forced > 0 ? cap : min<int64_t>(cap, max<int64_t>(512, 4 * seg_len));
+                                             int32_t forced, int32_t per_cand) {
+    int64_t budget = forced > 0 ? cap : min<int64_t>(cap, max<int64_t>(512, per_cand * seg_len));
     int S = forced > 0 ? forced : 1;
     while ((K + S - 1) / S > budget)
         S <<= 1;
@@ -401,7 +401,7 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
 
         const int64_t K = ke - kb;
         const int64_t *gk = a.keys + kb;
-        const int S = choose_stride(K, s1 - s0, a.lds_keys, a.fence_stride);
+        const int S = choose_stride(K, s1 - s0, a.lds_keys, a.fence_stride, a.fence_budget);
         const int64_t M = (K + S - 1) / S;
         // Stage the fences into LDS (after the previous segment's readers are done). Full
         // segments stage after issuing their first loads, so the two latencies overlap.
@@ -491,12 +491,16 @@ hipError_t launch_one(JoinArgs &a, int32_t workgroups, int device, hipStream_t s
     if (err != hipSuccess)
         return err;
     // Grid: about 1.5 resident waves of workgroups (a slight oversubscription lets early
-    // finishers take the remaining ranges), each owning a contiguous range of whole
-    // sub-tiles, rounded to a multiple of 8 so that each XCD gets an equal share.
+    // finishers take the remaining ranges), or exactly one wave for long key lists, each
+    // owning a contiguous range of whole sub-tiles, rounded to a multiple of 8 so that each
+    // XCD gets an equal share.
     const int64_t tiles = (a.total_cand + kBlock - 1) / kBlock;
     int64_t n_wg = workgroups;
-    if (n_wg <= 0)
-        n_wg = (int64_t)cu_count(device) * resident_per_cu(fn, lds) * 3 / 2;
+    if (n_wg <= 0) {
+        n_wg = (int64_t)cu_count(device) * resident_per_cu(fn, lds);
+        if (!a.one_wave)
+            n_wg = n_wg * 3 / 2;
+    }
     if (n_wg > tiles)
         n_wg = tiles;
     if (n_wg < 1)

@@ -29,8 +29,8 @@ namespace ccj {
 namespace {
 
 constexpr int kTile = 4096;                       // records per tile
-constexpr int kThreads = 256;                     // threads per workgroup
-constexpr int kEpt = kTile / kThreads;            // records per thread (16)
+constexpr int kThreads = 512;                     // threads per workgroup
+constexpr int kEpt = kTile / kThreads;            // records per thread (8)
 constexpr int kLdsElems = kTile + kTile / kEpt;   // padded LDS tile
 
 typedef unsigned int chunk_t __attribute__((ext_vector_type(4)));
@@ -177,7 +177,7 @@ __device__ __forceinline__ void emit(const Elem *s, int n, int64_t pos, Elem *__
     }
     for (int i = tid; i < n; i += kThreads)
         keys_out[pos + i] = s[pidx(i)].key;
-    constexpr int U = 4;
+    constexpr int U = 8;
     const int n_chunks = n * row_chunks;
     for (int g0 = tid; g0 < n_chunks; g0 += U * kThreads) {
         chunk_t c[U];

@@ -274,8 +274,9 @@ CC_API cc_status cc_store_create_indexed(cc_store **out_store, int64_t capacity,
  *                  aligned, caller-owned, not overlapping the inputs.
  *   n_new, n_rejected  host outputs (may be NULL): ids added, records skipped.
  *
- * Synchronises `stream` (twice: after the new ids are counted, and at the end). When the new
- * ids do not fit in the remaining capacity, or an id cannot be placed within the map's probe
+ * Synchronises `stream` once, at the end (whether the batch fits is decided on the device, and
+ * the rows, the map or the rollback are all enqueued before the wait). When the new ids do not
+ * fit in the remaining capacity, or an id cannot be placed within the map's probe
  * limit (64 groups; not expected below load 1/2), the batch is undone and CC_ERR_STORE_FULL is
  * returned with the store unchanged. Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_NOT_SUPPORTED,
  * CC_ERR_STORE_FULL, CC_ERR_DEVICE.

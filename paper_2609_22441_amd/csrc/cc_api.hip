@@ -337,6 +337,11 @@ cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc
     DeviceGuard guard(store->device);
     hipError_t e = ccj::launch_upsert_claim(store->d_map, store->map_groups, doc_ids, n_records,
                                             workspace, stream);
+    if (e == hipSuccess)
+        e = ccj::launch_upsert_finish(store->d_map, n_records, workspace, store->n_docs,
+                                      store->capacity, author_ids, doc_rows,
+                                      store->doc_row_bytes, store->d_author, store->d_rows,
+                                      stream);
     int64_t counts[3] = {0, 0, 0};
     if (e == hipSuccess)
         e = hipMemcpyAsync(counts, ccj::upsert_counts(workspace, n_records), sizeof(counts),
@@ -346,19 +351,8 @@ cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc
     if (e != hipSuccess)
         return device_error(e);
     const int64_t fresh = counts[0], rejected = counts[1], unplaced = counts[2];
-    if (unplaced > 0 || store->n_docs + fresh > store->capacity) {
-        e = ccj::launch_upsert_rollback(store->d_map, n_records, workspace, stream);
-        if (e == hipSuccess)
-            e = hipStreamSynchronize(stream);
-        return e == hipSuccess ? CC_ERR_STORE_FULL : device_error(e);
-    }
-    e = ccj::launch_upsert_apply(store->d_map, n_records, workspace, store->n_docs, author_ids,
-                                 doc_rows, store->doc_row_bytes, store->d_author, store->d_rows,
-                                 stream);
-    if (e == hipSuccess)
-        e = hipStreamSynchronize(stream);
-    if (e != hipSuccess)
-        return device_error(e);
+    if (unplaced > 0 || store->n_docs + fresh > store->capacity)
+        return CC_ERR_STORE_FULL;            // rolled back on the device: the store is unchanged
     store->n_docs += fresh;
     if (n_new)
         *n_new = fresh;

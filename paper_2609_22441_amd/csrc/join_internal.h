@@ -91,16 +91,18 @@ hipError_t launch_map_init(MapEntry *map, int64_t n_groups, hipStream_t stream);
 hipError_t launch_resolve(const MapEntry *map, int64_t n_groups, const int64_t *ids, int64_t n,
                           int64_t *pos, hipStream_t stream);
 
-// Ingestion batch in three parts: claim (map entries for every id, first/last occurrence,
-// ranks of the new ids, and the counts {n_new, n_rejected} at upsert_counts(ws, n)); then
-// either rollback (the batch does not fit) or apply (scatter rows, then commit the map).
+// Ingestion batch in two launches: claim (map entries for every id, first/last occurrence,
+// ranks of the new ids, and the counts {n_new, n_rejected, n_unplaced} at
+// upsert_counts(ws, n)), then finish: when the batch fits (nothing unplaced and
+// n_old + n_new <= capacity) scatter the rows and commit the map, otherwise roll the claim
+// back. The decision is taken on the device from the counts.
 int64_t upsert_workspace_bytes(int64_t n);
 int64_t *upsert_counts(void *workspace, int64_t n);
 hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *ids, int64_t n,
                                void *workspace, hipStream_t stream);
-hipError_t launch_upsert_rollback(MapEntry *map, int64_t n, void *workspace, hipStream_t stream);
-hipError_t launch_upsert_apply(MapEntry *map, int64_t n, void *workspace, int64_t n_old,
-                               const int64_t *author_in, const void *rows_in, int32_t row_bytes,
-                               int64_t *author, uint8_t *rows, hipStream_t stream);
+hipError_t launch_upsert_finish(MapEntry *map, int64_t n, void *workspace, int64_t n_old,
+                                int64_t capacity, const int64_t *author_in, const void *rows_in,
+                                int32_t row_bytes, int64_t *author, uint8_t *rows,
+                                hipStream_t stream);
 
 }  // namespace ccj

@@ -23,6 +23,9 @@
 //            position or to n_old + rank; then the first occurrence commits pos and every
 //            record clears aux.
 //   rollback (batch does not fit): pending entries are freed again, aux is cleared.
+// Whether the batch fits (every id placed, n_old + n_new <= capacity) is decided on the device
+// from the claim's counts: apply and rollback are both enqueued and each does nothing unless
+// it is the one that applies, so a batch needs a single synchronisation at its end.
 #include <stdint.h>
 
 #include <hip/hip_runtime.h>
@@ -263,7 +266,14 @@ __global__ __launch_bounds__(kThreads) void scan_apply_kernel(const MapEntry *ma
     }
 }
 
-__global__ void rollback_kernel(MapEntry *map, int64_t n, Ws w) {
+// The batch fits: every id was placed and the new ids fit in the remaining capacity.
+__device__ __forceinline__ bool batch_fits(const Ws &w, int64_t n_old, int64_t capacity) {
+    return w.counts[2] == 0 && n_old + w.counts[0] <= capacity;
+}
+
+__global__ void rollback_kernel(MapEntry *map, int64_t n, Ws w, int64_t n_old, int64_t capacity) {
+    if (batch_fits(w, n_old, capacity))
+        return;
     for (int64_t i = global_id(); i < n; i += grid_stride()) {
         const int64_t s = w.slot[i];
         if (s < 0)
@@ -278,12 +288,14 @@ __global__ void rollback_kernel(MapEntry *map, int64_t n, Ws w) {
 
 // The last occurrence of each id writes its row (one 16-byte chunk per thread) and author id.
 __global__ __launch_bounds__(kThreads) void scatter_kernel(const MapEntry *map, int64_t n, Ws w,
-                                                           int64_t n_old,
+                                                           int64_t n_old, int64_t capacity,
                                                            const int64_t *__restrict__ author_in,
                                                            const chunk_t *__restrict__ rows_in,
                                                            int32_t chunks,
                                                            int64_t *__restrict__ author,
                                                            chunk_t *__restrict__ rows) {
+    if (!batch_fits(w, n_old, capacity))
+        return;
     const int64_t total = n * chunks;
     for (int64_t g = global_id(); g < total; g += grid_stride()) {
         const int64_t i = g / chunks;
@@ -301,7 +313,9 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const MapEntry *map, 
     }
 }
 
-__global__ void commit_kernel(MapEntry *map, int64_t n, Ws w, int64_t n_old) {
+__global__ void commit_kernel(MapEntry *map, int64_t n, Ws w, int64_t n_old, int64_t capacity) {
+    if (!batch_fits(w, n_old, capacity))
+        return;
     for (int64_t i = global_id(); i < n; i += grid_stride()) {
         const int64_t s = w.slot[i];
         if (s < 0)
@@ -377,31 +391,27 @@ hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *i
     return hipGetLastError();
 }
 
-hipError_t launch_upsert_rollback(MapEntry *map, int64_t n, void *workspace, hipStream_t stream) {
-    if (n <= 0)
-        return hipSuccess;
-    const Ws w = carve(workspace, n);
-    hipLaunchKernelGGL(rollback_kernel, dim3(grid_for(n, kThreads)), dim3(kThreads), 0, stream,
-                       map, n, w);
-    return hipGetLastError();
-}
-
-hipError_t launch_upsert_apply(MapEntry *map, int64_t n, void *workspace, int64_t n_old,
-                               const int64_t *author_in, const void *rows_in, int32_t row_bytes,
-                               int64_t *author, uint8_t *rows, hipStream_t stream) {
+hipError_t launch_upsert_finish(MapEntry *map, int64_t n, void *workspace, int64_t n_old,
+                                int64_t capacity, const int64_t *author_in, const void *rows_in,
+                                int32_t row_bytes, int64_t *author, uint8_t *rows,
+                                hipStream_t stream) {
     if (n <= 0)
         return hipSuccess;
     const Ws w = carve(workspace, n);
     const int32_t chunks = row_bytes / 16;
     hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(n * chunks, kThreads)), dim3(kThreads), 0,
-                       stream, map, n, w, n_old, author_in,
+                       stream, map, n, w, n_old, capacity, author_in,
                        static_cast<const chunk_t *>(rows_in), chunks, author,
                        reinterpret_cast<chunk_t *>(rows));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
     hipLaunchKernelGGL(commit_kernel, dim3(grid_for(n, kThreads)), dim3(kThreads), 0, stream, map,
-                       n, w, n_old);
+                       n, w, n_old, capacity);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(rollback_kernel, dim3(grid_for(n, kThreads)), dim3(kThreads), 0, stream,
+                       map, n, w, n_old, capacity);
     return hipGetLastError();
 }
 

@@ -52,12 +52,12 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(torch, st, batch, wd, we, n_lookups=1):
-    """Bytes the method must move for one launch: per candidate its position, author id, doc
-    row, output row, hit bytes and (second lookup) its extra key; per viewer its keys and each
-    distinct edge row that some lookup hits."""
+def algorithmic_bytes(torch, st, batch, wd, we, n_lookups=1, author_bytes=8):
+    """Bytes the method must move for one launch: per candidate its position, author id (as
+    wide as the store keeps it: 4 or 8 bytes), doc row, output row, hit bytes and (second lookup)
+    its extra key; per viewer its keys and each distinct edge row that some lookup hits."""
     n = batch.cand_idx.numel()
-    per_cand = 8 + 8 + wd + (wd + n_lookups * we) + n_lookups + 8 * (n_lookups - 1)
+    per_cand = 8 + author_bytes + wd + (wd + n_lookups * we) + n_lookups + 8 * (n_lookups - 1)
     keys_bytes = batch.keys.numel() * 8
     co, ko = batch.cand_offsets.tolist(), batch.key_offsets.tolist()
     rows = 0
@@ -105,8 +105,8 @@ def all_configs(torch, P, W, dev, seed):
         L = 2 if r.actor else 1
         wd = st.doc_rows.shape[1] * st.doc_rows.element_size()
         we = r.edge_cols * b.edge_rows.element_size()
-        alg = algorithmic_bytes(torch, st, b, wd, we, L)
         store = P.cc_store_create(st.author_id, st.doc_rows)
+        alg = algorithmic_bytes(torch, st, b, wd, we, L, P.cc_store_layout(store)[0])
         if i == 5:
             st._by_author = None
             del st
@@ -309,7 +309,8 @@ def main():
     total = batches[0][1].cand_idx.numel()
     out = torch.empty(total, wd + we, dtype=torch.uint8, device=dev)
     hit = torch.empty(total, 1, dtype=torch.int8, device=dev)
-    alg = [algorithmic_bytes(torch, st, b, wd, we) for _, b in batches]
+    author_bytes = P.cc_store_layout(store)[0]
+    alg = [algorithmic_bytes(torch, st, b, wd, we, 1, author_bytes) for _, b in batches]
     torch.cuda.synchronize()
 
     def step(i):

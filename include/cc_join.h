@@ -71,13 +71,16 @@ typedef enum cc_status {
  *   doc_rows       [n_docs][doc_row_bytes] row-major document-feature rows.
  *   doc_row_bytes  bytes per row; a positive multiple of 16.
  *   flags          CC_SRC_HOST (sources are host memory) or CC_SRC_DEVICE (device memory).
- *   stream         the copies are enqueued on this stream; the sources must stay valid until
- *                  it has completed them. The store is usable by work later on the same stream
- *                  (other streams must wait for it).
+ *   stream         the copies are enqueued on this stream, which is synchronised once before
+ *                  the call returns (to learn whether every author id fits in 32 bits); the
+ *                  sources may be freed afterwards.
  *
  * The store is created on the current HIP device and stays on it. Layout in HBM: author ids
  * as one int64 column, rows as one row-major array, both 256-byte aligned, plus an 8-byte
- * counter of invalid candidate positions seen by joins.
+ * counter of invalid candidate positions seen by joins. When every author id fits in 32 bits
+ * the store also keeps a 32-bit copy of the author column, which the joins read instead
+ * (cc_store_layout reports it): the join's random author reads then touch half as many
+ * 64-byte sectors. Results never depend on it.
  * Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_OUT_OF_MEMORY (nothing leaked), CC_ERR_DEVICE,
  * CC_ERR_NOT_SUPPORTED.
  */
@@ -91,6 +94,17 @@ CC_API cc_status cc_store_destroy(cc_store *store);
 
 /* Report a store's size. Either output pointer may be NULL. */
 CC_API cc_status cc_store_info(const cc_store *store, int64_t *n_docs, int32_t *doc_row_bytes);
+
+/*
+ * cc_store_layout -- how a store holds its author ids and how many documents it can hold.
+ *   author_id_bytes  4 when every stored author id fits in 32 bits (the store then keeps a
+ *                    32-bit copy of the column, which the joins read: a 64-byte sector holds 16
+ *                    ids instead of 8), else 8.
+ *   capacity         rows allocated (n_docs for a store from cc_store_create).
+ * Either output may be NULL. Errors: CC_ERR_INVALID_ARGUMENT.
+ */
+CC_API cc_status cc_store_layout(const cc_store *store, int32_t *author_id_bytes,
+                                 int64_t *capacity);
 
 /* Read the number of invalid candidate positions (outside [0, n_docs)) that joins on this
  * store have met since creation or the last reset. Synchronises `stream` (debug/metrics). */

@@ -18,6 +18,7 @@ EXPORTS = (
     "cc_store_reset_invalid_count", "cc_join", "cc_join_batched", "cc_join_batched_tuned",
     "cc_join_batched_padded", "cc_sort_workspace_bytes", "cc_sort_affinity",
     "cc_store_create_indexed", "cc_upsert_workspace_bytes", "cc_store_upsert", "cc_store_read",
+    "cc_store_layout",
     "cc_resolve_ids",
     "cc_validate_keys", "cc_status_string", "cc_last_device_error",
 )
@@ -73,6 +74,7 @@ def lib():
             "cc_store_upsert": [vp, i64, vp, vp, vp, vp, i64, P64, P64, vp],
             "cc_resolve_ids": [vp, vp, i64, vp, vp],
             "cc_store_read": [vp, i64, i64, vp, vp, vp],
+            "cc_store_layout": [vp, ctypes.POINTER(i32), P64],
             "cc_validate_keys": [vp, vp, i32, i64, P64, vp],
             "cc_status_string": [st],
             "cc_last_device_error": [],
@@ -187,6 +189,13 @@ def cc_store_info(store: int):
     n, w = ctypes.c_int64(), ctypes.c_int32()
     _check(lib().cc_store_info(store, ctypes.byref(n), ctypes.byref(w)), "cc_store_info")
     return n.value, w.value
+
+
+def cc_store_layout(store: int):
+    """(author id bytes the joins read: 4 or 8, capacity)."""
+    b, c = ctypes.c_int32(), ctypes.c_int64()
+    _check(lib().cc_store_layout(store, ctypes.byref(b), ctypes.byref(c)), "cc_store_layout")
+    return b.value, c.value
 
 
 def cc_store_invalid_count(store: int, stream=None) -> int:

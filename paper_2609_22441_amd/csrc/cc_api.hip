@@ -16,6 +16,8 @@ struct cc_store {
     int64_t capacity;                // rows allocated (n_docs for a store without an id map)
     int32_t doc_row_bytes;
     int64_t *d_author;               // [capacity]
+    int32_t *d_author32;             // [capacity] the same ids in 32 bits, or null
+    bool compact;                    // every stored author id fits in 32 bits: joins read d_author32
     uint8_t *d_rows;                 // [capacity][doc_row_bytes]
     unsigned long long *d_invalid;   // invalid-position counter
     uint8_t *d_zero;                 // ccj::kZeroRowBytes zero bytes, read in place of absent rows
@@ -139,6 +141,7 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
 
     ccj::JoinArgs a;
     a.author = store->d_author;
+    a.author32 = store->compact ? store->d_author32 : nullptr;
     a.doc = store->d_rows;
     a.n_docs = store->n_docs;
     a.doc_bytes = store->doc_row_bytes;
@@ -197,6 +200,7 @@ cc_status current_gfx950(int *dev) {
 
 void free_store(cc_store *s) {
     (void)hipFree(s->d_author);
+    (void)hipFree(s->d_author32);
     (void)hipFree(s->d_rows);
     (void)hipFree(s->d_invalid);
     (void)hipFree(s->d_zero);
@@ -244,6 +248,12 @@ cc_status new_store(int64_t capacity, int32_t doc_row_bytes, bool with_map, hipS
         return alloc_failure(s, e);
     if (with_map && (e = hipMalloc(&s->d_map, (size_t)map_total)) != hipSuccess)
         return alloc_failure(s, e);
+    if (with_map) {
+        // Ingestion keeps the 32-bit author column next to the 64-bit one while every id fits.
+        if ((e = hipMalloc(&s->d_author32, (size_t)(capacity > 0 ? capacity * 4 : 256))) != hipSuccess)
+            return alloc_failure(s, e);
+        s->compact = true;
+    }
     if ((e = hipMemsetAsync(s->d_invalid, 0, sizeof(unsigned long long), stream)) != hipSuccess)
         return alloc_failure(s, e);
     if ((e = hipMemsetAsync(s->d_zero, 0, ccj::kZeroRowBytes, stream)) != hipSuccess)
@@ -284,6 +294,30 @@ cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *a
             return alloc_failure(s, e);
         if ((e = hipMemcpyAsync(s->d_rows, doc_rows, (size_t)row_total, kind, stream)) != hipSuccess)
             return alloc_failure(s, e);
+        // Keep a 32-bit copy of the author column when every id fits: the join's random author
+        // reads then touch half as many 64-byte sectors.
+        if ((e = hipMalloc(&s->d_author32, (size_t)(n_docs * 4))) != hipSuccess)
+            return alloc_failure(s, e);
+        unsigned long long *d_wide = nullptr;
+        unsigned long long wide = 1;
+        if ((e = hipMalloc(&d_wide, sizeof(unsigned long long))) != hipSuccess)
+            return alloc_failure(s, e);
+        e = hipMemsetAsync(d_wide, 0, sizeof(unsigned long long), stream);
+        if (e == hipSuccess)
+            e = ccj::launch_narrow_authors(s->d_author, s->d_author32, n_docs, d_wide, stream);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(&wide, d_wide, sizeof(wide), hipMemcpyDeviceToHost, stream);
+        if (e == hipSuccess)
+            e = hipStreamSynchronize(stream);
+        (void)hipFree(d_wide);
+        if (e != hipSuccess)
+            return alloc_failure(s, e);
+        if (wide == 0) {
+            s->compact = true;
+        } else {
+            (void)hipFree(s->d_author32);
+            s->d_author32 = nullptr;
+        }
     }
     *out_store = s;
     return CC_OK;
@@ -340,9 +374,9 @@ cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc
     if (e == hipSuccess)
         e = ccj::launch_upsert_finish(store->d_map, n_records, workspace, store->n_docs,
                                       store->capacity, author_ids, doc_rows,
-                                      store->doc_row_bytes, store->d_author, store->d_rows,
-                                      stream);
-    int64_t counts[3] = {0, 0, 0};
+                                      store->doc_row_bytes, store->d_author, store->d_author32,
+                                      store->d_rows, stream);
+    int64_t counts[4] = {0, 0, 0, 0};
     if (e == hipSuccess)
         e = hipMemcpyAsync(counts, ccj::upsert_counts(workspace, n_records), sizeof(counts),
                            hipMemcpyDeviceToHost, stream);
@@ -354,6 +388,8 @@ cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc
     if (unplaced > 0 || store->n_docs + fresh > store->capacity)
         return CC_ERR_STORE_FULL;            // rolled back on the device: the store is unchanged
     store->n_docs += fresh;
+    if (counts[3] > 0)
+        store->compact = false;              // an author id wider than 32 bits arrived
     if (n_new)
         *n_new = fresh;
     if (n_rejected)
@@ -414,6 +450,16 @@ cc_status cc_store_info(const cc_store *store, int64_t *n_docs, int32_t *doc_row
         *n_docs = store->n_docs;
     if (doc_row_bytes)
         *doc_row_bytes = store->doc_row_bytes;
+    return CC_OK;
+}
+
+cc_status cc_store_layout(const cc_store *store, int32_t *author_id_bytes, int64_t *capacity) {
+    if (!store)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (author_id_bytes)
+        *author_id_bytes = store->compact ? 4 : 8;
+    if (capacity)
+        *capacity = store->capacity;
     return CC_OK;
 }
 

@@ -19,6 +19,7 @@ constexpr int kZeroRowBytes = 1024;    // >= the widest row of a compile-time sp
 
 struct JoinArgs {
     const int64_t *author;       // store: author id per position
+    const int32_t *author32;     // store: the same ids narrowed to 32 bits, or nullptr
     const uint8_t *doc;          // store: rows, doc_bytes each
     int64_t n_docs;
     int32_t doc_bytes;
@@ -72,6 +73,11 @@ hipError_t launch_validate_keys(const int64_t *key_offsets, const int64_t *keys,
                                 int32_t n_viewers, int64_t total_keys,
                                 unsigned long long *first_bad, hipStream_t stream);
 
+// Narrow an author column to 32 bits: dst[i] = (int32_t)src[i]; *wide counts the ids outside
+// the int32 range (dst is then not usable).
+hipError_t launch_narrow_authors(const int64_t *src, int32_t *dst, int64_t n,
+                                 unsigned long long *wide, hipStream_t stream);
+
 // ---- document-id map (id -> store position), open addressing over 64-byte groups ----
 
 struct MapEntry {
@@ -92,7 +98,7 @@ hipError_t launch_resolve(const MapEntry *map, int64_t n_groups, const int64_t *
                           int64_t *pos, hipStream_t stream);
 
 // Ingestion batch in two launches: claim (map entries for every id, first/last occurrence,
-// ranks of the new ids, and the counts {n_new, n_rejected, n_unplaced} at
+// ranks of the new ids, and the counts {n_new, n_rejected, n_unplaced, n_wide_authors} at
 // upsert_counts(ws, n)), then finish: when the batch fits (nothing unplaced and
 // n_old + n_new <= capacity) scatter the rows and commit the map, otherwise roll the claim
 // back. The decision is taken on the device from the counts.
@@ -102,7 +108,7 @@ hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *i
                                void *workspace, hipStream_t stream);
 hipError_t launch_upsert_finish(MapEntry *map, int64_t n, void *workspace, int64_t n_old,
                                 int64_t capacity, const int64_t *author_in, const void *rows_in,
-                                int32_t row_bytes, int64_t *author, uint8_t *rows,
-                                hipStream_t stream);
+                                int32_t row_bytes, int64_t *author, int32_t *author32,
+                                uint8_t *rows, hipStream_t stream);
 
 }  // namespace ccj

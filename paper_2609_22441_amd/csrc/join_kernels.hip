@@ -129,6 +129,18 @@ __device__ __forceinline__ int choose_stride(int64_t K, int64_t seg_len, int32_t
     return S;
 }
 
+// Author id of a store position: from the 32-bit column when the store has one (every id fits
+// in 32 bits, so a 64-byte sector holds 16 ids instead of 8), else from the 64-bit column. The
+// column is a compile-time choice: a branch in the prefetch would split the pipeline's basic
+// blocks and cost more than the narrower reads save.
+template <bool A32>
+__device__ __forceinline__ int64_t author_of(const JoinArgs &a, int64_t c) {
+    if constexpr (A32)
+        return (int64_t)a.author32[c];
+    else
+        return a.author[c];
+}
+
 __device__ __forceinline__ int64_t range_index(int b, int n) {
     const int per_xcd = n >> 3;
     return (int64_t)(b & 7) * per_xcd + (b >> 3);
@@ -292,7 +304,7 @@ __device__ __forceinline__ void resolve_tile(const JoinArgs &a, int64_t *src,
 // so that the loop body has no branch. All loads are unconditional from clamped indices: a
 // load under a branch, or a second path into the loop latch, would leave the compiler unable
 // to count outstanding loads, and it would then wait for every store of a sub-tile first.
-template <int DOC_CH, int EDGE_CH, int NL, typename Stage>
+template <int DOC_CH, int EDGE_CH, int NL, bool A32, typename Stage>
 __device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t (*s_src)[kBlock],
                                            int64_t (*s_row)[NL][kBlock],
                                            unsigned int *s_invalid, const int64_t *s_tab,
@@ -316,8 +328,8 @@ __device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t (*s_src)[k
     {
         const int64_t c0 = a.cand_idx[base(0) + tid];
         const int64_t e0 = extra(0);
-        const int64_t x0 = a.author[clamp64(c0, last_doc)];
-        x1 = a.author[clamp64(c1, last_doc)];
+        const int64_t x0 = author_of<A32>(a, clamp64(c0, last_doc));
+        x1 = author_of<A32>(a, clamp64(c1, last_doc));
         stage();
         resolve_tile<NL>(a, s_src[0], s_row[0], s_invalid, s_tab, M, S, gk, K, kb, base(0),
                          shift, fresh(0), c0, x0, e0);
@@ -335,7 +347,7 @@ __device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t (*s_src)[k
                                  kb, base(k + 1), shift, fresh(k + 1), c1, x1, e1);
                 const int64_t c3 = a.cand_idx[base(k + 3) + tid];
                 const int64_t e2 = extra(k + 2);
-                const int64_t x2 = a.author[clamp64(c2, last_doc)];
+                const int64_t x2 = author_of<A32>(a, clamp64(c2, last_doc));
                 c1 = c2;
                 c2 = c3;
                 x1 = x2;
@@ -347,7 +359,7 @@ __device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t (*s_src)[k
 
 // BATCHED selects the CSR form (viewer offsets in device memory); the single-viewer form has
 // one implicit viewer and skips the offset lookups.
-template <int DOC_CH, int EDGE_CH, int NL, bool BATCHED>
+template <int DOC_CH, int EDGE_CH, int NL, bool BATCHED, bool A32>
 __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
     extern __shared__ int64_t s_tab[];            // fence table, a.lds_keys entries
     __shared__ int64_t s_src[2][kBlock];          // doc position of each sub-tile row, or -1
@@ -413,7 +425,7 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
         const int64_t seg = s1 - s0;
         if constexpr (DOC_CH > 0) {
             if (seg >= kBlock) {
-                full_tiles<DOC_CH, EDGE_CH, NL>(a, s_src, s_row, &s_invalid, s_tab, M, S, gk, K,
+                full_tiles<DOC_CH, EDGE_CH, NL, A32>(a, s_src, s_row, &s_invalid, s_tab, M, S, gk, K,
                                                 kb, s0, s1, shift, miss_row, stage);
                 continue;
             }
@@ -426,7 +438,7 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
             if (tid < n) {
                 const int64_t c = a.cand_idx[t0 + tid];
                 const bool ok = c >= 0 && c < a.n_docs;
-                const int64_t x0 = ok ? a.author[c] : 0;
+                const int64_t x0 = ok ? author_of<A32>(a, c) : 0;
                 const int64_t x1 = NL == 2 ? a.extra[t0 + tid] : 0;
                 resolve_tile<NL>(a, s_src[0], s_row[0], &s_invalid, s_tab, M, S, gk, K, kb, t0,
                                  shift, 0, c, x0, x1);
@@ -474,13 +486,13 @@ int resident_per_cu(const void *fn, size_t lds) {
     return n;
 }
 
-template <int D, int E, int L, bool BATCHED>
+template <int D, int E, int L, bool BATCHED, bool A32>
 hipError_t launch_one(JoinArgs &a, int32_t workgroups, int device, hipStream_t stream) {
     // The largest LDS table plus the kernel's static tables must fit a workgroup's 160 KiB.
     static_assert(kMaxLdsKeys * sizeof(int64_t) + (2 + 2 * L) * kBlock * sizeof(int64_t) +
                           sizeof(unsigned int) <= 160 * 1024,
                   "LDS budget exceeded");
-    const void *fn = reinterpret_cast<const void *>(&join_kernel<D, E, L, BATCHED>);
+    const void *fn = reinterpret_cast<const void *>(&join_kernel<D, E, L, BATCHED, A32>);
     const size_t lds = (size_t)max(1, a.lds_keys) * sizeof(int64_t);
     static std::once_flag lds_limit;
     hipError_t err = hipSuccess;
@@ -510,15 +522,18 @@ hipError_t launch_one(JoinArgs &a, int32_t workgroups, int device, hipStream_t s
     n_wg = (a.total_cand + a.per_wg - 1) / a.per_wg;
     n_wg = (n_wg + 7) & ~int64_t(7);
     a.n_wg = (int32_t)n_wg;
-    hipLaunchKernelGGL((join_kernel<D, E, L, BATCHED>), dim3(a.n_wg), dim3(kBlock), lds, stream,
+    hipLaunchKernelGGL((join_kernel<D, E, L, BATCHED, A32>), dim3(a.n_wg), dim3(kBlock), lds, stream,
                        a);
     return hipGetLastError();
 }
 
 template <int D, int E, int L>
 hipError_t launch_form(JoinArgs &a, int32_t wgs, int device, hipStream_t stream) {
-    return a.cand_offsets ? launch_one<D, E, L, true>(a, wgs, device, stream)
-                          : launch_one<D, E, L, false>(a, wgs, device, stream);
+    if (a.author32)
+        return a.cand_offsets ? launch_one<D, E, L, true, true>(a, wgs, device, stream)
+                              : launch_one<D, E, L, false, true>(a, wgs, device, stream);
+    return a.cand_offsets ? launch_one<D, E, L, true, false>(a, wgs, device, stream)
+                          : launch_one<D, E, L, false, false>(a, wgs, device, stream);
 }
 
 template <int L>

@@ -65,7 +65,7 @@ struct Ws {
     int64_t *slot;
     int32_t *rank;
     int32_t *partial;
-    int64_t *counts;     // {n_new, n_rejected, n_unplaced, unused}
+    int64_t *counts;     // {n_new, n_rejected, n_unplaced, n_wide_authors}
     int64_t blocks;
 };
 
@@ -293,6 +293,7 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const MapEntry *map, 
                                                            const chunk_t *__restrict__ rows_in,
                                                            int32_t chunks,
                                                            int64_t *__restrict__ author,
+                                                           int32_t *__restrict__ author32,
                                                            chunk_t *__restrict__ rows) {
     if (!batch_fits(w, n_old, capacity))
         return;
@@ -308,8 +309,13 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const MapEntry *map, 
             continue;                             // a later record carries this id's row
         const int64_t target = e.pos >= 0 ? (int64_t)e.pos : n_old + w.rank[-(int64_t)e.pos - 3];
         rows[target * chunks + q] = rows_in[i * chunks + q];
-        if (q == 0)
-            author[target] = author_in[i];
+        if (q == 0) {
+            const int64_t x = author_in[i];
+            author[target] = x;
+            author32[target] = (int32_t)x;
+            if (x < INT32_MIN || x > INT32_MAX)
+                atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[3]), 1ULL);
+        }
     }
 }
 
@@ -333,7 +339,28 @@ unsigned grid_for(int64_t work, int64_t per_block) {
     return (unsigned)(b < 65536 ? b : 65536);
 }
 
+__global__ void narrow_kernel(const int64_t *__restrict__ src, int32_t *__restrict__ dst,
+                              int64_t n, unsigned long long *wide) {
+    unsigned long long local = 0;
+    for (int64_t i = global_id(); i < n; i += grid_stride()) {
+        const int64_t x = src[i];
+        dst[i] = (int32_t)x;
+        local += (x < INT32_MIN || x > INT32_MAX) ? 1 : 0;
+    }
+    if (local)
+        atomicAdd(wide, local);
+}
+
 }  // namespace
+
+hipError_t launch_narrow_authors(const int64_t *src, int32_t *dst, int64_t n,
+                                 unsigned long long *wide, hipStream_t stream) {
+    if (n <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(narrow_kernel, dim3(grid_for(n, kThreads)), dim3(kThreads), 0, stream, src,
+                       dst, n, wide);
+    return hipGetLastError();
+}
 
 int64_t map_groups_for(int64_t capacity) {
     int64_t g = 64;
@@ -393,15 +420,15 @@ hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *i
 
 hipError_t launch_upsert_finish(MapEntry *map, int64_t n, void *workspace, int64_t n_old,
                                 int64_t capacity, const int64_t *author_in, const void *rows_in,
-                                int32_t row_bytes, int64_t *author, uint8_t *rows,
-                                hipStream_t stream) {
+                                int32_t row_bytes, int64_t *author, int32_t *author32,
+                                uint8_t *rows, hipStream_t stream) {
     if (n <= 0)
         return hipSuccess;
     const Ws w = carve(workspace, n);
     const int32_t chunks = row_bytes / 16;
     hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(n * chunks, kThreads)), dim3(kThreads), 0,
                        stream, map, n, w, n_old, capacity, author_in,
-                       static_cast<const chunk_t *>(rows_in), chunks, author,
+                       static_cast<const chunk_t *>(rows_in), chunks, author, author32,
                        reinterpret_cast<chunk_t *>(rows));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)

@@ -292,3 +292,43 @@ def test_concurrent_streams_share_a_store():
             assert_same((out.cpu().numpy(), hit.cpu().numpy()), want, f"stream {i}")
     finally:
         P.cc_store_destroy(store)
+
+
+def _remap_ids(tc, f):
+    """The same case with every author id, key and actor id passed through the increasing map f
+    (ranks of the distinct ids -> new ids), so keys stay sorted and every match is kept."""
+    b = tc.batch
+    parts = [tc.author_id, b.keys] + ([b.actor] if b.actor is not None else [])
+    ids = torch.unique(torch.cat(parts))
+    rank = lambda t: torch.searchsorted(ids, t)
+    new = lambda t: None if t is None else f(rank(t))
+    nb = W.Batch(b.cand_offsets, b.cand_idx, b.key_offsets, new(b.keys), b.edge_rows, new(b.actor))
+    return W.TinyCase(new(tc.author_id), tc.doc_rows, nb, tc.default_row, tc.n_lookups)
+
+
+def test_author_column_layouts():
+    """Stores whose author ids fit in 32 bits keep a 32-bit column that the joins read; wider
+    ids keep the 64-bit column. Both give the oracle's result, including ids at the int32
+    limits and negative ids."""
+    note("author column layouts")
+    lo, hi = -(1 << 31), (1 << 31) - 1
+    maps = {
+        4: [lambda r: r - 7, lambda r: lo + r, lambda r: hi - 40 + r],
+        8: [lambda r: (r - 3) << 33, lambda r: hi - 3 + r],       # the second crosses 2^31
+    }
+    for seed in range(16):
+        tc = W.tiny_case(5000 + seed, max_k=60, max_n=300, max_viewers=4, max_docs=40)
+        for width, fs in maps.items():
+            for k, f in enumerate(fs):
+                t = _remap_ids(tc, f)
+                store = P.cc_store_create(t.author_id.to(DEV), t.doc_rows.to(DEV))
+                try:
+                    got_w = P.cc_store_layout(store)[0]
+                    fits = bool(((t.author_id >= lo) & (t.author_id <= hi)).all())
+                    assert got_w == (4 if fits else 8), f"seed {seed}: layout {got_w}"
+                    if width == 4:
+                        assert got_w == 4
+                finally:
+                    P.cc_store_destroy(store)
+                for tu in (None, (4, 0, 0)):
+                    _tiny(t, tu, what=f"seed {seed} map {width}/{k} tuning {tu}")

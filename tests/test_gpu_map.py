@@ -288,3 +288,46 @@ def test_argument_errors_on_device():
             P.cc_store_read(ix.store, 0, 1, ids, None)
     finally:
         ix.close()
+
+
+def test_wide_author_id_switches_the_column():
+    """Ingestion keeps the 32-bit author column while every id fits; the first wider author id
+    switches the store to its 64-bit column for good. Joins match the oracle before and after."""
+    note("map: author column switch")
+    ix = DeviceIndex(64, 16)
+    try:
+        ids = W.doc_ids(torch.arange(40), 3)
+        rows = torch.arange(40 * 16, dtype=torch.int64).to(torch.uint8).reshape(40, 16)
+        authors = torch.arange(40, dtype=torch.int64) * 1000 - 7000
+        assert ix.upsert(ids[:30], authors[:30], rows[:30]) == (30, 0)
+        assert P.cc_store_layout(ix.store) == (4, 64)
+
+        def check_join(what):
+            n = ix.ref.n_docs
+            keys = torch.sort(torch.unique(torch.from_numpy(ix.ref.author[:n].copy()))).values[::2]
+            cand = torch.arange(-1, n + 1, dtype=torch.int64)
+            edge = torch.arange(keys.numel() * 16, dtype=torch.int64).to(torch.uint8).reshape(-1, 16)
+            b = W.Batch(torch.tensor([0, cand.numel()]), cand, torch.tensor([0, keys.numel()]),
+                        keys, edge, None)
+            got = gpu_join(ix.store, None, b.to(DEV), 16, 16, 1)
+            want = oracle_join(torch.from_numpy(ix.ref.author[:n].copy()),
+                               torch.from_numpy(ix.ref.rows[:n].copy()), b, 1)
+            assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1]), what
+
+        check_join("32-bit column")
+        wide = authors[30:35].clone()
+        wide[2] = (1 << 40) + 5
+        assert ix.upsert(ids[30:35], wide, rows[30:35]) == (5, 0)
+        assert P.cc_store_layout(ix.store)[0] == 8
+        check_join("64-bit column")
+        ix.check_state("after the switch")
+        # a batch that does not fit leaves the layout alone
+        ix2 = DeviceIndex(4, 16)
+        try:
+            big = torch.full((6,), 1 << 40, dtype=torch.int64)
+            assert ix2.upsert(ids[:6], big, rows[:6]) is None
+            assert P.cc_store_layout(ix2.store)[0] == 4
+        finally:
+            ix2.close()
+    finally:
+        ix.close()

@@ -427,7 +427,7 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": PEAK_GBPS, "unit": "GB/s",
             "frac": achieved / PEAK_GBPS, "traffic": load_traffic(),
-            "kernel": "join_kernel<8, 4, 1, true>", "algorithmic_bytes_per_launch": alg_per_launch,
+            "kernel": "join_kernel<8, 4, 1, true, true>", "algorithmic_bytes_per_launch": alg_per_launch,
         },
         "cpu_baseline": cpu,
         "wall_s_timed_region": wall,

@@ -22,6 +22,7 @@ struct cc_store {
     unsigned long long *d_invalid;   // invalid-position counter
     uint8_t *d_zero;                 // ccj::kZeroRowBytes zero bytes, read in place of absent rows
     ccj::MapEntry *d_map;            // document-id map, or null (store without ids)
+    int64_t *h_counts;               // pinned host copy of an ingestion batch's counts
     int64_t map_groups;              // probe groups in d_map (a power of two)
 };
 
@@ -205,6 +206,7 @@ void free_store(cc_store *s) {
     (void)hipFree(s->d_invalid);
     (void)hipFree(s->d_zero);
     (void)hipFree(s->d_map);
+    (void)hipHostFree(s->h_counts);
     delete s;
 }
 
@@ -253,6 +255,8 @@ cc_status new_store(int64_t capacity, int32_t doc_row_bytes, bool with_map, hipS
         if ((e = hipMalloc(&s->d_author32, (size_t)(capacity > 0 ? capacity * 4 : 256))) != hipSuccess)
             return alloc_failure(s, e);
         s->compact = true;
+        if ((e = hipHostMalloc(&s->h_counts, 4 * sizeof(int64_t), hipHostMallocDefault)) != hipSuccess)
+            return alloc_failure(s, e);
     }
     if ((e = hipMemsetAsync(s->d_invalid, 0, sizeof(unsigned long long), stream)) != hipSuccess)
         return alloc_failure(s, e);
@@ -376,9 +380,9 @@ cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc
                                       store->capacity, author_ids, doc_rows,
                                       store->doc_row_bytes, store->d_author, store->d_author32,
                                       store->d_rows, stream);
-    int64_t counts[4] = {0, 0, 0, 0};
+    int64_t *counts = store->h_counts;        // pinned: the read-back is one small DMA
     if (e == hipSuccess)
-        e = hipMemcpyAsync(counts, ccj::upsert_counts(workspace, n_records), sizeof(counts),
+        e = hipMemcpyAsync(counts, ccj::upsert_counts(workspace, n_records), 4 * sizeof(int64_t),
                            hipMemcpyDeviceToHost, stream);
     if (e == hipSuccess)
         e = hipStreamSynchronize(stream);

@@ -91,7 +91,23 @@ __global__ void map_init_kernel(MapEntry *map, int64_t n_entries) {
 }
 
 // One query per quad of lanes: each lane reads one entry of the probed group (a quad reads the
-// group's 64 contiguous bytes) and the quad votes.
+// group's 64 contiguous bytes) and the quad votes. A quad takes kResolvePer queries at a time and
+// issues their first-group reads together, so each wavefront keeps several HBM round trips in
+// flight; the rare query whose first group is full and does not hold its id probes on alone.
+constexpr int kResolvePer = 4;
+
+__device__ __forceinline__ bool quad_vote(const MapEntry &e, int64_t key, int quad0,
+                                          int64_t &result) {
+    const unsigned hit = (unsigned)(__ballot(e.key == key) >> quad0) & 0xF;
+    const unsigned emp = (unsigned)(__ballot(e.key == kEmptyKey) >> quad0) & 0xF;
+    if (hit) {
+        const int32_t p = __shfl(e.pos, quad0 + __builtin_ctz(hit));
+        result = p >= 0 ? p : -1;
+        return true;
+    }
+    return emp != 0;                              // a free entry ends the probe: absent
+}
+
 __global__ __launch_bounds__(kThreads) void resolve_kernel(const MapEntry *__restrict__ map,
                                                            uint64_t mask,
                                                            const int64_t *__restrict__ ids,
@@ -100,27 +116,36 @@ __global__ __launch_bounds__(kThreads) void resolve_kernel(const MapEntry *__res
     const int sub = lane & (kGroup - 1);
     const int quad0 = lane & ~(kGroup - 1);
     const int64_t stride = grid_stride() / kGroup;
-    for (int64_t q = global_id() / kGroup; q < n; q += stride) {
-        const int64_t key = ids[q];
-        int64_t result = -1;
-        if (key != kEmptyKey) {
-            uint64_t g = mix((uint64_t)key) & mask;
-            for (uint64_t probe = 0; probe < kMaxProbeGroups && probe <= mask; ++probe) {
-                const MapEntry e = map[g * kGroup + sub];
-                const unsigned hit = (unsigned)(__ballot(e.key == key) >> quad0) & 0xF;
-                const unsigned emp = (unsigned)(__ballot(e.key == kEmptyKey) >> quad0) & 0xF;
-                if (hit) {
-                    const int32_t p = __shfl(e.pos, quad0 + __builtin_ctz(hit));
-                    result = p >= 0 ? p : -1;
-                    break;
-                }
-                if (emp)
-                    break;
-                g = (g + 1) & mask;
-            }
+    for (int64_t q0 = global_id() / kGroup; q0 < n; q0 += kResolvePer * stride) {
+        int64_t key[kResolvePer];
+        uint64_t g[kResolvePer];
+        MapEntry e[kResolvePer];
+#pragma unroll
+        for (int r = 0; r < kResolvePer; ++r) {
+            const int64_t q = q0 + r * stride;
+            key[r] = q < n ? ids[q] : kEmptyKey;
+            g[r] = mix((uint64_t)key[r]) & mask;
         }
-        if (sub == 0)
-            pos[q] = result;
+#pragma unroll
+        for (int r = 0; r < kResolvePer; ++r)
+            e[r] = map[g[r] * kGroup + sub];      // in bounds for every key, used or not
+#pragma unroll
+        for (int r = 0; r < kResolvePer; ++r) {
+            const int64_t q = q0 + r * stride;
+            if (q >= n)
+                break;                            // uniform per quad
+            int64_t result = -1;
+            if (key[r] != kEmptyKey && !quad_vote(e[r], key[r], quad0, result)) {
+                uint64_t gg = g[r];
+                for (uint64_t probe = 1; probe < kMaxProbeGroups && probe <= mask; ++probe) {
+                    gg = (gg + 1) & mask;
+                    if (quad_vote(map[gg * kGroup + sub], key[r], quad0, result))
+                        break;
+                }
+            }
+            if (sub == 0)
+                pos[q] = result;
+        }
     }
 }
 
@@ -380,7 +405,8 @@ hipError_t launch_resolve(const MapEntry *map, int64_t n_groups, const int64_t *
                           int64_t *pos, hipStream_t stream) {
     if (n <= 0)
         return hipSuccess;
-    hipLaunchKernelGGL(resolve_kernel, dim3(grid_for(n * kGroup, kThreads)), dim3(kThreads), 0,
+    const int64_t quads = (n + kResolvePer - 1) / kResolvePer;
+    hipLaunchKernelGGL(resolve_kernel, dim3(grid_for(quads * kGroup, kThreads)), dim3(kThreads), 0,
                        stream, map, (uint64_t)(n_groups - 1), ids, n, pos);
     return hipGetLastError();
 }

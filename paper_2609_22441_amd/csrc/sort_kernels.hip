@@ -270,7 +270,12 @@ __global__ __launch_bounds__(kThreads) void block_sort_kernel(const int64_t *__r
         for (int m = 0; m < kEpt; ++m)
             r[m] = s[pidx(tid * kEpt + m)];
         sort_regs(r);
-        for (int L = kEpt; L < kTile; L <<= 1) {
+        // Records sit at positions [0, n) and pads after them, so once the runs reach the power
+        // of two p >= n the records are one sorted run; later rounds would only merge pads.
+        int p = kEpt;
+        while (p < n)
+            p <<= 1;
+        for (int L = kEpt; L < p; L <<= 1) {
             lds_sync();                                  // every thread has read s
             store_regs(s, r, tid * kEpt, kTile);
             lds_sync();

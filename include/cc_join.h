@@ -171,6 +171,7 @@ CC_API cc_status cc_join(const cc_store *store,
  *                  row]; out_row_stride is a multiple of 16 and >= doc_row_bytes +
  *                  L * edge_row_bytes.
  *   hit_mask       [total_cand][L] int8.
+ * out and hit_mask must not overlap each other or any input (checked: CC_ERR_INVALID_ARGUMENT).
  *
  * Defined outcomes for data the host cannot check without synchronising:
  *   - cand_idx[j] outside [0, n_docs): doc segment = zero bytes, every edge segment = the

@@ -114,6 +114,28 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
         !aligned(cand_idx, 8) || !aligned(edge_keys, 8) || !aligned(cand_offsets, 8) ||
         !aligned(key_offsets, 8) || !aligned(extra, 8))
         return CC_ERR_INVALID_ARGUMENT;
+    {
+        // The outputs must not overlap any input or each other.
+        const int64_t rows = padded ? slots : total_cand;
+        const int64_t nv1 = cand_offsets ? (int64_t)n_viewers + 1 : 0;
+        const struct { const void *p; int64_t n; } in[] = {
+            {cand_idx, total_cand * 8}, {edge_keys, total_keys * 8},
+            {edge_feats, total_keys * edge_row_bytes}, {extra, extra ? total_cand * 8 : 0},
+            {cand_offsets, nv1 * 8}, {key_offsets, nv1 * 8},
+            {default_row, default_row ? edge_row_bytes : 0}};
+        const struct { const void *p; int64_t n; } outs[] = {
+            {out, rows * out_row_stride}, {hit_mask, rows * n_lookups},
+            {valid_mask, padded ? slots : 0}};
+        for (const auto &o : outs) {
+            for (const auto &i : in)
+                if (overlaps(o.p, o.n, i.p, i.n))
+                    return CC_ERR_INVALID_ARGUMENT;
+        }
+        if (overlaps(outs[0].p, outs[0].n, outs[1].p, outs[1].n) ||
+            overlaps(outs[0].p, outs[0].n, outs[2].p, outs[2].n) ||
+            overlaps(outs[1].p, outs[1].n, outs[2].p, outs[2].n))
+            return CC_ERR_INVALID_ARGUMENT;
+    }
     int32_t lds_cap = ccj::kDefaultLdsKeys, stride = 0, wgs = 0, budget = 4;
     bool one_wave = false;
     const int64_t viewers = cand_offsets ? n_viewers : 1;
@@ -299,23 +321,25 @@ cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *a
         if ((e = hipMemcpyAsync(s->d_rows, doc_rows, (size_t)row_total, kind, stream)) != hipSuccess)
             return alloc_failure(s, e);
         // Keep a 32-bit copy of the author column when every id fits: the join's random author
-        // reads then touch half as many 64-byte sectors.
-        if ((e = hipMalloc(&s->d_author32, (size_t)(n_docs * 4))) != hipSuccess)
-            return alloc_failure(s, e);
+        // reads then touch half as many 64-byte sectors. The copy is optional: if it cannot be
+        // allocated the store keeps to its 64-bit column.
         unsigned long long *d_wide = nullptr;
         unsigned long long wide = 1;
-        if ((e = hipMalloc(&d_wide, sizeof(unsigned long long))) != hipSuccess)
-            return alloc_failure(s, e);
-        e = hipMemsetAsync(d_wide, 0, sizeof(unsigned long long), stream);
-        if (e == hipSuccess)
-            e = ccj::launch_narrow_authors(s->d_author, s->d_author32, n_docs, d_wide, stream);
-        if (e == hipSuccess)
-            e = hipMemcpyAsync(&wide, d_wide, sizeof(wide), hipMemcpyDeviceToHost, stream);
-        if (e == hipSuccess)
-            e = hipStreamSynchronize(stream);
-        (void)hipFree(d_wide);
-        if (e != hipSuccess)
-            return alloc_failure(s, e);
+        if (hipMalloc(&s->d_author32, (size_t)(n_docs * 4)) == hipSuccess &&
+            hipMalloc(&d_wide, sizeof(unsigned long long)) == hipSuccess) {
+            e = hipMemsetAsync(d_wide, 0, sizeof(unsigned long long), stream);
+            if (e == hipSuccess)
+                e = ccj::launch_narrow_authors(s->d_author, s->d_author32, n_docs, d_wide, stream);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync(&wide, d_wide, sizeof(wide), hipMemcpyDeviceToHost, stream);
+            if (e == hipSuccess)
+                e = hipStreamSynchronize(stream);
+            (void)hipFree(d_wide);
+            if (e != hipSuccess)
+                return alloc_failure(s, e);
+        } else {
+            (void)hipGetLastError();              // an allocation failure is not sticky
+        }
         if (wide == 0) {
             s->compact = true;
         } else {

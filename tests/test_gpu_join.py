@@ -332,3 +332,33 @@ def test_author_column_layouts():
                     P.cc_store_destroy(store)
                 for tu in (None, (4, 0, 0)):
                     _tiny(t, tu, what=f"seed {seed} map {width}/{k} tuning {tu}")
+
+
+def test_outputs_overlapping_inputs_are_rejected():
+    """The join refuses outputs that overlap an input or each other (checked on the host)."""
+    note("overlapping outputs")
+    tc = W.tiny_case(77, max_k=30, max_n=100, max_viewers=2, n_lookups=1, doc_bytes=32,
+                     edge_bytes=16)
+    b = tc.batch.to(DEV)
+    n, k = b.cand_idx.numel(), b.keys.numel()
+    assert n > 0 and k > 0
+    store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+    lib = B.lib()
+    out = torch.zeros(n, 48, dtype=torch.uint8, device=DEV)
+    hit = torch.zeros(n, 1, dtype=torch.int8, device=DEV)
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def call(out_p, hit_p):
+        return lib.cc_join_batched(store, b.n_viewers, b.cand_offsets.data_ptr(),
+                                   b.cand_idx.data_ptr(), n, b.key_offsets.data_ptr(),
+                                   b.keys.data_ptr(), k, b.edge_rows.data_ptr(), 16, None, 1, None,
+                                   out_p, 48, hit_p, stream)
+    try:
+        assert call(b.cand_idx.data_ptr(), hit.data_ptr()) == 1        # out over the positions
+        assert call(b.edge_rows.data_ptr(), hit.data_ptr()) == 1       # out over the edge rows
+        assert call(out.data_ptr(), out.data_ptr() + 32) == 1          # hit mask inside out
+        assert call(out.data_ptr(), b.keys.data_ptr()) == 1            # hit mask over the keys
+        assert call(out.data_ptr(), hit.data_ptr()) == 0               # disjoint: accepted
+        torch.cuda.synchronize()
+    finally:
+        P.cc_store_destroy(store)

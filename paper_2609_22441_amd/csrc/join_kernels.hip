@@ -453,10 +453,12 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
         atomicAdd(a.invalid_counter, (unsigned long long)s_invalid);
 }
 
+constexpr int kMaxDevices = 64;
+
 // Multiprocessor count per device (cached; devices are few).
 int cu_count(int device) {
-    static std::atomic<int> cache[64];
-    if (device >= 0 && device < 64) {
+    static std::atomic<int> cache[kMaxDevices];
+    if (device >= 0 && device < kMaxDevices) {
         int v = cache[device].load(std::memory_order_relaxed);
         if (v > 0)
             return v;
@@ -465,7 +467,7 @@ int cu_count(int device) {
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
         v <= 0)
         v = 256;
-    if (device >= 0 && device < 64)
+    if (device >= 0 && device < kMaxDevices)
         cache[device].store(v, std::memory_order_relaxed);
     return v;
 }
@@ -494,9 +496,12 @@ hipError_t launch_one(JoinArgs &a, int32_t workgroups, int device, hipStream_t s
                   "LDS budget exceeded");
     const void *fn = reinterpret_cast<const void *>(&join_kernel<D, E, L, BATCHED, A32>);
     const size_t lds = (size_t)max(1, a.lds_keys) * sizeof(int64_t);
-    static std::once_flag lds_limit;
+    // Raise the kernel's dynamic LDS limit once per device (the attribute is per device).
+    static std::once_flag lds_limit[kMaxDevices];
+    if (device < 0 || device >= kMaxDevices)
+        return hipErrorInvalidDevice;
     hipError_t err = hipSuccess;
-    std::call_once(lds_limit, [&] {
+    std::call_once(lds_limit[device], [&] {
         err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                   kMaxLdsKeys * (int)sizeof(int64_t));
     });

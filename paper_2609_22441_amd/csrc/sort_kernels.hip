@@ -1,13 +1,20 @@
 // Alg. 1 Step 1 on the device (Connected Content Retriever §3.1): sort each viewer's affinity
 // records by author id and move their feature rows with them.
 //
-// Each viewer's records (a CSR segment) are cut into tiles of kTile records. Elements are
-// 16 bytes, (key, input position), ordered by key then position. That order is unique, so any
-// correct sort is stable.
-//   0. plan: tile offsets per viewer (an exclusive scan of ceil(K_v / kTile)).
+// Each viewer's records (a CSR segment) are cut into tiles of kTile records. A record is sorted
+// as an element that orders by (key, input position). That order is unique, so any correct sort
+// is stable. Elements take one of two forms, chosen on the device for the whole call:
+//   * packed, 8 bytes: ((key - kmin) << pbits) | (position within the viewer), when the span of
+//     the call's keys leaves room for pbits position bits (pbits covers the largest viewer);
+//     one 64-bit compare orders it, and it halves the bytes every pass moves;
+//   * wide, 16 bytes: (key, flat input position), for any keys.
+// Passes:
+//   0. key range: the minimum and maximum key (per-workgroup slots, reduced by the plan), from
+//      which every kernel derives the same form; plan: tile offsets per viewer (an exclusive
+//      scan of ceil(K_v / kTile)).
 //   1. block sort: a workgroup loads one tile; every thread sorts kEpt records in registers
-//      with a bitonic network, then log2(kTile / kEpt) merge-path rounds in LDS double the
-//      sorted runs until the tile is one run.
+//      with a bitonic network, then merge-path rounds in LDS double the sorted runs until the
+//      tile's records are one run.
 //   2. merge rounds: within each viewer, runs of kTile << r records are merged pairwise, one
 //      output tile per workgroup. A viewer with n tiles takes part in ceil(log2 n) rounds. The
 //      tile's split on the merge path is found by a 64-ary search run by one wavefront (a few
@@ -35,17 +42,57 @@ constexpr int kLdsElems = kTile + kTile / kEpt;   // padded LDS tile
 
 typedef unsigned int chunk_t __attribute__((ext_vector_type(4)));
 
-struct Elem {
-    int64_t key;
-    int64_t f;    // flat input position
+// Shared by every kernel of one call: the key range (written by range_kernel) and the number of
+// position bits a packed element needs.
+struct Codec {
+    const int64_t *range;   // {min key, max key} in the workspace
+    int32_t pbits;
 };
 
-__device__ __forceinline__ bool elem_less(const Elem &a, const Elem &b) {
-    return a.key != b.key ? a.key < b.key : a.f < b.f;
-}
+struct Wide {
+    struct T {
+        int64_t key;
+        int64_t f;    // flat input position
+    };
+    __device__ static bool less(const T &a, const T &b) {
+        return a.key != b.key ? a.key < b.key : a.f < b.f;
+    }
+    __device__ static T pad() { return T{INT64_MAX, INT64_MAX}; }
+    // c ? x : y field by field (a select of the whole struct is lowered through scratch memory).
+    __device__ static T sel(bool c, const T &x, const T &y) {
+        return T{c ? x.key : y.key, c ? x.f : y.f};
+    }
+    __device__ T make(int64_t key, int64_t f, int64_t) const { return T{key, f}; }
+    __device__ int64_t key(const T &e) const { return e.key; }
+    __device__ int64_t src(const T &e, int64_t) const { return e.f; }
+};
 
-// a goes first in a merge (ties go to the first run).
-__device__ __forceinline__ bool first_le(const Elem &a, const Elem &b) { return !elem_less(b, a); }
+struct Packed {
+    typedef uint64_t T;
+    int64_t kmin;
+    int32_t pbits;
+    __device__ static bool less(T a, T b) { return a < b; }
+    __device__ static T pad() { return ~(uint64_t)0; }    // above every packed record
+    __device__ static T sel(bool c, T x, T y) { return c ? x : y; }
+    __device__ T make(int64_t key, int64_t f, int64_t kb) const {
+        return (((uint64_t)key - (uint64_t)kmin) << pbits) | (uint64_t)(f - kb);
+    }
+    __device__ int64_t key(T e) const { return (int64_t)((e >> pbits) + (uint64_t)kmin); }
+    __device__ int64_t src(T e, int64_t kb) const {
+        return kb + (int64_t)(e & ((((uint64_t)1) << pbits) - 1));
+    }
+};
+
+// Packed elements are usable when key - kmin < 2^(64 - pbits) - 1 for every key (the largest
+// value stays free for padding). Every kernel evaluates this on the same range.
+__device__ __forceinline__ bool use_packed(const Codec &c, int64_t &kmin) {
+    kmin = c.range[0];
+    const int64_t kmax = c.range[1];
+    if (kmax < kmin)
+        return true;                                    // no keys
+    const uint64_t span = (uint64_t)kmax - (uint64_t)kmin;
+    return span < (((uint64_t)1) << (64 - c.pbits)) - 1;
+}
 
 __device__ __forceinline__ int pidx(int i) { return i + i / kEpt; }
 
@@ -88,17 +135,17 @@ __device__ __forceinline__ int64_t owner(const int64_t *tile_off, int64_t B, int
     return lo;
 }
 
-__device__ __forceinline__ Elem pad_elem() { return Elem{INT64_MAX, INT64_MAX}; }
-
-// c ? x : y field by field (a select of the whole struct is lowered through scratch memory).
-__device__ __forceinline__ Elem sel(bool c, const Elem &x, const Elem &y) {
-    return Elem{c ? x.key : y.key, c ? x.f : y.f};
+// a goes first in a merge (ties go to the first run).
+template <typename F>
+__device__ __forceinline__ bool first_le(const typename F::T &a, const typename F::T &b) {
+    return !F::less(b, a);
 }
 
 // Compare-exchange: afterwards a <= b when up, a >= b otherwise.
-__device__ __forceinline__ void cx(Elem &a, Elem &b, bool up) {
-    const bool sw = up ? elem_less(b, a) : elem_less(a, b);
-    const Elem x = sel(sw, b, a), y = sel(sw, a, b);
+template <typename F>
+__device__ __forceinline__ void cx(typename F::T &a, typename F::T &b, bool up) {
+    const bool sw = up ? F::less(b, a) : F::less(a, b);
+    const typename F::T x = F::sel(sw, b, a), y = F::sel(sw, a, b);
     a = x;
     b = y;
 }
@@ -106,69 +153,84 @@ __device__ __forceinline__ void cx(Elem &a, Elem &b, bool up) {
 // Bitonic network over a thread's kEpt registers. Written with template recursion so that every
 // register index is a compile-time constant (a runtime partner index would put the array in
 // scratch memory).
-template <int K, int J>
-__device__ __forceinline__ void bitonic_stage(Elem (&r)[kEpt]) {
+template <typename F, int K, int J>
+__device__ __forceinline__ void bitonic_stage(typename F::T (&r)[kEpt]) {
 #pragma unroll
     for (int i = 0; i < kEpt; ++i) {
         const int p = i ^ J;
         if (p > i)
-            cx(r[i], r[p], (i & K) == 0);
+            cx<F>(r[i], r[p], (i & K) == 0);
     }
     if constexpr (J > 1)
-        bitonic_stage<K, J / 2>(r);
+        bitonic_stage<F, K, J / 2>(r);
 }
 
-template <int K>
-__device__ __forceinline__ void bitonic_level(Elem (&r)[kEpt]) {
-    bitonic_stage<K, K / 2>(r);
+template <typename F, int K>
+__device__ __forceinline__ void bitonic_level(typename F::T (&r)[kEpt]) {
+    bitonic_stage<F, K, K / 2>(r);
     if constexpr (K < kEpt)
-        bitonic_level<K * 2>(r);
+        bitonic_level<F, K * 2>(r);
 }
 
-__device__ __forceinline__ void sort_regs(Elem (&r)[kEpt]) { bitonic_level<2>(r); }
+template <typename F>
+__device__ __forceinline__ void sort_regs(typename F::T (&r)[kEpt]) {
+    bitonic_level<F, 2>(r);
+}
 
 // Outputs [d, d + kEpt) of merge(A, B), A = s[a_off, a_off + la), B = s[b_off, b_off + lb)
 // (logical indices, padded in LDS). Outputs past la + lb are pad elements.
-__device__ __forceinline__ void merge_ept(const Elem *s, int a_off, int la, int b_off, int lb,
-                                          int d, Elem (&r)[kEpt]) {
+template <typename F>
+__device__ __forceinline__ void merge_ept(const typename F::T *s, int a_off, int la, int b_off,
+                                          int lb, int d, typename F::T (&r)[kEpt]) {
+    typedef typename F::T T;
     int lo = d > lb ? d - lb : 0, hi = d < la ? d : la;
     while (lo < hi) {                      // smallest i with A[i] not among the first d outputs
         const int mid = (lo + hi) >> 1;
-        if (first_le(s[pidx(a_off + mid)], s[pidx(b_off + d - 1 - mid)]))
+        if (first_le<F>(s[pidx(a_off + mid)], s[pidx(b_off + d - 1 - mid)]))
             lo = mid + 1;
         else
             hi = mid;
     }
     int ia = lo, ib = d - lo;
-    Elem a = ia < la ? s[pidx(a_off + ia)] : pad_elem();
-    Elem b = ib < lb ? s[pidx(b_off + ib)] : pad_elem();
+    T a = ia < la ? s[pidx(a_off + ia)] : F::pad();
+    T b = ib < lb ? s[pidx(b_off + ib)] : F::pad();
 #pragma unroll
     for (int m = 0; m < kEpt; ++m) {
-        const bool take_a = ib >= lb || (ia < la && first_le(a, b));
-        r[m] = sel(take_a, a, b);
+        const bool take_a = ib >= lb || (ia < la && first_le<F>(a, b));
+        r[m] = F::sel(take_a, a, b);
         ia += take_a;
         ib += !take_a;
         const bool ok = take_a ? ia < la : ib < lb;
-        const Elem nx = ok ? s[pidx(take_a ? a_off + ia : b_off + ib)] : pad_elem();
-        a = sel(take_a, nx, a);
-        b = sel(take_a, b, nx);
+        const T nx = ok ? s[pidx(take_a ? a_off + ia : b_off + ib)] : F::pad();
+        a = F::sel(take_a, nx, a);
+        b = F::sel(take_a, b, nx);
     }
 }
 
-__device__ __forceinline__ void store_regs(Elem *s, const Elem (&r)[kEpt], int first, int n) {
+template <typename F>
+__device__ __forceinline__ void store_regs(typename F::T *s, const typename F::T (&r)[kEpt],
+                                           int first, int n) {
 #pragma unroll
     for (int m = 0; m < kEpt; ++m)
         if (first + m < n)
             s[pidx(first + m)] = r[m];
 }
 
-// The first n records of s (sorted) belong at flat positions [pos, pos + n). Either write the
-// elements to dst, or, on a viewer's last pass, the keys and the rows they came from.
-__device__ __forceinline__ void emit(const Elem *s, int n, int64_t pos, Elem *__restrict__ dst,
-                                     bool last, int64_t total,
-                                     const chunk_t *__restrict__ rows_in, int row_chunks,
-                                     int64_t *__restrict__ keys_out,
-                                     chunk_t *__restrict__ rows_out) {
+struct SortOut {
+    int64_t total;
+    const chunk_t *rows_in;
+    int32_t row_chunks;
+    int64_t *keys_out;
+    chunk_t *rows_out;
+};
+
+// The first n records of s (sorted) belong at flat positions [pos, pos + n) of the viewer that
+// starts at kb. Either write the elements to dst, or, on a viewer's last pass, the keys and the
+// rows they came from.
+template <typename F>
+__device__ __forceinline__ void emit(const F &fm, const typename F::T *s, int n, int64_t pos,
+                                     int64_t kb, typename F::T *__restrict__ dst, bool last,
+                                     const SortOut &o) {
     const int tid = threadIdx.x;
     if (!last) {
         for (int i = tid; i < n; i += kThreads)
@@ -176,8 +238,9 @@ __device__ __forceinline__ void emit(const Elem *s, int n, int64_t pos, Elem *__
         return;
     }
     for (int i = tid; i < n; i += kThreads)
-        keys_out[pos + i] = s[pidx(i)].key;
+        o.keys_out[pos + i] = fm.key(s[pidx(i)]);
     constexpr int U = 8;
+    const int row_chunks = o.row_chunks;
     const int n_chunks = n * row_chunks;
     for (int g0 = tid; g0 < n_chunks; g0 += U * kThreads) {
         chunk_t c[U];
@@ -189,27 +252,51 @@ __device__ __forceinline__ void emit(const Elem *s, int n, int64_t pos, Elem *__
             if (g < n_chunks) {
                 const int rec = g / row_chunks;
                 const int q = g - rec * row_chunks;
-                const int64_t f = clampk(s[pidx(rec)].f, total - 1);
-                c[u] = rows_in[f * row_chunks + q];
+                const int64_t f = clampk(fm.src(s[pidx(rec)], kb), o.total - 1);
+                c[u] = o.rows_in[f * row_chunks + q];
                 dst_i[u] = (pos + rec) * row_chunks + q;
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
             if (dst_i[u] >= 0)
-                rows_out[dst_i[u]] = c[u];
+                o.rows_out[dst_i[u]] = c[u];
     }
 }
 
-// tile_off[v] = sum of tiles of viewers < v, for v in [0, B]. One workgroup.
+// tile_off[v] = sum of tiles of viewers < v, for v in [0, B]. One workgroup. Also reduces the
+// per-workgroup key ranges of range_kernel (n_slots pairs) into range = {min, max}.
 __global__ __launch_bounds__(kThreads) void plan_kernel(const int64_t *off, int32_t B,
-                                                        int64_t total, int64_t *tile_off) {
+                                                        int64_t total, int64_t *tile_off,
+                                                        const int64_t *slots, int n_slots,
+                                                        int64_t *range) {
     __shared__ int64_t s[kThreads];
+    __shared__ int64_t s_hi[kThreads];
     __shared__ int64_t carry;
     const int tid = threadIdx.x;
-    if (tid == 0)
-        carry = 0;
-    lds_sync();
+    {
+        int64_t lo = INT64_MAX, hi = INT64_MIN;
+        for (int i = tid; i < n_slots; i += kThreads) {
+            lo = min(lo, slots[2 * i]);
+            hi = max(hi, slots[2 * i + 1]);
+        }
+        s[tid] = lo;
+        s_hi[tid] = hi;
+        lds_sync();
+        for (int d = kThreads / 2; d > 0; d >>= 1) {
+            if (tid < d) {
+                s[tid] = min(s[tid], s[tid + d]);
+                s_hi[tid] = max(s_hi[tid], s_hi[tid + d]);
+            }
+            lds_sync();
+        }
+        if (tid == 0) {
+            range[0] = s[0];
+            range[1] = s_hi[0];
+            carry = 0;
+        }
+        lds_sync();
+    }
     for (int64_t b0 = 0; b0 <= B; b0 += kThreads) {
         const int64_t v = b0 + tid;
         int64_t n = 0;
@@ -235,22 +322,58 @@ __global__ __launch_bounds__(kThreads) void plan_kernel(const int64_t *off, int3
     }
 }
 
-struct SortOut {
-    int64_t total;
-    const chunk_t *rows_in;
-    int32_t row_chunks;
-    int64_t *keys_out;
-    chunk_t *rows_out;
-};
+// slots[2b], slots[2b + 1] = min and max of the keys workgroup b reads (a grid-stride slice of
+// keys[0, total)); the plan kernel reduces the slots. No atomics and nothing to initialise.
+constexpr int kRangeThreads = 256;
+constexpr int kRangeUnroll = 4;
 
-__global__ __launch_bounds__(kThreads) void block_sort_kernel(const int64_t *__restrict__ keys,
-                                                              const int64_t *off, int32_t B,
-                                                              const int64_t *tile_off,
-                                                              Elem *__restrict__ out, SortOut o) {
-    __shared__ Elem s[kLdsElems];
+__global__ __launch_bounds__(kRangeThreads) void range_kernel(const int64_t *__restrict__ keys,
+                                                              int64_t total, int64_t *slots) {
+    __shared__ int64_t s_lo[kRangeThreads / 64], s_hi[kRangeThreads / 64];
+    int64_t lo = INT64_MAX, hi = INT64_MIN;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < total;
+         i0 += kRangeUnroll * stride) {
+        int64_t k[kRangeUnroll];
+#pragma unroll
+        for (int u = 0; u < kRangeUnroll; ++u)
+            k[u] = keys[min(i0 + u * stride, total - 1)];      // clamped: repeats change nothing
+#pragma unroll
+        for (int u = 0; u < kRangeUnroll; ++u) {
+            lo = min(lo, k[u]);
+            hi = max(hi, k[u]);
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        lo = min(lo, (int64_t)__shfl_down(lo, off));
+        hi = max(hi, (int64_t)__shfl_down(hi, off));
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        s_lo[wave] = lo;
+        s_hi[wave] = hi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int k = 1; k < kRangeThreads / 64; ++k) {
+            lo = min(lo, s_lo[k]);
+            hi = max(hi, s_hi[k]);
+        }
+        slots[2 * blockIdx.x] = lo;
+        slots[2 * blockIdx.x + 1] = hi;
+    }
+}
+
+template <typename F>
+__device__ __forceinline__ void block_sort_body(const F &fm, char *lds,
+                                                const int64_t *__restrict__ keys,
+                                                const int64_t *off, int32_t B,
+                                                const int64_t *tile_off, void *out_v,
+                                                const SortOut &o) {
+    typedef typename F::T T;
+    T *s = reinterpret_cast<T *>(lds);
+    T *out = static_cast<T *>(out_v);
     const int tid = threadIdx.x;
-    if (B <= 0)
-        return;
     const int64_t n_tiles = tile_off[B];
     for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {   // uniform per workgroup
         const int64_t v = owner(tile_off, B, t);
@@ -262,14 +385,14 @@ __global__ __launch_bounds__(kThreads) void block_sort_kernel(const int64_t *__r
 #pragma unroll
         for (int m = 0; m < kEpt; ++m) {
             const int i = m * kThreads + tid;
-            s[pidx(i)] = i < n ? Elem{keys[base + i], base + i} : pad_elem();   // pads sort last
+            s[pidx(i)] = i < n ? fm.make(keys[base + i], base + i, kb) : F::pad();  // pads last
         }
         lds_sync();
-        Elem r[kEpt];
+        T r[kEpt];
 #pragma unroll
         for (int m = 0; m < kEpt; ++m)
             r[m] = s[pidx(tid * kEpt + m)];
-        sort_regs(r);
+        sort_regs<F>(r);
         // Records sit at positions [0, n) and pads after them, so once the runs reach the power
         // of two p >= n the records are one sorted run; later rounds would only merge pads.
         int p = kEpt;
@@ -277,24 +400,40 @@ __global__ __launch_bounds__(kThreads) void block_sort_kernel(const int64_t *__r
             p <<= 1;
         for (int L = kEpt; L < p; L <<= 1) {
             lds_sync();                                  // every thread has read s
-            store_regs(s, r, tid * kEpt, kTile);
+            store_regs<F>(s, r, tid * kEpt, kTile);
             lds_sync();
             const int d = tid * kEpt;
             const int a_off = (d / (2 * L)) * (2 * L);
-            merge_ept(s, a_off, L, a_off + L, L, d - a_off, r);
+            merge_ept<F>(s, a_off, L, a_off + L, L, d - a_off, r);
         }
         lds_sync();
-        store_regs(s, r, tid * kEpt, kTile);
+        store_regs<F>(s, r, tid * kEpt, kTile);
         lds_sync();
-        emit(s, n, base, out, last, o.total, o.rows_in, o.row_chunks, o.keys_out, o.rows_out);
+        emit<F>(fm, s, n, base, kb, out, last, o);
         lds_sync();                                      // s is reused by the next tile
     }
+}
+
+__global__ __launch_bounds__(kThreads) void block_sort_kernel(const int64_t *__restrict__ keys,
+                                                              const int64_t *off, int32_t B,
+                                                              const int64_t *tile_off,
+                                                              void *out, SortOut o, Codec c) {
+    __shared__ __attribute__((aligned(16))) char lds[kLdsElems * sizeof(Wide::T)];
+    if (B <= 0)
+        return;
+    int64_t kmin;
+    if (use_packed(c, kmin))
+        block_sort_body(Packed{kmin, c.pbits}, lds, keys, off, B, tile_off, out, o);
+    else
+        block_sort_body(Wide{}, lds, keys, off, B, tile_off, out, o);
 }
 
 // Merge-path split: the number of A elements among the first d outputs of merge(A, B), i.e.
 // the smallest i in [lo, hi] such that A[i] is not among them. Run by all 64 lanes of one
 // wavefront (64 probes per round); returns the same value in every lane.
-__device__ int64_t split64(const Elem *A, int64_t la, const Elem *B, int64_t lb, int64_t d) {
+template <typename F>
+__device__ int64_t split64(const typename F::T *A, int64_t la, const typename F::T *B, int64_t lb,
+                           int64_t d) {
     int64_t lo = d > lb ? d - lb : 0;
     int64_t hi = d < la ? d : la;
     const int lane = threadIdx.x & 63;
@@ -304,7 +443,7 @@ __device__ int64_t split64(const Elem *A, int64_t la, const Elem *B, int64_t lb,
         const int64_t m = lo + lane * step;
         bool in_out = false;                     // A[m] is among the first d outputs
         if (m < hi)
-            in_out = first_le(A[m], B[d - 1 - m]);
+            in_out = first_le<F>(A[m], B[d - 1 - m]);
         const uint64_t ballot = __ballot(m < hi && !in_out);
         if (step == 1)
             return ballot ? lo + __builtin_ctzll(ballot) : hi;   // first false, else hi
@@ -322,18 +461,16 @@ __device__ int64_t split64(const Elem *A, int64_t la, const Elem *B, int64_t lb,
     return lo;
 }
 
-// Round r: within every viewer with more than 2^r tiles, merge runs of kTile << r records
-// pairwise from src into dst (a run without a partner is copied).
-__global__ __launch_bounds__(kThreads) void merge_kernel(const Elem *__restrict__ src,
-                                                         Elem *__restrict__ dst,
-                                                         const int64_t *off, int32_t B,
-                                                         const int64_t *tile_off, int r,
-                                                         SortOut o) {
-    __shared__ Elem s[kLdsElems];
-    __shared__ int64_t s_split[2];
+template <typename F>
+__device__ __forceinline__ void merge_body(const F &fm, char *lds, int64_t *s_split,
+                                           const void *src_v, void *dst_v, const int64_t *off,
+                                           int32_t B, const int64_t *tile_off, int r,
+                                           const SortOut &o) {
+    typedef typename F::T T;
+    T *s = reinterpret_cast<T *>(lds);
+    const T *src = static_cast<const T *>(src_v);
+    T *dst = static_cast<T *>(dst_v);
     const int tid = threadIdx.x;
-    if (B <= 0)
-        return;
     const int64_t n_tiles = tile_off[B];
     for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {   // uniform per workgroup
         const int64_t v = owner(tile_off, B, t);
@@ -352,11 +489,11 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const Elem *__restrict_
         const int64_t lb = max<int64_t>(0, min(run, n_seg - b0));
         const int64_t d0 = out0 - a0;
         const int64_t d1 = min<int64_t>(d0 + kTile, la + lb);
-        const Elem *A = src + kb + a0;
-        const Elem *Bv = src + kb + b0;
+        const T *A = src + kb + a0;
+        const T *Bv = src + kb + b0;
         if (tid < 64) {
-            const int64_t i0 = split64(A, la, Bv, lb, d0);
-            const int64_t i1 = split64(A, la, Bv, lb, d1);
+            const int64_t i0 = split64<F>(A, la, Bv, lb, d0);
+            const int64_t i1 = split64<F>(A, la, Bv, lb, d1);
             if (tid == 0) {
                 s_split[0] = i0;
                 s_split[1] = i1;
@@ -374,28 +511,47 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const Elem *__restrict_
         for (int i = tid; i < n; i += kThreads)
             s[pidx(i)] = i < na ? A[i0 + i] : Bv[j0 + (i - na)];
         lds_sync();
-        Elem rr[kEpt];
+        T rr[kEpt];
         const int d = tid * kEpt;
         if (d < n)
-            merge_ept(s, 0, na, na, nb, d, rr);
+            merge_ept<F>(s, 0, na, na, nb, d, rr);
         lds_sync();
         if (d < n)
-            store_regs(s, rr, d, n);
+            store_regs<F>(s, rr, d, n);
         lds_sync();
-        emit(s, n, kb + a0 + d0, dst, last, o.total, o.rows_in, o.row_chunks, o.keys_out,
-             o.rows_out);
+        emit<F>(fm, s, n, kb + a0 + d0, kb, dst, last, o);
         lds_sync();                                      // s and s_split are reused
     }
 }
 
+// Round r: within every viewer with more than 2^r tiles, merge runs of kTile << r records
+// pairwise from src into dst (a run without a partner is copied).
+__global__ __launch_bounds__(kThreads) void merge_kernel(const void *src, void *dst,
+                                                         const int64_t *off, int32_t B,
+                                                         const int64_t *tile_off, int r,
+                                                         SortOut o, Codec c) {
+    __shared__ __attribute__((aligned(16))) char lds[kLdsElems * sizeof(Wide::T)];
+    __shared__ int64_t s_split[2];
+    if (B <= 0)
+        return;
+    int64_t kmin;
+    if (use_packed(c, kmin))
+        merge_body(Packed{kmin, c.pbits}, lds, s_split, src, dst, off, B, tile_off, r, o);
+    else
+        merge_body(Wide{}, lds, s_split, src, dst, off, B, tile_off, r, o);
+}
+
 int64_t round_up(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+constexpr int kRangeSlots = 1024;   // range_kernel workgroups at most
 
 }  // namespace
 
 int64_t sort_workspace_bytes(int64_t total, int32_t n_viewers) {
     if (total <= 0 || n_viewers <= 0)
         return 0;
-    return 2 * round_up(total * (int64_t)sizeof(Elem)) + round_up((n_viewers + 1) * 8);
+    return 2 * round_up(total * (int64_t)sizeof(Wide::T)) + round_up((n_viewers + 1) * 8) + 256 +
+           round_up(2 * kRangeSlots * 8);
 }
 
 hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
@@ -404,34 +560,50 @@ hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int6
     if (total <= 0 || n_viewers <= 0)
         return hipSuccess;
     uint8_t *w = static_cast<uint8_t *>(workspace);
-    Elem *buf0 = reinterpret_cast<Elem *>(w);
-    Elem *buf1 = reinterpret_cast<Elem *>(w + round_up(total * (int64_t)sizeof(Elem)));
-    int64_t *tile_off = reinterpret_cast<int64_t *>(w + 2 * round_up(total * (int64_t)sizeof(Elem)));
+    const int64_t buf_bytes = round_up(total * (int64_t)sizeof(Wide::T));
+    void *buf0 = w;
+    void *buf1 = w + buf_bytes;
+    int64_t *tile_off = reinterpret_cast<int64_t *>(w + 2 * buf_bytes);
+    int64_t *range = reinterpret_cast<int64_t *>(w + 2 * buf_bytes + round_up((n_viewers + 1) * 8));
+    int64_t *slots = range + 32;                       // 256 bytes after range
     // Upper bound on tiles (every viewer adds at most one partial tile); larger counts are
     // covered by the kernels' grid-stride loops.
     int64_t grid = (total + kTile - 1) / kTile + n_viewers;
     if (grid > (1 << 20))
         grid = 1 << 20;
-    const int64_t per_viewer = max_keys > 0 ? ((max_keys < total ? max_keys : total) + kTile - 1) / kTile
-                                            : (total + kTile - 1) / kTile;
+    const int64_t largest = max_keys > 0 ? (max_keys < total ? max_keys : total) : total;
+    const int64_t per_viewer = (largest + kTile - 1) / kTile;
     int rounds = 0;
     while (((int64_t)1 << rounds) < per_viewer)
         ++rounds;
+    // Position bits of a packed element: enough for the largest viewer.
+    int32_t pbits = 1;
+    while (((int64_t)1 << pbits) < largest)
+        ++pbits;
+    const Codec c{range, pbits};
     const SortOut o{total, static_cast<const chunk_t *>(rows_in), row_bytes / 16, keys_out,
                     static_cast<chunk_t *>(rows_out)};
-    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kThreads), 0, stream, key_offsets, n_viewers,
-                       total, tile_off);
+    int64_t n_slots = (total + kRangeThreads * kRangeUnroll - 1) / (kRangeThreads * kRangeUnroll);
+    if (n_slots > kRangeSlots)
+        n_slots = kRangeSlots;
+    hipLaunchKernelGGL(range_kernel, dim3((unsigned)n_slots), dim3(kRangeThreads), 0, stream,
+                       keys_in, total, slots);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess) {
+        hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kThreads), 0, stream, key_offsets,
+                           n_viewers, total, tile_off, slots, (int)n_slots, range);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess) {
         hipLaunchKernelGGL(block_sort_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream,
-                           keys_in, key_offsets, n_viewers, tile_off, buf0, o);
+                           keys_in, key_offsets, n_viewers, tile_off, buf0, o, c);
         e = hipGetLastError();
     }
     for (int r = 0; e == hipSuccess && r < rounds; ++r) {
-        const Elem *src = (r & 1) ? buf1 : buf0;
-        Elem *dst = (r & 1) ? buf0 : buf1;
+        const void *src = (r & 1) ? buf1 : buf0;
+        void *dst = (r & 1) ? buf0 : buf1;
         hipLaunchKernelGGL(merge_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream, src, dst,
-                           key_offsets, n_viewers, tile_off, r, o);
+                           key_offsets, n_viewers, tile_off, r, o, c);
         e = hipGetLastError();
     }
     return e;

@@ -119,3 +119,20 @@ def test_sort_then_join_equals_oracle():
         assert np.array_equal(out.cpu().numpy(), want[0]) and np.array_equal(hit.cpu().numpy(), want[1])
     finally:
         P.cc_store_destroy(store)
+
+
+def test_key_span_at_the_packed_limit():
+    """Records whose keys span just under, and exactly at, the limit of the 8-byte element form
+    (2^(64 - b) - 1 for b position bits): the first is sorted packed, the second wide; both
+    must match the oracle."""
+    note("sort: key span at the packed limit")
+    n = 1000                                     # b = 10 position bits
+    g = W.gen("cpu", 5, 3)
+    rows = torch.randint(0, 256, (n, 16), generator=g, dtype=torch.int64).to(torch.uint8)
+    for span in ((1 << 54) - 2, (1 << 54) - 1, (1 << 63) - 1):
+        base = -(1 << 62)
+        keys = base + torch.randint(0, 50, (n,), generator=g) * (span // 49)
+        keys[0], keys[1] = base, base + span    # the span is exact
+        keys[2:6] = base + span // 2            # repeats
+        _check(torch.tensor([0, n]), keys, rows, f"span {span}")
+        _check(torch.tensor([0, n]), keys, rows, f"span {span} with hint", max_keys=n)

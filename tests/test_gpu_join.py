@@ -362,3 +362,46 @@ def test_outputs_overlapping_inputs_are_rejected():
         torch.cuda.synchronize()
     finally:
         P.cc_store_destroy(store)
+
+
+@pytest.mark.parametrize("tuning", [None, (1, 4096, 0), (4, 0, 0), (16, 8, 0), (0, 2, 0)])
+def test_unsorted_keys_stay_in_bounds(tuning):
+    """Keys out of order give an unspecified result, but every access stays in bounds and the
+    output is consistent: doc segments are exact, a miss carries the default row and hit 0,
+    and a hit carries one of the same viewer's edge rows."""
+    note(f"unsorted keys, tuning {tuning}")
+    for seed in range(12):
+        tc = W.tiny_case(9100 + seed, max_k=120, max_n=400, max_viewers=4, n_lookups=1,
+                         dup_keys=False)
+        b = tc.batch
+        ko = b.key_offsets.tolist()
+        g = W.gen("cpu", seed, 11)
+        keys = b.keys.clone()
+        for v in range(len(ko) - 1):
+            if ko[v + 1] > ko[v]:
+                keys[ko[v]:ko[v + 1]] = keys[ko[v]:ko[v + 1]][
+                    torch.randperm(ko[v + 1] - ko[v], generator=g)]
+        ub = W.Batch(b.cand_offsets, b.cand_idx, b.key_offsets, keys, b.edge_rows, None)
+        wd, we = row_bytes(tc.doc_rows), row_bytes(b.edge_rows)
+        store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+        try:
+            d = None if tc.default_row is None else tc.default_row.to(DEV)
+            out, hit = gpu_join(store, None, ub.to(DEV), wd, we, 1, default_row=d,
+                                tuning=_tuning(tuning))
+        finally:
+            P.cc_store_destroy(store)
+        want, _, _ = oracle_join(tc.author_id, tc.doc_rows, b, 1, default_row=tc.default_row)
+        assert np.array_equal(out[:, :wd], want[:, :wd]), f"seed {seed}: doc segments"
+        assert set(np.unique(hit).tolist()) <= {0, 1}
+        default = (np.zeros(we, np.uint8) if tc.default_row is None
+                   else tc.default_row.numpy())
+        edge = b.edge_rows.numpy().reshape(b.edge_rows.shape[0], -1).view(np.uint8)
+        co = b.cand_offsets.tolist()
+        for v in range(len(co) - 1):
+            rows_v = {bytes(r) for r in edge[ko[v]:ko[v + 1]]}
+            for j in range(co[v], co[v + 1]):
+                seg = out[j, wd:wd + we]
+                if hit[j, 0]:
+                    assert bytes(seg) in rows_v, f"seed {seed}: hit row from another viewer"
+                else:
+                    assert np.array_equal(seg, default), f"seed {seed}: miss row"

@@ -211,6 +211,10 @@ def index_workloads(torch, P, W, dev, seed):
                       "ms_median": med, "ms_mean": mean, "ids_per_s": m / (med / 1e3),
                       "algorithmic_bytes": alg, "hbm_gbps": alg / (med / 1e3) / 1e9,
                       "hbm_frac_of_peak": alg / (med / 1e3) / 1e9 / PEAK_GBPS}
+    # One request end to end on the same index: 50,000 ids resolved (Eq. 6), then joined (Eq. 1)
+    # against one viewer's 5,000 keys; eagerly, and replayed from a captured HIP graph (the two
+    # launches without their host-side launch cost).
+    res.update(request_latency(torch, P, W, dev, seed, store, spec))
     # §6.2 ingestion: bootstrap-size batches, then steady-state batches (a third of the size)
     next_item = n
     for tag, size, count in (("upsert", spec.upsert_batch, 10),
@@ -239,6 +243,50 @@ def index_workloads(torch, P, W, dev, seed):
     P.cc_store_destroy(store)
     torch.cuda.empty_cache()
     return res
+
+
+def request_latency(torch, P, W, dev, seed, store, spec, calls=400):
+    n, k = spec.ids_per_request, 5000
+    g = W.gen(dev, seed, 40)
+    items = torch.randint(0, spec.n_index + spec.n_index // 50, (n,), generator=g, device=dev)
+    q = W.doc_ids(items, seed)
+    pos = torch.empty_like(q)
+    keys = torch.sort(torch.randperm(spec.n_authors, generator=g, device=dev)[:k]).values
+    edge = torch.randn(k, 32, generator=g, device=dev).to(torch.bfloat16)
+    out = torch.empty(n, spec.row_cols * 2 + 64, dtype=torch.uint8, device=dev)
+    hit = torch.empty(n, 1, dtype=torch.int8, device=dev)
+
+    def request():
+        P.cc_resolve_ids(store, q, pos)
+        P.cc_join(store, pos, keys, edge, out, hit)
+
+    def percentiles(fn):
+        for _ in range(10):
+            fn()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(calls)]
+        for a, b in evs:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        ms = sorted(a.elapsed_time(b) for a, b in evs)
+        return ms[len(ms) // 2], ms[int(len(ms) * 0.99)]
+
+    eager = percentiles(request)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(graph, stream=s):
+            request()
+    torch.cuda.synchronize()
+    replay = percentiles(graph.replay)
+    return {"request-eager": {"entry": "cc_resolve_ids + cc_join", "ids": n, "keys": k,
+                              "ms_median": eager[0], "p99_ms": eager[1]},
+            "request-graph": {"entry": "cc_resolve_ids + cc_join, replayed HIP graph", "ids": n,
+                              "keys": k, "ms_median": replay[0], "p99_ms": replay[1]}}
 
 
 def kernel_hash():

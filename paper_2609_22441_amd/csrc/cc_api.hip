@@ -136,12 +136,14 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
             overlaps(outs[1].p, outs[1].n, outs[2].p, outs[2].n))
             return CC_ERR_INVALID_ARGUMENT;
     }
-    int32_t lds_cap = ccj::kDefaultLdsKeys, stride = 0, wgs = 0, budget = 4;
+    // Up to 16 fences per candidate of a segment: a larger table costs bulk reads from L2,
+    // while a longer window between fences costs every lookup another dependent line.
+    int32_t lds_cap = ccj::kDefaultLdsKeys, stride = 0, wgs = 0;
+    const int32_t budget = 16;
     bool one_wave = false;
     const int64_t viewers = cand_offsets ? n_viewers : 1;
     if (viewers > 0 && total_keys / viewers > ccj::kLongListKeys) {
         lds_cap = ccj::kMaxLdsKeys;
-        budget = 16;
         one_wave = true;
     }
     if (tuning) {

@@ -11,9 +11,9 @@ constexpr int kWindow = 15;          // keys between two fences read from L2 in 
 constexpr int kMaxLdsKeys = 18432;   // LDS key table limit: 144 KiB + at most 12 KiB of static
                                      // tables stays within the 160 KiB a workgroup may use
 constexpr int kDefaultLdsKeys = 8192;   // 64 KiB: within the register-limited occupancy
-// Average key-list length above which a launch uses the whole LDS table, one resident wave of
-// workgroups (one per CU) and a larger fence budget: staging more fences per workgroup keeps
-// each lookup's window of keys within one 64-byte sector.
+// Average key-list length above which a launch uses the whole LDS table and one resident wave
+// of workgroups (one per CU): the larger table keeps each lookup's window of keys within one
+// 64-byte sector, and one wave leaves no half-empty last wave.
 constexpr int64_t kLongListKeys = 4 * (int64_t)kDefaultLdsKeys;
 constexpr int kZeroRowBytes = 1024;    // >= the widest row of a compile-time specialisation
 

@@ -405,3 +405,24 @@ def test_unsorted_keys_stay_in_bounds(tuning):
                     assert bytes(seg) in rows_v, f"seed {seed}: hit row from another viewer"
                 else:
                     assert np.array_equal(seg, default), f"seed {seed}: miss row"
+
+
+def test_thousands_of_small_viewers():
+    """3,000 viewers with 0 to 40 candidates and 0 to 60 keys each (many workgroups cross
+    several viewers): bit-exact with the oracle."""
+    note("3,000 small viewers")
+    g = W.gen("cpu", 31, 4)
+    n_docs = 5000
+    author = torch.randint(0, 2000, (n_docs,), generator=g)
+    doc = torch.randint(0, 256, (n_docs, 32), generator=g, dtype=torch.int64).to(torch.uint8)
+    reqs = []
+    for v in range(3000):
+        k = int(torch.randint(0, 61, (1,), generator=g))
+        keys = torch.sort(torch.randperm(2000, generator=g)[:k]).values
+        edge = torch.randint(0, 256, (k, 16), generator=g, dtype=torch.int64).to(torch.uint8)
+        n = int(torch.randint(0, 41, (1,), generator=g))
+        cand = torch.randint(-1, n_docs + 1, (n,), generator=g)
+        reqs.append(W.Request(keys, edge, cand, None))
+    tc = W.TinyCase(author, doc, W.pack(reqs), None, 1)
+    for t in (None, (4, 0, 0), (0, 0, 8)):
+        _tiny(tc, t, what=f"3000 viewers tuning {t}")

@@ -331,3 +331,20 @@ def test_wide_author_id_switches_the_column():
             ix2.close()
     finally:
         ix.close()
+
+
+def test_batch_of_one_repeated_id():
+    """10,000 records with the same new id, then 10,000 with one stored id: one position, and
+    the last record's row and author win."""
+    note("map: one id repeated")
+    ix = DeviceIndex(8, 16)
+    try:
+        one = torch.full((10_000,), 1234567, dtype=torch.int64)
+        rows = (torch.arange(10_000 * 16, dtype=torch.int64) % 251).to(torch.uint8).reshape(-1, 16)
+        assert ix.upsert(one, torch.arange(10_000), rows) == (1, 0)
+        ix.check_state("repeated new id")
+        assert ix.upsert(one, torch.arange(10_000) + 7, rows.flip(0)) == (0, 0)
+        ix.check_state("repeated stored id")
+        ix.resolve(torch.tensor([1234567, 7654321]), "repeated id")
+    finally:
+        ix.close()

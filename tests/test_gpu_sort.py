@@ -136,3 +136,17 @@ def test_key_span_at_the_packed_limit():
         keys[2:6] = base + span // 2            # repeats
         _check(torch.tensor([0, n]), keys, rows, f"span {span}")
         _check(torch.tensor([0, n]), keys, rows, f"span {span} with hint", max_keys=n)
+
+
+def test_thousands_of_small_viewers():
+    """5,000 viewers of 0 to 40 records: the tile plan scans the viewers in several chunks and
+    every tile finds its viewer by search."""
+    note("sort: 5,000 small viewers")
+    g = W.gen("cpu", 21, 3)
+    sizes = torch.randint(0, 41, (5000,), generator=g)
+    sizes[::97] = 0
+    ko = torch.cat([torch.zeros(1, dtype=torch.int64), torch.cumsum(sizes, 0)])
+    n = int(ko[-1])
+    keys = torch.randint(-50, 50, (n,), generator=g)
+    rows = torch.randint(0, 256, (n, 16), generator=g, dtype=torch.int64).to(torch.uint8)
+    _check(ko, keys, rows, "5000 viewers")

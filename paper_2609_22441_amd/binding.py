@@ -1,8 +1,10 @@
 """ctypes binding of libccjoin.so: argument marshalling only.
 
-Tensor arguments are anything with ``data_ptr()``, ``numel()``, ``element_size()`` and
-``shape`` (torch tensors in practice); plain integers are taken as raw device pointers. The
-stream defaults to torch's current stream on the current device.
+Tensor arguments are torch tensors. Before a call, each one is checked for what the C ABI
+cannot see behind a pointer: element type, dense layout, enough elements for the sizes passed
+with it, and GPU memory. A failed check raises ValueError or TypeError and nothing is enqueued.
+Plain integers in place of 1-D arrays are taken as raw device pointers and are not checked.
+The stream defaults to torch's current stream on the current device.
 """
 from __future__ import annotations
 
@@ -105,14 +107,6 @@ def _check(status: int, where: str):
         raise CCError(status, where)
 
 
-def _ptr(x) -> Optional[int]:
-    if x is None:
-        return None
-    if isinstance(x, int):
-        return x
-    return x.data_ptr()
-
-
 def _stream(stream) -> Optional[int]:
     if stream is None:
         import torch
@@ -129,18 +123,144 @@ def _prod(xs):
     return p
 
 
-def _out_stride(out) -> int:
-    return out.stride(0) * out.element_size()
+# ---- checks the C ABI cannot make ----
+# The library receives plain pointers. A host pointer, a buffer shorter than the sizes passed
+# with it, or a strided view would reach a kernel as an out-of-bounds or unmapped access, so
+# every tensor argument is checked here before the call: element type, dense layout, length
+# and GPU residency. Offsets and keys held in device memory are not read here; the kernels
+# clamp them.
+
+def _fail(name: str, what: str, exc=ValueError):
+    raise exc(f"{name}: {what}")
+
+
+_DTYPES = None
+
+
+def _i64():
+    global _DTYPES
+    if _DTYPES is None:
+        import torch
+        _DTYPES = (torch.int64, torch.int8)
+    return _DTYPES[0]
+
+
+def _i8():
+    _i64()
+    return _DTYPES[1]
+
+
+def _row_bytes(x) -> int:
+    """Bytes per row (dim 0 indexes rows; the trailing dims make up a row)."""
+    if x.dim() == 2:
+        return x.shape[1] * x.element_size()
+    return _prod(x.shape[1:]) * x.element_size()
+
+
+def _dense_from(x, d: int) -> bool:
+    """Dims d.. of x are laid out row-major without gaps."""
+    expect = 1
+    for size, st in zip(reversed(x.shape[d:]), reversed(x.stride()[d:])):
+        if size != 1 and st != expect:
+            return False
+        expect *= size
+    return True
+
+
+def _arr(x, name: str, dtype=None, numel: int = 0, optional: bool = False,
+         gpu: bool = True) -> Optional[int]:
+    """Pointer of a dense array of at least `numel` elements of `dtype`, in GPU memory unless
+    `gpu` is False. None is allowed when `optional` or nothing is needed; an int is a raw device
+    pointer and is passed through unchecked."""
+    if x is None:
+        if optional or numel == 0:
+            return None
+        _fail(name, "is required")
+    if isinstance(x, int):
+        return x
+    if ((dtype is not None and x.dtype != dtype) or not x.is_contiguous()
+            or x.numel() < numel or (gpu and not x.is_cuda)):
+        if dtype is not None and x.dtype != dtype:
+            _fail(name, f"must be {dtype} (is {x.dtype})", TypeError)
+        if not x.is_contiguous():
+            _fail(name, "must be contiguous")
+        if x.numel() < numel:
+            _fail(name, f"needs at least {numel} elements (has {x.numel()})")
+        _fail(name, f"must be in GPU memory (is on {x.device})")
+    return x.data_ptr()
+
+
+def _bytes_arr(x, name: str, nbytes: int) -> Optional[int]:
+    """Device pointer of a dense buffer of at least `nbytes` bytes (any element type), or None."""
+    if x is None or isinstance(x, int):
+        return x
+    if x.numel() * x.element_size() < nbytes:
+        _fail(name, f"needs at least {nbytes} bytes (has {x.numel() * x.element_size()})")
+    return _arr(x, name)
+
+
+def _rows(x, name: str, n: int, row_bytes: Optional[int] = None) -> Optional[int]:
+    """Device pointer of a dense [>= n, ...] array of rows (of `row_bytes` bytes, if given)."""
+    if x is None:
+        if n == 0:
+            return None
+        _fail(name, "is required")
+    if x.dim() < 1 or x.shape[0] < n:
+        _fail(name, f"needs at least {n} rows (shape {tuple(x.shape)})")
+    if row_bytes is not None and _row_bytes(x) != row_bytes:
+        _fail(name, f"rows must be {row_bytes} bytes (are {_row_bytes(x)})")
+    return _arr(x, name)
+
+
+def _out_rows(out, name: str, n: int, width: int, per_group: int = 0):
+    """(pointer, row stride in bytes) of an output of n rows whose rows may sit inside a wider
+    tensor. Each row (the trailing dims) must be dense and hold `width` bytes. With per_group,
+    a 3-D output [groups, per_group, row] is addressed as groups * per_group rows, so its outer
+    stride must equal per_group row strides."""
+    if out.dim() == 2 and out.stride(1) == 1:
+        # the common case: [rows, bytes-per-row] with any row stride
+        rows, rb, stride = out.shape[0], out.shape[1] * out.element_size(), out.stride(0)
+    else:
+        lead = 1
+        if out.dim() == 3 and per_group:
+            lead = 2
+            if out.shape[1] != per_group:
+                _fail(name, f"dim 1 must be n_max = {per_group} (shape {tuple(out.shape)})")
+            if out.shape[0] > 1 and out.stride(0) != per_group * out.stride(1):
+                _fail(name, "must address its slots with one row stride")
+        if out.dim() <= lead or not _dense_from(out, lead):
+            _fail(name, "rows must be dense (the trailing dims contiguous)")
+        rows = _prod(out.shape[:lead])
+        rb = _prod(out.shape[lead:]) * out.element_size()
+        stride = out.stride(lead - 1)
+    if rows < n:
+        _fail(name, f"needs at least {n} rows (shape {tuple(out.shape)})")
+    if rb < width:
+        _fail(name, f"rows must hold at least {width} bytes (hold {rb})")
+    if not out.is_cuda:
+        _fail(name, f"must be in GPU memory (is on {out.device})")
+    return out.data_ptr(), stride * out.element_size()
+
+
+def _doc_row_bytes(store: int) -> int:
+    return cc_store_info(store)[1]
 
 
 def cc_store_create(author_ids, doc_rows, stream=None) -> int:
-    """Copy (author_ids [n] int64, doc_rows [n, ...]) into a new device store; returns its handle."""
+    """Copy (author_ids [n] int64, doc_rows [n, ...]) into a new device store; returns its handle.
+    Both are host tensors or both are GPU tensors."""
     n = author_ids.numel()
-    flags = CC_SRC_DEVICE if getattr(author_ids, "is_cuda", False) else CC_SRC_HOST
+    on_gpu = bool(author_ids.is_cuda)
+    if bool(doc_rows.is_cuda) != on_gpu:
+        _fail("doc_rows", "must be in the same memory (host or GPU) as author_ids")
+    if doc_rows.dim() < 1 or doc_rows.shape[0] != n:
+        _fail("doc_rows", f"needs {n} rows, one per author id (shape {tuple(doc_rows.shape)})")
+    pa = _arr(author_ids, "author_ids", _i64(), gpu=on_gpu)
+    pr = _arr(doc_rows, "doc_rows", gpu=on_gpu)
+    flags = CC_SRC_DEVICE if on_gpu else CC_SRC_HOST
     h = ctypes.c_void_p()
-    _check(lib().cc_store_create(ctypes.byref(h), n, _ptr(author_ids), _ptr(doc_rows),
-                                 int(_prod(doc_rows.shape[1:])) * doc_rows.element_size(),
-                                 flags, _stream(stream)), "cc_store_create")
+    _check(lib().cc_store_create(ctypes.byref(h), n, pa, pr, _row_bytes(doc_rows), flags,
+                                 _stream(stream)), "cc_store_create")
     return h.value
 
 
@@ -160,25 +280,33 @@ def cc_store_upsert(store: int, doc_ids, author_ids, doc_rows, workspace, stream
     """Apply one ingestion batch (§6.2); returns (n_new, n_rejected). Synchronises the stream.
     Raises CCError with status CC_ERR_STORE_FULL (store unchanged) when the batch does not fit."""
     n = doc_ids.numel()
-    nn, nr = ctypes.c_int64(), ctypes.c_int64()
+    pi = _arr(doc_ids, "doc_ids", _i64())
+    pa = _arr(author_ids, "author_ids", _i64(), n)
+    pr = _rows(doc_rows, "doc_rows", n, _doc_row_bytes(store))
+    pw = _arr(workspace, "workspace", optional=True)
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    _check(lib().cc_store_upsert(store, n, _ptr(doc_ids), _ptr(author_ids), _ptr(doc_rows),
-                                 _ptr(workspace), ws_bytes, ctypes.byref(nn), ctypes.byref(nr),
-                                 _stream(stream)), "cc_store_upsert")
+    nn, nr = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().cc_store_upsert(store, n, pi, pa, pr, pw, ws_bytes, ctypes.byref(nn),
+                                 ctypes.byref(nr), _stream(stream)), "cc_store_upsert")
     return nn.value, nr.value
 
 
 def cc_store_read(store: int, first: int, count: int, author_out=None, rows_out=None,
                   stream=None) -> None:
     """Copy positions [first, first + count) of the store into device buffers."""
-    _check(lib().cc_store_read(store, first, count, _ptr(author_out), _ptr(rows_out),
-                               _stream(stream)), "cc_store_read")
+    n = max(int(count), 0)
+    pa = _arr(author_out, "author_out", _i64(), n, optional=True)
+    pr = None if rows_out is None else _bytes_arr(rows_out, "rows_out",
+                                                  n * _doc_row_bytes(store))
+    _check(lib().cc_store_read(store, first, count, pa, pr, _stream(stream)), "cc_store_read")
 
 
 def cc_resolve_ids(store: int, doc_ids, positions, stream=None) -> None:
     """Eq. 6 (§6.3.1): positions[i] = store position of doc_ids[i], or -1."""
-    _check(lib().cc_resolve_ids(store, _ptr(doc_ids), doc_ids.numel(), _ptr(positions),
-                                _stream(stream)), "cc_resolve_ids")
+    n = doc_ids.numel()
+    pi = _arr(doc_ids, "doc_ids", _i64())
+    pp = _arr(positions, "positions", _i64(), n)
+    _check(lib().cc_resolve_ids(store, pi, n, pp, _stream(stream)), "cc_resolve_ids")
 
 
 def cc_store_destroy(store: int) -> None:
@@ -210,13 +338,43 @@ def cc_store_reset_invalid_count(store: int, stream=None) -> None:
            "cc_store_reset_invalid_count")
 
 
+def _edge_args(edge_keys, edge_feats, tk: int, default_row):
+    """Checked pointers (keys, rows, default row) and the edge row width in bytes."""
+    pk = _arr(edge_keys, "edge_keys", _i64(), tk)
+    ew = _row_bytes(edge_feats)
+    pf = _rows(edge_feats, "edge_feats", tk)
+    pd = _bytes_arr(default_row, "default_row", ew)
+    return pk, pf, pd, ew
+
+
 def cc_join(store: int, cand_idx, edge_keys, edge_feats, out, hit_mask, default_row=None,
             stream=None) -> None:
     """One viewer (see include/cc_join.h). out is [n_cand, >= doc+edge bytes] (any dtype)."""
-    ew = int(_prod(edge_feats.shape[1:])) * edge_feats.element_size()
-    _check(lib().cc_join(store, _ptr(cand_idx), cand_idx.numel(), _ptr(edge_keys),
-                         edge_keys.numel(), _ptr(edge_feats), ew, _ptr(default_row), _ptr(out),
-                         _out_stride(out), _ptr(hit_mask), _stream(stream)), "cc_join")
+    n = cand_idx.numel()
+    pc = _arr(cand_idx, "cand_idx", _i64())
+    pk, pf, pd, ew = _edge_args(edge_keys, edge_feats, edge_keys.numel(), default_row)
+    po, stride = _out_rows(out, "out", n, _doc_row_bytes(store) + ew)
+    ph = _arr(hit_mask, "hit_mask", _i8(), n)
+    _check(lib().cc_join(store, pc, n, pk, edge_keys.numel(), pf, ew, pd, po, stride, ph,
+                         _stream(stream)), "cc_join")
+
+
+def _batched_args(store, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats,
+                  default_row, extra_keys, total_cand, total_keys):
+    """Checked inputs of the batched joins: (B, L, pointers..., extra array, edge width)."""
+    n_lookups = 1 + (len(extra_keys) if extra_keys else 0)
+    B = cand_offsets.numel() - 1
+    tc = cand_idx.numel() if total_cand is None else int(total_cand)
+    tk = edge_keys.numel() if total_keys is None else int(total_keys)
+    pco = _arr(cand_offsets, "cand_offsets", _i64(), 1)
+    pko = _arr(key_offsets, "key_offsets", _i64(), B + 1)
+    pc = _arr(cand_idx, "cand_idx", _i64(), tc)
+    pk, pf, pd, ew = _edge_args(edge_keys, edge_feats, tk, default_row)
+    ex = None
+    if extra_keys:
+        ex = (ctypes.c_void_p * len(extra_keys))(
+            *[_arr(e, f"extra_keys[{i}]", _i64(), tc) for i, e in enumerate(extra_keys)])
+    return B, n_lookups, tc, tk, pco, pc, pko, pk, pf, pd, ex, ew
 
 
 def cc_join_batched(store: int, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats, out,
@@ -224,16 +382,12 @@ def cc_join_batched(store: int, cand_offsets, cand_idx, key_offsets, edge_keys, 
                     total_cand: Optional[int] = None, total_keys: Optional[int] = None,
                     tuning: Optional[Tuning] = None, stream=None) -> None:
     """B viewers in CSR form, 1 + len(extra_keys) lookups (see include/cc_join.h)."""
-    n_lookups = 1 + (len(extra_keys) if extra_keys else 0)
-    ex = None
-    if extra_keys:
-        ex = (ctypes.c_void_p * len(extra_keys))(*[_ptr(e) for e in extra_keys])
-    ew = int(_prod(edge_feats.shape[1:])) * edge_feats.element_size()
-    tc = cand_idx.numel() if total_cand is None else total_cand
-    tk = edge_keys.numel() if total_keys is None else total_keys
-    args = (store, cand_offsets.numel() - 1, _ptr(cand_offsets), _ptr(cand_idx), tc,
-            _ptr(key_offsets), _ptr(edge_keys), tk, _ptr(edge_feats), ew, _ptr(default_row),
-            n_lookups, ex, _ptr(out), _out_stride(out), _ptr(hit_mask))
+    B, L, tc, tk, pco, pc, pko, pk, pf, pd, ex, ew = _batched_args(
+        store, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats, default_row,
+        extra_keys, total_cand, total_keys)
+    po, stride = _out_rows(out, "out", tc, _doc_row_bytes(store) + L * ew)
+    ph = _arr(hit_mask, "hit_mask", _i8(), tc * L)
+    args = (store, B, pco, pc, tc, pko, pk, tk, pf, ew, pd, L, ex, po, stride, ph)
     if tuning is None:
         _check(lib().cc_join_batched(*args, _stream(stream)), "cc_join_batched")
     else:
@@ -246,20 +400,19 @@ def cc_join_batched_padded(store: int, cand_offsets, cand_idx, key_offsets, edge
                            extra_keys: Optional[Sequence] = None,
                            total_cand: Optional[int] = None, total_keys: Optional[int] = None,
                            stream=None) -> None:
-    """B viewers written into the padded [B, n_max] layout (see include/cc_join.h)."""
-    n_lookups = 1 + (len(extra_keys) if extra_keys else 0)
-    ex = None
-    if extra_keys:
-        ex = (ctypes.c_void_p * len(extra_keys))(*[_ptr(e) for e in extra_keys])
-    ew = int(_prod(edge_feats.shape[1:])) * edge_feats.element_size()
-    tc = cand_idx.numel() if total_cand is None else total_cand
-    tk = edge_keys.numel() if total_keys is None else total_keys
-    stride = out.stride(-2) * out.element_size() if out.dim() == 3 else _out_stride(out)
-    _check(lib().cc_join_batched_padded(
-        store, cand_offsets.numel() - 1, _ptr(cand_offsets), _ptr(cand_idx), tc,
-        _ptr(key_offsets), _ptr(edge_keys), tk, _ptr(edge_feats), ew, _ptr(default_row),
-        n_lookups, ex, n_max, _ptr(out), stride, _ptr(hit_mask), _ptr(valid_mask),
-        _stream(stream)), "cc_join_batched_padded")
+    """B viewers written into the padded [B, n_max] layout (see include/cc_join.h). out is
+    [B, n_max, >= row bytes] or [B * n_max, >= row bytes]."""
+    B, L, tc, tk, pco, pc, pko, pk, pf, pd, ex, ew = _batched_args(
+        store, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats, default_row,
+        extra_keys, total_cand, total_keys)
+    slots = max(B, 0) * max(int(n_max), 0)
+    po, stride = _out_rows(out, "out", slots, _doc_row_bytes(store) + L * ew,
+                           per_group=max(int(n_max), 0))
+    ph = _arr(hit_mask, "hit_mask", _i8(), slots * L)
+    pv = _arr(valid_mask, "valid_mask", _i8(), slots)
+    _check(lib().cc_join_batched_padded(store, B, pco, pc, tc, pko, pk, tk, pf, ew, pd, L, ex,
+                                        n_max, po, stride, ph, pv, _stream(stream)),
+           "cc_join_batched_padded")
 
 
 def cc_sort_workspace_bytes(total_keys: int, n_viewers: int) -> int:
@@ -269,21 +422,28 @@ def cc_sort_workspace_bytes(total_keys: int, n_viewers: int) -> int:
 def cc_sort_affinity(key_offsets, keys_in, rows_in, keys_out, rows_out, workspace,
                      max_keys: int = 0, total_keys: Optional[int] = None, stream=None) -> None:
     """Stable per-viewer sort of affinity records (Alg. 1 Step 1; see include/cc_join.h)."""
-    tk = keys_in.numel() if total_keys is None else total_keys
-    rb = int(_prod(rows_in.shape[1:])) * rows_in.element_size()
+    B = key_offsets.numel() - 1
+    tk = keys_in.numel() if total_keys is None else int(total_keys)
+    rb = _row_bytes(rows_in)
+    pko = _arr(key_offsets, "key_offsets", _i64(), 1)
+    pki = _arr(keys_in, "keys_in", _i64(), tk)
+    pri = _rows(rows_in, "rows_in", tk)
+    pk = _arr(keys_out, "keys_out", _i64(), tk)
+    pr = _rows(rows_out, "rows_out", tk, rb)
+    pw = _arr(workspace, "workspace")
     ws_bytes = workspace.numel() * workspace.element_size()
-    _check(lib().cc_sort_affinity(key_offsets.numel() - 1, _ptr(key_offsets), _ptr(keys_in),
-                                  _ptr(rows_in), rb, tk, max_keys, _ptr(keys_out),
-                                  _ptr(rows_out), _ptr(workspace), ws_bytes, _stream(stream)),
-           "cc_sort_affinity")
+    _check(lib().cc_sort_affinity(B, pko, pki, pri, rb, tk, max_keys, pk, pr, pw, ws_bytes,
+                                  _stream(stream)), "cc_sort_affinity")
 
 
 def cc_validate_keys(key_offsets, edge_keys, total_keys: Optional[int] = None, stream=None):
     """Returns -1 when every viewer's keys are strictly increasing, else the first bad viewer."""
     bad = ctypes.c_int64()
-    tk = edge_keys.numel() if total_keys is None else total_keys
-    st = lib().cc_validate_keys(_ptr(key_offsets), _ptr(edge_keys), key_offsets.numel() - 1, tk,
-                                ctypes.byref(bad), _stream(stream))
+    tk = edge_keys.numel() if total_keys is None else int(total_keys)
+    pko = _arr(key_offsets, "key_offsets", _i64(), 1)
+    pk = _arr(edge_keys, "edge_keys", _i64(), tk)
+    st = lib().cc_validate_keys(pko, pk, key_offsets.numel() - 1, tk, ctypes.byref(bad),
+                                _stream(stream))
     if st == CC_ERR_UNSORTED_KEYS:
         return bad.value
     _check(st, "cc_validate_keys")

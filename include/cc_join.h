@@ -110,7 +110,8 @@ CC_API cc_status cc_store_layout(const cc_store *store, int32_t *author_id_bytes
  * store have met since creation or the last reset. Synchronises `stream` (debug/metrics). */
 CC_API cc_status cc_store_invalid_count(const cc_store *store, int64_t *count, hipStream_t stream);
 
-/* Reset that counter to zero, ordered on `stream` (no synchronisation). */
+/* Reset that counter to zero, ordered on `stream` (no synchronisation). A kernel clears it, so
+ * the call may be captured into a HIP graph. Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_DEVICE. */
 CC_API cc_status cc_store_reset_invalid_count(cc_store *store, hipStream_t stream);
 
 /*

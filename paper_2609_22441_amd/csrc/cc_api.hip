@@ -511,7 +511,9 @@ cc_status cc_store_reset_invalid_count(cc_store *store, hipStream_t stream) {
     if (!store)
         return CC_ERR_INVALID_ARGUMENT;
     DeviceGuard guard(store->device);
-    hipError_t e = hipMemsetAsync(store->d_invalid, 0, sizeof(unsigned long long), stream);
+    if (guard.error() != hipSuccess)
+        return device_error(guard.error());
+    const hipError_t e = ccj::launch_clear_counter(store->d_invalid, stream);
     return e == hipSuccess ? CC_OK : device_error(e);
 }
 

@@ -68,6 +68,9 @@ hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int6
                        const void *rows_in, int32_t row_bytes, int64_t total, int64_t max_keys,
                        int64_t *keys_out, void *rows_out, void *workspace, hipStream_t stream);
 
+// Enqueue a kernel that sets *counter (device) to zero.
+hipError_t launch_clear_counter(unsigned long long *counter, hipStream_t stream);
+
 // Enqueue the key-order check; *first_bad (device) must hold UINT64_MAX beforehand.
 hipError_t launch_validate_keys(const int64_t *key_offsets, const int64_t *keys,
                                 int32_t n_viewers, int64_t total_keys,

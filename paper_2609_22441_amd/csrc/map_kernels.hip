@@ -376,7 +376,19 @@ __global__ void narrow_kernel(const int64_t *__restrict__ src, int32_t *__restri
         atomicAdd(wide, local);
 }
 
+// Sets one store counter to zero. A kernel, not a memset: a memset node recorded into a HIP
+// graph can leave wrong contents on replays after the first.
+__global__ void clear_counter_kernel(unsigned long long *counter) {
+    if (threadIdx.x == 0)
+        *counter = 0;
+}
+
 }  // namespace
+
+hipError_t launch_clear_counter(unsigned long long *counter, hipStream_t stream) {
+    hipLaunchKernelGGL(clear_counter_kernel, dim3(1), dim3(64), 0, stream, counter);
+    return hipGetLastError();
+}
 
 hipError_t launch_narrow_authors(const int64_t *src, int32_t *dst, int64_t n,
                                  unsigned long long *wide, hipStream_t stream) {

@@ -1,6 +1,6 @@
 """The per-request calls are safe inside a HIP graph (no synchronisation, allocation or memset):
-resolve (Eq. 6) then join (Eq. 1) captured once and replayed with new inputs, every replay
-checked against the same calls made eagerly."""
+a counter reset, resolve (Eq. 6) and join (Eq. 1) captured once and replayed with new inputs,
+every replay checked against the same calls made eagerly."""
 from __future__ import annotations
 
 import numpy as np
@@ -43,6 +43,7 @@ def test_resolve_then_join_replays_in_a_graph():
             return W.doc_ids(items, 4)
 
         def request():
+            P.cc_store_reset_invalid_count(store)
             P.cc_resolve_ids(store, q, pos)
             P.cc_join_batched(store, co, pos, ko, keys, edge, out, hit)
 
@@ -64,6 +65,9 @@ def test_resolve_then_join_replays_in_a_graph():
             graph.replay()
             torch.cuda.synchronize()
             got_out, got_hit, got_pos = out.clone(), hit.clone(), pos.clone()
+            # the join counts every position of -1 (an absent id) since the captured reset
+            assert P.cc_store_invalid_count(store) == int((got_pos < 0).sum()), \
+                f"replay {rep}: invalid count"
             out.fill_(0x5A)
             request()                               # the same calls, eagerly
             torch.cuda.synchronize()

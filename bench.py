@@ -239,7 +239,7 @@ def index_workloads(torch, P, W, dev, seed):
         res[tag] = {"entry": "cc_store_upsert", "records": size, "batches": count,
                     "new_ids": fresh, "ms_median": med * 1e3, "records_per_s": size / med,
                     "algorithmic_bytes": alg, "hbm_gbps": alg / med / 1e9,
-                    "note": "host wall clock per call, including its two stream synchronisations"}
+                    "note": "host wall clock per call, including its one stream synchronisation"}
     P.cc_store_destroy(store)
     torch.cuda.empty_cache()
     return res

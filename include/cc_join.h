@@ -72,15 +72,15 @@ typedef enum cc_status {
  *   doc_row_bytes  bytes per row; a positive multiple of 16.
  *   flags          CC_SRC_HOST (sources are host memory) or CC_SRC_DEVICE (device memory).
  *   stream         the copies are enqueued on this stream, which is synchronised once before
- *                  the call returns (to learn whether every author id fits in 32 bits); the
- *                  sources may be freed afterwards.
+ *                  the call returns (also to learn whether every author id fits in 32 bits);
+ *                  the sources may then be freed and any stream may use the store.
  *
  * The store is created on the current HIP device and stays on it. Layout in HBM: author ids
  * as one int64 column, rows as one row-major array, both 256-byte aligned, plus an 8-byte
  * counter of invalid candidate positions seen by joins. When every author id fits in 32 bits
  * the store also keeps a 32-bit copy of the author column, which the joins read instead
- * (cc_store_layout reports it): the join's random author reads then touch half as many
- * 64-byte sectors. Results never depend on it.
+ * (cc_store_layout reports it): the column then spans half as many cache lines, so more of
+ * it stays in the L2 cache. Results never depend on it.
  * Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_OUT_OF_MEMORY (nothing leaked), CC_ERR_DEVICE,
  * CC_ERR_NOT_SUPPORTED.
  */
@@ -98,8 +98,8 @@ CC_API cc_status cc_store_info(const cc_store *store, int64_t *n_docs, int32_t *
 /*
  * cc_store_layout -- how a store holds its author ids and how many documents it can hold.
  *   author_id_bytes  4 when every stored author id fits in 32 bits (the store then keeps a
- *                    32-bit copy of the column, which the joins read: a 64-byte sector holds 16
- *                    ids instead of 8), else 8.
+ *                    32-bit copy of the column, which the joins read: a 128-byte cache line
+ *                    holds 32 ids instead of 16), else 8.
  *   capacity         rows allocated (n_docs for a store from cc_store_create).
  * Either output may be NULL. Errors: CC_ERR_INVALID_ARGUMENT.
  */
@@ -260,7 +260,8 @@ CC_API cc_status cc_join_batched_tuned(const cc_store *store, int32_t n_viewers,
  *   capacity       documents the store can hold, 0 <= capacity <= 2^31 - 1. Rows, author ids
  *                  and the id map are allocated for this many documents up front.
  *   doc_row_bytes  bytes per document row; a positive multiple of 16.
- *   stream         initialisation is enqueued on this stream.
+ *   stream         the map is cleared on this stream, which is synchronised before the call
+ *                  returns; any stream may then use the store.
  *
  * Layout in HBM: author ids [capacity] int64, rows [capacity][doc_row_bytes], and the id map:
  * an open-addressing table of 16-byte entries {id, position} in 64-byte probe groups, sized

@@ -317,37 +317,49 @@ cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *a
     const hipMemcpyKind kind = flags == CC_SRC_HOST ? hipMemcpyHostToDevice
                                                     : hipMemcpyDeviceToDevice;
     hipError_t e;
+    unsigned long long *d_wide = nullptr;
+    unsigned long long wide = 1;
     if (n_docs > 0) {
         if ((e = hipMemcpyAsync(s->d_author, author_ids, (size_t)id_total, kind, stream)) != hipSuccess)
             return alloc_failure(s, e);
         if ((e = hipMemcpyAsync(s->d_rows, doc_rows, (size_t)row_total, kind, stream)) != hipSuccess)
             return alloc_failure(s, e);
-        // Keep a 32-bit copy of the author column when every id fits: the join's random author
-        // reads then touch half as many 64-byte sectors. The copy is optional: if it cannot be
-        // allocated the store keeps to its 64-bit column.
-        unsigned long long *d_wide = nullptr;
-        unsigned long long wide = 1;
-        if (hipMalloc(&s->d_author32, (size_t)(n_docs * 4)) == hipSuccess &&
-            hipMalloc(&d_wide, sizeof(unsigned long long)) == hipSuccess) {
+        // Keep a 32-bit copy of the author column when every id fits: it spans half as many
+        // cache lines, so more of it stays in L2 under the join's random author reads. The copy
+        // is optional: if it cannot be allocated the store keeps to its 64-bit column.
+        void *a32 = nullptr, *w = nullptr;
+        bool ok = hipMalloc(&a32, (size_t)(n_docs * 4)) == hipSuccess;
+        if (ok)
+            s->d_author32 = static_cast<int32_t *>(a32);
+        ok = ok && hipMalloc(&w, sizeof(unsigned long long)) == hipSuccess;
+        if (ok)
+            d_wide = static_cast<unsigned long long *>(w);
+        if (ok) {
             e = hipMemsetAsync(d_wide, 0, sizeof(unsigned long long), stream);
             if (e == hipSuccess)
                 e = ccj::launch_narrow_authors(s->d_author, s->d_author32, n_docs, d_wide, stream);
             if (e == hipSuccess)
                 e = hipMemcpyAsync(&wide, d_wide, sizeof(wide), hipMemcpyDeviceToHost, stream);
-            if (e == hipSuccess)
-                e = hipStreamSynchronize(stream);
-            (void)hipFree(d_wide);
-            if (e != hipSuccess)
+            if (e != hipSuccess) {
+                (void)hipStreamSynchronize(stream);
+                (void)hipFree(d_wide);
                 return alloc_failure(s, e);
+            }
         } else {
             (void)hipGetLastError();              // an allocation failure is not sticky
         }
-        if (wide == 0) {
-            s->compact = true;
-        } else {
-            (void)hipFree(s->d_author32);
-            s->d_author32 = nullptr;
-        }
+    }
+    // Every path synchronises once: the copies and the counter clears have completed when the
+    // call returns, so the sources may be freed and any stream may use the store.
+    e = hipStreamSynchronize(stream);
+    (void)hipFree(d_wide);
+    if (e != hipSuccess)
+        return alloc_failure(s, e);
+    if (wide == 0) {
+        s->compact = true;
+    } else if (s->d_author32) {
+        (void)hipFree(s->d_author32);
+        s->d_author32 = nullptr;
     }
     *out_store = s;
     return CC_OK;
@@ -364,6 +376,10 @@ cc_status cc_store_create_indexed(cc_store **out_store, int64_t capacity, int32_
     cc_status st = new_store(capacity, doc_row_bytes, true, stream, &s);
     if (st != CC_OK)
         return st;
+    // The map is cleared on `stream`; synchronise so that any stream may use the store.
+    const hipError_t e = hipStreamSynchronize(stream);
+    if (e != hipSuccess)
+        return alloc_failure(s, e);
     *out_store = s;
     return CC_OK;
 }
@@ -399,6 +415,8 @@ cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc
         overlaps(workspace, workspace_bytes, doc_rows, n_records * rb))
         return CC_ERR_INVALID_ARGUMENT;
     DeviceGuard guard(store->device);
+    if (guard.error() != hipSuccess)
+        return device_error(guard.error());
     hipError_t e = ccj::launch_upsert_claim(store->d_map, store->map_groups, doc_ids, n_records,
                                             workspace, stream);
     if (e == hipSuccess)
@@ -436,6 +454,8 @@ cc_status cc_store_read(const cc_store *store, int64_t first, int64_t count, int
     if (count == 0)
         return CC_OK;
     DeviceGuard guard(store->device);
+    if (guard.error() != hipSuccess)
+        return device_error(guard.error());
     const int64_t rb = store->doc_row_bytes;
     hipError_t e = hipSuccess;
     if (author_out)
@@ -455,11 +475,15 @@ cc_status cc_resolve_ids(const cc_store *store, const int64_t *doc_ids, int64_t 
         return CC_ERR_NOT_SUPPORTED;
     if (n == 0)
         return CC_OK;
-    if (!doc_ids || !positions || !aligned(doc_ids, 8) || !aligned(positions, 8))
+    int64_t bytes = 0;
+    if (!doc_ids || !positions || !aligned(doc_ids, 8) || !aligned(positions, 8) ||
+        !mul_ok(n, 8, &bytes))
         return CC_ERR_INVALID_ARGUMENT;
-    if (doc_ids != positions && overlaps(doc_ids, n * 8, positions, n * 8))
+    if (doc_ids != positions && overlaps(doc_ids, bytes, positions, bytes))
         return CC_ERR_INVALID_ARGUMENT;
     DeviceGuard guard(store->device);
+    if (guard.error() != hipSuccess)
+        return device_error(guard.error());
     hipError_t e = ccj::launch_resolve(store->d_map, store->map_groups, doc_ids, n, positions,
                                        stream);
     return e == hipSuccess ? CC_OK : device_error(e);
@@ -497,6 +521,8 @@ cc_status cc_store_invalid_count(const cc_store *store, int64_t *count, hipStrea
     if (!store || !count)
         return CC_ERR_INVALID_ARGUMENT;
     DeviceGuard guard(store->device);
+    if (guard.error() != hipSuccess)
+        return device_error(guard.error());
     unsigned long long v = 0;
     hipError_t e = hipMemcpyAsync(&v, store->d_invalid, sizeof(v), hipMemcpyDeviceToHost, stream);
     if (e == hipSuccess)

@@ -83,6 +83,52 @@ def test_no_candidates_is_a_no_op():
         P.cc_store_destroy(store)
 
 
+def test_store_from_host_memory():
+    """A store copied from host memory (CC_SRC_HOST) joins exactly like one copied from device
+    memory, and both match the oracle."""
+    note("store from host memory")
+    for seed in range(6):
+        tc = W.tiny_case(4000 + seed, n_lookups=1)
+        b = tc.batch.to(DEV)
+        wd, we = row_bytes(tc.doc_rows), row_bytes(tc.batch.edge_rows)
+        want = oracle_join(tc.author_id, tc.doc_rows, tc.batch, 1, default_row=tc.default_row)
+        d = None if tc.default_row is None else tc.default_row.to(DEV)
+        for src in ("host", "device"):
+            a, r = (tc.author_id, tc.doc_rows) if src == "host" else \
+                (tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+            store = P.cc_store_create(a, r)
+            try:
+                assert P.cc_store_info(store) == (tc.author_id.numel(), wd)
+                got = gpu_join(store, None, b, wd, we, 1, default_row=d)
+                assert_same(got, want, f"seed {seed}, store from {src} memory")
+            finally:
+                P.cc_store_destroy(store)
+
+
+def test_empty_store_makes_every_position_invalid():
+    """A store of 0 documents: every candidate position is out of range, so each row is a zero
+    doc segment plus the default edge row, every hit bit is 0 and every candidate is counted."""
+    note("empty store")
+    store = P.cc_store_create(torch.zeros(0, dtype=torch.int64),
+                              torch.zeros(0, 32, dtype=torch.uint8))
+    try:
+        assert P.cc_store_info(store) == (0, 32)
+        cand = torch.tensor([0, 1, -1, 7, 0], dtype=torch.int64)
+        keys = torch.tensor([0, 1, 7], dtype=torch.int64)
+        edge = torch.arange(3 * 16, dtype=torch.int64).to(torch.uint8).reshape(3, 16)
+        default = torch.full((16,), 0xAB, dtype=torch.uint8)
+        batch = W.pack([W.Request(keys, edge, cand, None)])
+        got = gpu_join(store, None, batch.to(DEV), 32, 16, 1, default_row=default.to(DEV))
+        want = oracle_join(torch.zeros(0, dtype=torch.int64), torch.zeros(0, 32, dtype=torch.uint8),
+                           batch, 1, default_row=default)
+        assert_same(got, want, "empty store")
+        assert (got[0][:, :32] == 0).all() and (got[0][:, 32:] == 0xAB).all()
+        assert not got[1].any()
+        assert P.cc_store_invalid_count(store) == cand.numel()
+    finally:
+        P.cc_store_destroy(store)
+
+
 def _scaled_store(seed, cfg=2, **kw):
     kw = {"store_n_docs": 300_000, "store_n_authors": 200_000, **kw}
     s, r = W.config(cfg, **kw)

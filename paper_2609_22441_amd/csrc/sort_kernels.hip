@@ -17,9 +17,9 @@
 //      tile's records are one run.
 //   2. merge rounds: within each viewer, runs of kTile << r records are merged pairwise, one
 //      output tile per workgroup. A viewer with n tiles takes part in ceil(log2 n) rounds. The
-//      tile's split on the merge path is found by a 64-ary search run by one wavefront (a few
-//      rounds of 64 probes instead of a ~20-step dependent binary search); the tile is merged
-//      in LDS, kEpt outputs per thread.
+//      tile's two split points on the merge path are found by 64-ary searches, one wavefront
+//      each (a few rounds of 64 probes instead of a ~20-step dependent binary search); the tile
+//      is merged in LDS, kEpt outputs per thread.
 //   3. A viewer's last pass (its block sort when it has one tile, else its last merge round)
 //      writes the sorted keys and copies each record's feature row from the input, straight
 //      from LDS; earlier passes write elements to two ping-pong arrays in a caller-provided
@@ -491,13 +491,10 @@ __device__ __forceinline__ void merge_body(const F &fm, char *lds, int64_t *s_sp
         const int64_t d1 = min<int64_t>(d0 + kTile, la + lb);
         const T *A = src + kb + a0;
         const T *Bv = src + kb + b0;
-        if (tid < 64) {
-            const int64_t i0 = split64<F>(A, la, Bv, lb, d0);
-            const int64_t i1 = split64<F>(A, la, Bv, lb, d1);
-            if (tid == 0) {
-                s_split[0] = i0;
-                s_split[1] = i1;
-            }
+        if (tid < 128) {                                 // wavefront 0: d0, wavefront 1: d1
+            const int64_t i = split64<F>(A, la, Bv, lb, tid < 64 ? d0 : d1);
+            if ((tid & 63) == 0)
+                s_split[tid >> 6] = i;
         }
         lds_sync();
         const int64_t i0 = s_split[0], i1 = s_split[1];

@@ -25,7 +25,9 @@
 //      from LDS; earlier passes write elements to two ping-pong arrays in a caller-provided
 //      workspace.
 // LDS rows are padded by one element every kEpt elements so that the per-thread blocked
-// accesses (stride kEpt elements) spread over the banks.
+// accesses (stride kEpt elements) spread over the banks. Other layouts (no padding, one pad per 16
+// or 32 elements, XOR swizzles) timed the same within run-to-run noise: most of the LDS bank
+// conflicts come from the data-dependent merge-path probes, which no static layout removes.
 #include <stdint.h>
 
 #include <hip/hip_runtime.h>

@@ -107,10 +107,25 @@ def _check(status: int, where: str):
         raise CCError(status, where)
 
 
+_RAW_STREAM = None
+
+
+def _current_stream() -> int:
+    """Handle of torch's current stream on the current device. torch's raw-stream query costs
+    a tenth of building a Stream object (about 0.3 us against 3 us per call); the public call
+    is the fallback where the query is missing."""
+    global _RAW_STREAM
+    import torch
+    if _RAW_STREAM is None:
+        raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+        _RAW_STREAM = (lambda: raw(torch.cuda.current_device())) if raw is not None else \
+            (lambda: torch.cuda.current_stream().cuda_stream)
+    return _RAW_STREAM()
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
-        import torch
-        return torch.cuda.current_stream().cuda_stream
+        return _current_stream()
     if isinstance(stream, int):
         return stream
     return stream.cuda_stream

@@ -1,0 +1,49 @@
+"""The binding enqueues on torch's current stream: the stream handle it passes is the one
+torch reports, on the default stream and inside a stream context, and work launched there is
+ordered with torch's own work on that stream."""
+from __future__ import annotations
+
+import pytest
+import torch
+
+import paper_2609_22441_amd as P
+from paper_2609_22441_amd import binding as B
+import workload as W
+from gpu_common import assert_same, note, oracle_join, row_bytes
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+def test_launch_stream_is_torchs_current_stream():
+    note("binding: current stream")
+    torch.cuda.set_device(DEV)
+    assert B._stream(None) == torch.cuda.current_stream().cuda_stream
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        assert B._stream(None) == side.cuda_stream
+    assert B._stream(None) == torch.cuda.current_stream().cuda_stream
+
+
+def test_join_on_a_side_stream_is_ordered_with_torch_work():
+    """Inputs written by torch on a side stream, the join launched on that stream without a
+    synchronisation in between, and the output read back after the stream ends."""
+    note("binding: side-stream ordering")
+    tc = W.tiny_case(77, n_lookups=1, max_n=600, max_viewers=3)
+    wd, we = row_bytes(tc.doc_rows), row_bytes(tc.batch.edge_rows)
+    store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+    try:
+        b = tc.batch
+        side = torch.cuda.Stream()
+        with torch.cuda.stream(side):
+            cand = torch.empty_like(b.cand_idx, device=DEV)
+            cand.copy_(b.cand_idx, non_blocking=False)
+            out = torch.full((b.cand_idx.numel(), wd + we), 0xEE, dtype=torch.uint8, device=DEV)
+            hit = torch.full((b.cand_idx.numel(), 1), -7, dtype=torch.int8, device=DEV)
+            P.cc_join_batched(store, b.cand_offsets.to(DEV), cand, b.key_offsets.to(DEV),
+                              b.keys.to(DEV), b.edge_rows.to(DEV), out, hit)
+        side.synchronize()
+        want = oracle_join(tc.author_id, tc.doc_rows, b, 1)
+        assert_same((out.cpu().numpy(), hit.cpu().numpy()), want, "side stream")
+    finally:
+        P.cc_store_destroy(store)

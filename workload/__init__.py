@@ -170,8 +170,11 @@ class Batch:
 
 
 def _zipf_ids(n: int, m: int, s: float, perm: torch.Tensor, g, device, chunk=1 << 24):
-    ranks = torch.arange(1, m + 1, dtype=torch.float64, device=device)
-    cdf = torch.cumsum(ranks.pow_(-s), 0)
+    # The CDF is accumulated on the host: a device scan adds its tiles in a timing-dependent
+    # order, so the CDF's last bits, and with them a few ids, could change from run to run.
+    ranks = torch.arange(1, m + 1, dtype=torch.float64)
+    cdf = torch.cumsum(ranks.pow_(-s), 0).to(device)
+    del ranks
     total = cdf[-1].item()
     out = torch.empty(n, dtype=torch.int64, device=device)
     for lo in range(0, n, chunk):

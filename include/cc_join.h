@@ -69,7 +69,7 @@ typedef enum cc_status {
  *   n_docs         number of documents, >= 0.
  *   author_ids     [n_docs] int64 author id of each document (any int64 value).
  *   doc_rows       [n_docs][doc_row_bytes] row-major document-feature rows.
- *   doc_row_bytes  bytes per row; a positive multiple of 16.
+ *   doc_row_bytes  bytes per row; a positive multiple of 16, at most 2^20 (1 MiB).
  *   flags          CC_SRC_HOST (sources are host memory) or CC_SRC_DEVICE (device memory).
  *   stream         the copies are enqueued on this stream, which is synchronised once before
  *                  the call returns (also to learn whether every author id fits in 32 bits);
@@ -125,7 +125,7 @@ CC_API cc_status cc_store_reset_invalid_count(cc_store *store, hipStream_t strea
  *   edge_keys      [n_keys] int64 viewer's affinity author ids, ascending in signed order.
  *   n_keys         K >= 0; K = 0 makes every candidate a miss.
  *   edge_feats     [n_keys][edge_row_bytes] feature row of each key (row i belongs to key i).
- *   edge_row_bytes bytes per edge row; a positive multiple of 16.
+ *   edge_row_bytes bytes per edge row; a positive multiple of 16, at most 2^20 (1 MiB).
  *   default_row    [edge_row_bytes] row written on a miss, or NULL for zero bytes.
  *   out            [n_cand][out_row_stride] output; row j gets
  *                  [doc row (doc_row_bytes) | edge row or default (edge_row_bytes)];
@@ -259,7 +259,7 @@ CC_API cc_status cc_join_batched_tuned(const cc_store *store, int32_t n_viewers,
  *   out_store      receives the new store handle (set to NULL on error).
  *   capacity       documents the store can hold, 0 <= capacity <= 2^31 - 1. Rows, author ids
  *                  and the id map are allocated for this many documents up front.
- *   doc_row_bytes  bytes per document row; a positive multiple of 16.
+ *   doc_row_bytes  bytes per document row; a positive multiple of 16, at most 2^20 (1 MiB).
  *   stream         the map is cleared on this stream, which is synchronised before the call
  *                  returns; any stream may then use the store.
  *
@@ -340,7 +340,7 @@ CC_API cc_status cc_resolve_ids(const cc_store *store, const int64_t *doc_ids, i
  *                  are [key_offsets[v], key_offsets[v+1]); sorted within that range).
  *   keys_in        [total_keys] int64 device, any order within a viewer.
  *   rows_in        [total_keys][row_bytes] device.
- *   row_bytes      positive multiple of 16.
+ *   row_bytes      positive multiple of 16, at most 2^20 (1 MiB).
  *   total_keys     host copy of key_offsets[B]; < 2^32.
  *   max_keys       host upper bound on any one viewer's record count (fewer merge passes), or
  *                  0 if unknown. The output of a viewer with more records than max_keys is

@@ -77,7 +77,7 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
     // ---- host-side validation; nothing touches the device before it passes ----
     if (!store || n_viewers < 0 || total_cand < 0 || total_keys < 0)
         return CC_ERR_INVALID_ARGUMENT;
-    if (edge_row_bytes <= 0 || (edge_row_bytes & 15))
+    if (edge_row_bytes <= 0 || (edge_row_bytes & 15) || edge_row_bytes > ccj::kMaxRowBytes)
         return CC_ERR_INVALID_ARGUMENT;
     if (n_lookups != 1 && n_lookups != 2)
         return CC_ERR_INVALID_ARGUMENT;
@@ -300,7 +300,8 @@ cc_status cc_store_create(cc_store **out_store, int64_t n_docs, const int64_t *a
     if (!out_store)
         return CC_ERR_INVALID_ARGUMENT;
     *out_store = nullptr;
-    if (n_docs < 0 || doc_row_bytes <= 0 || (doc_row_bytes & 15))
+    if (n_docs < 0 || doc_row_bytes <= 0 || (doc_row_bytes & 15) ||
+        doc_row_bytes > ccj::kMaxRowBytes)
         return CC_ERR_INVALID_ARGUMENT;
     if (flags != CC_SRC_HOST && flags != CC_SRC_DEVICE)
         return CC_ERR_INVALID_ARGUMENT;
@@ -370,7 +371,8 @@ cc_status cc_store_create_indexed(cc_store **out_store, int64_t capacity, int32_
     if (!out_store)
         return CC_ERR_INVALID_ARGUMENT;
     *out_store = nullptr;
-    if (capacity < 0 || capacity > INT32_MAX || doc_row_bytes <= 0 || (doc_row_bytes & 15))
+    if (capacity < 0 || capacity > INT32_MAX || doc_row_bytes <= 0 || (doc_row_bytes & 15) ||
+        doc_row_bytes > ccj::kMaxRowBytes)
         return CC_ERR_INVALID_ARGUMENT;
     cc_store *s = nullptr;
     cc_status st = new_store(capacity, doc_row_bytes, true, stream, &s);
@@ -618,7 +620,7 @@ cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets, const 
                            int64_t workspace_bytes, hipStream_t stream) {
     if (n_viewers < 0 || total_keys < 0 || total_keys >= ((int64_t)1 << 32) || max_keys < 0)
         return CC_ERR_INVALID_ARGUMENT;
-    if (row_bytes <= 0 || (row_bytes & 15))
+    if (row_bytes <= 0 || (row_bytes & 15) || row_bytes > ccj::kMaxRowBytes)
         return CC_ERR_INVALID_ARGUMENT;
     if (n_viewers > 0 && !key_offsets)
         return CC_ERR_INVALID_ARGUMENT;

@@ -15,6 +15,9 @@ constexpr int kDefaultLdsKeys = 8192;   // 64 KiB: within the register-limited o
 // of workgroups (one per CU): the larger table keeps each lookup's window of keys within one
 // 64-byte sector, and one wave leaves no half-empty last wave.
 constexpr int64_t kLongListKeys = 4 * (int64_t)kDefaultLdsKeys;
+// Largest row (document, edge or affinity record) in bytes. Copy loops count a tile's row
+// chunks in 32 bits: 256 rows (or 4096 sort records) of this many bytes stay far below 2^31.
+constexpr int32_t kMaxRowBytes = 1 << 20;
 constexpr int kZeroRowBytes = 1024;    // >= the widest row of a compile-time specialisation
 
 struct JoinArgs {

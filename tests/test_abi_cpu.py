@@ -42,6 +42,7 @@ def test_status_strings():
     (-1, None, None, 16, 1),          # negative size
     (4, 8, 8, 24, 1),                 # row width not a multiple of 16
     (4, 8, 8, 0, 1),                  # zero row width
+    (4, 8, 8, (1 << 20) + 16, 1),     # row wider than 1 MiB
     (4, None, 8, 16, 1),              # missing author ids
     (4, 8, None, 16, 1),              # missing rows
     (0, None, None, 16, 3),           # unknown source flag
@@ -106,6 +107,8 @@ def test_sort_rejects_bad_arguments():
                                     a["mk"], a["kout"], a["rout"], a["w"], a["wb"], None)
 
     assert call(rb=24) == 1                      # row width not a multiple of 16
+    assert call(rb=(1 << 20) + 16) == 1          # row wider than 1 MiB
+    assert call(rb=1 << 20, tk=0, kin=None, rin=None, kout=None, rout=None, w=None, wb=0) == 0
     assert call(tk=-1) == 1
     assert call(tk=1 << 32) == 1                 # record count must fit 32 bits
     assert call(nv=-1) == 1
@@ -130,6 +133,7 @@ def test_indexed_store_rejects_bad_arguments():
     assert lib.cc_store_create_indexed(ctypes.byref(h), 1 << 31, 16, None) == 1   # > INT32_MAX
     assert lib.cc_store_create_indexed(ctypes.byref(h), 10, 24, None) == 1        # row width
     assert lib.cc_store_create_indexed(ctypes.byref(h), 10, 0, None) == 1
+    assert lib.cc_store_create_indexed(ctypes.byref(h), 10, (1 << 20) + 16, None) == 1
 
 
 def test_upsert_and_resolve_reject_bad_arguments():

@@ -278,6 +278,7 @@ def test_argument_errors_with_a_real_store():
         assert join(stride=40) == 1                         # stride below the row width
         assert join(stride=56) == 1                         # stride not a multiple of 16
         assert join(ew=24) == 1                             # edge width not a multiple of 16
+        assert join(ew=(1 << 20) + 16, stride=(1 << 20) + 64) == 1   # edge row above 1 MiB
         assert join(n=-1) == 1
         assert join(k=-1) == 1
         assert join(cand=None) == 1

@@ -1,8 +1,11 @@
-"""Property-based pins of the oracle (CPU only): for inputs that hypothesis draws and shrinks,
-all three of the oracle's ways to find the leftmost equal key (lower bound, linear scan, hash
-map) give the result of Eq. 1 written out as a plain Python scan, and the join is equivariant
-under a permutation of the candidates. Ids are drawn from a small pool that includes the int64
-extremes, so keys collide and repeat often."""
+"""Property-based pins of the oracle (CPU only), on inputs that hypothesis draws and shrinks:
+* join (Eq. 1): all three ways to find the leftmost equal key (lower bound, linear scan, hash
+  map) give Eq. 1 written out as a plain Python scan, and the join is equivariant under a
+  permutation of each viewer's candidates;
+* ingestion (§6.2) and resolution (Eq. 6): the sequential replay equals plain Python over a
+  dict, batch after batch, including refused batches and the reserved id;
+* the sort (Alg. 1 Step 1): equals Python's stable sort within each viewer.
+Ids come from a small pool that includes the int64 extremes, so keys collide and repeat often."""
 from __future__ import annotations
 
 import numpy as np
@@ -90,3 +93,78 @@ def test_candidate_permutation_permutes_rows(tc, rnd):
     assert pinv == inv
     assert np.array_equal(pout, out[perm.numpy()])
     assert np.array_equal(phit, hit[perm.numpy()])
+
+
+# ---- ingestion (§6.2) and id resolution (Eq. 6) ----
+
+class DictModel:
+    """Ingestion written as plain Python over a dict: records applied one at a time; a batch
+    whose new ids do not fit in the capacity leaves everything unchanged."""
+
+    def __init__(self, capacity, row_bytes):
+        self.capacity, self.pos, self.ids, self.author, self.rows = capacity, {}, [], [], []
+        self.row_bytes = row_bytes
+
+    def upsert(self, batch):
+        pos, ids = dict(self.pos), list(self.ids)
+        author, rows = list(self.author), list(self.rows)
+        rejected = 0
+        for i, a, r in batch:
+            if i == -(1 << 63):
+                rejected += 1
+                continue
+            if i not in pos:
+                if len(ids) == self.capacity:
+                    return None
+                pos[i] = len(ids)
+                ids.append(i)
+                author.append(0)
+                rows.append(bytes(self.row_bytes))
+            author[pos[i]] = a
+            rows[pos[i]] = r
+        n_new = len(ids) - len(self.ids)
+        self.pos, self.ids, self.author, self.rows = pos, ids, author, rows
+        return n_new, rejected
+
+
+@SETTINGS
+@given(st.integers(0, 10), st.lists(st.lists(st.tuples(ids, ids, st.binary(min_size=16,
+                                                                           max_size=16)),
+                                             max_size=8), max_size=5),
+       st.lists(ids, max_size=12))
+def test_upsert_replay_matches_a_dict(capacity, batches, queries):
+    state = oracle.IndexState(capacity, 16)
+    model = DictModel(capacity, 16)
+    for batch in batches:
+        ids_ = np.array([b[0] for b in batch], dtype=np.int64)
+        authors = np.array([b[1] for b in batch], dtype=np.int64)
+        rows = np.frombuffer(b"".join(b[2] for b in batch), dtype=np.uint8).reshape(len(batch), 16)
+        got = state.upsert(ids_, authors, rows)
+        assert got == model.upsert(batch)
+        n = state.n_docs
+        assert n == len(model.ids)
+        assert state.ids[:n].tolist() == model.ids
+        assert state.author[:n].tolist() == model.author
+        assert [bytes(r) for r in state.rows[:n]] == model.rows
+    got = state.resolve(np.array(queries, dtype=np.int64))
+    want = [model.pos.get(q, -1) if q != -(1 << 63) else -1 for q in queries]
+    assert np.asarray(got).tolist() == want
+
+
+# ---- Alg. 1 Step 1: the per-viewer stable sort ----
+
+@SETTINGS
+@given(st.lists(st.lists(ids, max_size=12), min_size=1, max_size=4))
+def test_sort_is_pythons_stable_sort_per_viewer(viewers):
+    keys = [k for v in viewers for k in v]
+    offs = np.cumsum([0] + [len(v) for v in viewers]).astype(np.int64)
+    # row j carries its input index, so the test sees which record went where
+    rows = np.zeros((len(keys), 16), dtype=np.uint8)
+    rows[:, :8] = np.arange(len(keys), dtype=np.int64).view(np.uint8).reshape(-1, 8)
+    k_out, r_out = oracle.sort_affinity(offs, np.array(keys, dtype=np.int64), rows)
+    want = []
+    for v in range(len(viewers)):
+        want += sorted(range(offs[v], offs[v + 1]), key=lambda j: keys[j])   # stable
+    src = r_out[:, :8].copy().view(np.int64).ravel().tolist()
+    assert src == want
+    assert k_out.tolist() == [keys[j] for j in want]

@@ -83,6 +83,8 @@ typedef struct {
     uint64_t mask;
 } table_t;
 
+/* The 64-bit finalizer of MurmurHash3 (fmix64, Austin Appleby): a bijective mixer, so keys that
+ * differ in any bit spread over the slots. */
 static uint64_t mix64(uint64_t z)
 {
     z ^= z >> 33;

@@ -90,7 +90,7 @@ def all_configs(torch, P, W, dev, seed):
     res = {}
     st10 = None
     for i in (1, 2, 3, 4, 5):
-        s, r = W.CONFIGS[i]
+        s, r = W.SHAPES[i]
         if i == 1:
             st = W.make_store(s, seed, device=dev)
         elif i in (2, 3, 4):
@@ -181,7 +181,7 @@ def index_workloads(torch, P, W, dev, seed):
     """The document-id map (§6.3.1, Eq. 6) and ingestion (§6.2) on the one-shard index: build it
     by ingestion, resolve b x tens-of-thousands ids, and apply ingestion batches."""
     import time
-    spec = W.INDEX_CONFIG
+    spec = W.INDEX_SHAPE
     n = spec.n_index
     rb = spec.row_cols * 2
     n_batches = 20
@@ -344,7 +344,7 @@ def main():
         __graft_entry__.build()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    s, r = W.CONFIGS[2]
+    s, r = W.SHAPES[2]
     st = W.make_store(s, args.seed, device=dev)
     store = P.cc_store_create(st.author_id, st.doc_rows)
     batches = []

@@ -188,8 +188,9 @@ def pin_alg1(lib, seeds=range(40)):
 
 # --------------------------------------------------------------------------------------------
 def _scaled_case(seed, cfg=2, lookups=False, viewers=3):
-    s, r = W.config(cfg, store_n_docs=60_000, store_n_authors=50_000, req_k=700,
-                    req_n_cand=4_000, req_n_viewers=viewers, req_actor=lookups, req_k_range=None)
+    s, r = W.shape(cfg, store_n_docs=60_000, store_n_authors=50_000, req_k=700,
+                   req_n_cand=4_000, req_n_viewers=viewers, req_actor=lookups,
+                   req_k_range=None)
     st = W.make_store(s, seed)
     reqs = W.make_requests(st, r, seed)
     return st, reqs

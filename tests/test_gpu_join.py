@@ -131,7 +131,7 @@ def test_empty_store_makes_every_position_invalid():
 
 def _scaled_store(seed, cfg=2, **kw):
     kw = {"store_n_docs": 300_000, "store_n_authors": 200_000, **kw}
-    s, r = W.config(cfg, **kw)
+    s, r = W.shape(cfg, **kw)
     st = W.make_store(s, seed, device=DEV)
     return st, r
 
@@ -194,7 +194,7 @@ def test_special_bit_patterns_are_copied_exactly():
 
 def test_fp32_rows_of_the_tiny_shape():
     note("fp32 rows (16 + 8 columns)")
-    s, r = W.config(1, store_n_docs=100_000)
+    s, r = W.shape(1, store_n_docs=100_000)
     st = W.make_store(s, 12, device=DEV)
     b = W.pack([W.make_request(st, r, 12, 0)])
     store = P.cc_store_create(st.author_id, st.doc_rows)

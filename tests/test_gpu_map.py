@@ -181,7 +181,7 @@ def test_full_size_index_sampled():
     stored id resolves to its item index (the replay gives item i position i when items arrive
     in order without repeats); then one ingestion batch of the benchmark's mix is checked on
     its counts and on sampled rows and positions."""
-    spec = W.INDEX_CONFIG
+    spec = W.INDEX_SHAPE
     n = spec.n_index
     note(f"map: full-size index, {n} documents")
     store = P.cc_store_create_indexed(n + 4 * spec.upsert_batch, 128)

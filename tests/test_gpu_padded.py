@@ -107,9 +107,9 @@ def test_padded_without_candidates_fills_pads():
 
 
 @pytest.mark.timeout(300)
-def test_config3_padded():
+def test_workload3_padded():
     note("workload 3 in the padded layout")
-    s, r = W.CONFIGS[3]
+    s, r = W.SHAPES[3]
     st = W.make_store(s, 2, device=DEV)
     reqs = W.make_requests(st, r, 3)
     b = W.pack(reqs)

@@ -84,7 +84,7 @@ def test_many_ragged_viewers():
 @pytest.mark.parametrize("cfg", [3, 5])
 def test_workload_record_sets(cfg):
     note(f"sort: workload {cfg} record sets")
-    s, r = W.CONFIGS[cfg]
+    s, r = W.SHAPES[cfg]
     s = W.StoreSpec(1_000_000, s.n_authors, s.zipf_s, s.doc_cols, s.doc_dtype)
     st = W.make_store(s, 2, device=DEV)
     b = W.pack(W.make_requests(st, r, cfg))
@@ -96,8 +96,8 @@ def test_workload_record_sets(cfg):
 
 def test_sort_then_join_equals_oracle():
     note("sort then join")
-    s, r = W.config(2, store_n_docs=300_000, store_n_authors=200_000, req_k=3000,
-                    req_n_cand=20_000, req_n_viewers=3)
+    s, r = W.shape(2, store_n_docs=300_000, store_n_authors=200_000, req_k=3000,
+                   req_n_cand=20_000, req_n_viewers=3)
     st = W.make_store(s, 4, device=DEV)
     b = W.pack(W.make_requests(st, r, 4))
     k, rw = _shuffle_within(b.key_offsets, b.keys, b.edge_rows, 4)

@@ -23,7 +23,7 @@ STORE_SEED = 2
 @pytest.fixture(scope="module")
 def store10m():
     note("generating the 10M-document store")
-    s, _ = W.CONFIGS[2]
+    s, _ = W.SHAPES[2]
     st = W.make_store(s, STORE_SEED, device=DEV)
     h = P.cc_store_create(st.author_id, st.doc_rows)
     torch.cuda.synchronize()
@@ -44,8 +44,8 @@ def _check(st, handle, cpu, reqs, n_lookups, single=False, what=""):
 
 
 @pytest.mark.timeout(300)
-def test_config1_single_viewer_tiny():
-    s, r = W.CONFIGS[1]
+def test_workload1_single_viewer_tiny():
+    s, r = W.SHAPES[1]
     st = W.make_store(s, 1, device=DEV)
     h = P.cc_store_create(st.author_id, st.doc_rows)
     try:
@@ -58,27 +58,27 @@ def test_config1_single_viewer_tiny():
 
 
 @pytest.mark.timeout(300)
-def test_config2_single_viewer_production(store10m):
+def test_workload2_single_viewer_production(store10m):
     st, h, cpu = store10m
-    _, r = W.CONFIGS[2]
+    _, r = W.SHAPES[2]
     reqs = W.make_requests(st, r, 2)
     _, hit = _check(st, h, cpu, reqs, 1, single=True, what="workload 2")
     assert 0.6 < hit.mean() < 0.8                  # ~70.7% expected
 
 
 @pytest.mark.timeout(300)
-def test_config2_batched_as_benchmarked(store10m):
+def test_workload2_batched_as_benchmarked(store10m):
     """64 production-shaped requests in one batched launch (the benchmark's step)."""
     st, h, cpu = store10m
-    _, r = W.CONFIGS[2]
+    _, r = W.SHAPES[2]
     reqs = W.make_requests(st, r, 2, n_viewers=64)
     _check(st, h, cpu, reqs, 1, what="workload 2 x64 batched")
 
 
 @pytest.mark.timeout(300)
-def test_config3_batched_ragged(store10m):
+def test_workload3_batched_ragged(store10m):
     st, h, cpu = store10m
-    _, r = W.CONFIGS[3]
+    _, r = W.SHAPES[3]
     reqs = W.make_requests(st, r, 3)
     ks = [q.keys.numel() for q in reqs]
     assert min(ks) >= 100 and max(ks) <= 30_000
@@ -86,17 +86,17 @@ def test_config3_batched_ragged(store10m):
 
 
 @pytest.mark.timeout(300)
-def test_config4_double_join(store10m):
+def test_workload4_double_join(store10m):
     st, h, cpu = store10m
-    _, r = W.CONFIGS[4]
+    _, r = W.SHAPES[4]
     reqs = W.make_requests(st, r, 4)
     _, hit = _check(st, h, cpu, reqs, 2, what="workload 4")
     assert 0.6 < hit[:, 0].mean() < 0.8 and 0.45 < hit[:, 1].mean() < 0.55
 
 
 @pytest.mark.timeout(900)
-def test_config5_large_scale():
-    s, r = W.CONFIGS[5]
+def test_workload5_large_scale():
+    s, r = W.SHAPES[5]
     note("generating the 200M-document store on the device")
     st = W.make_store(s, 5, device=DEV)
     reqs = W.make_requests(st, r, 5)

@@ -123,7 +123,7 @@ def test_special_bit_patterns_copied(lib):
 
 def test_generator_hit_rate_closed_form():
     """Generator sanity (not the join): uniform keys over the author space hit with rate K/M."""
-    s, r = W.config(1, store_n_docs=200_000)
+    s, r = W.shape(1, store_n_docs=200_000)
     st = W.make_store(s, 11)
     q = W.make_request(st, r, 11, 0)
     rate = torch.isin(st.author_id[q.cand_idx], q.keys).double().mean().item()

@@ -45,9 +45,9 @@ from typing import List, Optional, Sequence
 import torch
 
 __all__ = [
-    "StoreSpec", "RequestSpec", "CONFIGS", "Store", "Request", "Batch",
-    "gen", "make_store", "make_requests", "pack", "salt_special_values", "config",
-    "IndexSpec", "INDEX_CONFIG", "doc_ids", "index_records", "resolve_queries", "upsert_batch",
+    "StoreSpec", "RequestSpec", "SHAPES", "Store", "Request", "Batch",
+    "gen", "make_store", "make_requests", "pack", "salt_special_values", "shape",
+    "IndexSpec", "INDEX_SHAPE", "doc_ids", "index_records", "resolve_queries", "upsert_batch",
 ]
 
 
@@ -78,7 +78,7 @@ class RequestSpec:
 F32, BF16 = torch.float32, torch.bfloat16
 
 # The five workload shapes: (store, requests).
-CONFIGS = {
+SHAPES = {
     # Single viewer, tiny: 1M docs, uniform authors over [0,1e5), 16 fp32 doc cols;
     # K=1000 uniform keys, 8 fp32 edge cols; N=10k uniform candidates without replacement.
     1: (StoreSpec(1_000_000, 100_000, 0.0, 16, F32),
@@ -101,13 +101,13 @@ CONFIGS = {
 }
 
 
-def config(i: int, **scale) -> tuple:
+def shape(i: int, **scale) -> tuple:
     """Return (StoreSpec, RequestSpec) of workload i, with optional field overrides.
 
     Overrides are given as ``store_<field>=`` / ``req_<field>=`` keyword arguments, e.g.
-    ``config(2, store_n_docs=100_000, req_n_cand=2_000)`` for a scaled-down copy.
+    ``shape(2, store_n_docs=100_000, req_n_cand=2_000)`` for a scaled-down copy.
     """
-    s, r = CONFIGS[i]
+    s, r = SHAPES[i]
     s = replace(s, **{k[6:]: v for k, v in scale.items() if k.startswith("store_")})
     r = replace(r, **{k[4:]: v for k, v in scale.items() if k.startswith("req_")})
     return s, r
@@ -445,7 +445,7 @@ class IndexSpec:
 # batches of b = 8 requests x 50,000 ids (§6.3.1 quotes batch 8 with tens of thousands of ids
 # per request against a few-hundred-million-entry index); ingestion batches of 300,000 records
 # (§6.2: bootstrap batches of hundreds of thousands of documents).
-INDEX_CONFIG = IndexSpec(200_000_000, 50_000_000, 64, BF16, 8, 50_000, 0.02, 300_000, 0.2, 0.05)
+INDEX_SHAPE = IndexSpec(200_000_000, 50_000_000, 64, BF16, 8, 50_000, 0.02, 300_000, 0.2, 0.05)
 
 _ID_MASK = (1 << 62) - 1
 _ID_MULT = 0x2545F4914F6CDD1D & _ID_MASK       # odd

@@ -49,6 +49,9 @@ def parse():
                     help="also time each of the five workload shapes (adds a 'configs' field)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (known bytes) for counter scaling")
+    ap.add_argument("--only-workloads", default="",
+                    help="time only the joins of these workload shapes (e.g. 3,5), without the "
+                         "benchmark step, the sort or the id map: for per-workload counter passes")
     return ap.parse_args()
 
 
@@ -85,11 +88,24 @@ def time_launches(torch, fn, iters, warm=5):
     return ms[len(ms) // 2], sum(ms) / len(ms)
 
 
-def all_configs(torch, P, W, dev, seed):
-    """Per-launch time and algorithmic bandwidth of each workload shape at full size."""
+def calibration_copy(torch, dev):
+    """Four plain 256 MiB device-to-device copies: known bytes for scaling traffic counters."""
+    src = torch.empty(1 << 28, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(4):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def all_configs(torch, P, W, dev, seed, only=(1, 2, 3, 4, 5), joins_only=False):
+    """Per-launch time and algorithmic bandwidth of each workload shape at full size (only the
+    join launches of the listed shapes when joins_only)."""
     res = {}
     st10 = None
     for i in (1, 2, 3, 4, 5):
+        if i not in only:
+            continue
         s, r = W.SHAPES[i]
         if i == 1:
             st = W.make_store(s, seed, device=dev)
@@ -124,7 +140,7 @@ def all_configs(torch, P, W, dev, seed):
                                            b.keys, b.edge_rows, out, hit, extra_keys=ex)
             entry = "cc_join_batched"
         med, mean = time_launches(torch, fn, 100 if n < 500_000 else 30)
-        if i == 3:
+        if i == 3 and not joins_only:
             # The same requests written into the padded [B, n_max] layout of the paper's batching
             # (pad rows and the valid mask are extra output bytes).
             n_max = r.n_cand
@@ -143,7 +159,7 @@ def all_configs(torch, P, W, dev, seed):
                                "hbm_gbps": algp / (pm / 1e3) / 1e9,
                                "hbm_frac_of_peak": algp / (pm / 1e3) / 1e9 / PEAK_GBPS}
             del outp, hitp, valid
-        if i in (2, 3, 5):
+        if i in (2, 3, 5) and not joins_only:
             # Alg. 1 Step 1 on the same records (shuffled within each viewer): the sort that
             # precedes the join when affinity records arrive unsorted.
             bs = b if i != 2 else W.pack(W.make_requests(st10, r, seed, n_viewers=64))
@@ -173,7 +189,8 @@ def all_configs(torch, P, W, dev, seed):
                        "hbm_frac_of_peak": alg / (med / 1e3) / 1e9 / PEAK_GBPS}
         del out, hit, b, reqs
         torch.cuda.empty_cache()
-    res.update(index_workloads(torch, P, W, dev, seed))
+    if not joins_only:
+        res.update(index_workloads(torch, P, W, dev, seed))
     return res
 
 
@@ -344,6 +361,14 @@ def main():
         __graft_entry__.build()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.only_workloads:
+        ids = tuple(int(x) for x in args.only_workloads.split(","))
+        res = all_configs(torch, P, W, dev, args.seed, only=ids, joins_only=True)
+        if args.calibration_copy:
+            calibration_copy(torch, dev)
+        print(json.dumps({"metric": METRIC, "only_workloads": list(ids), "configs": res}),
+              flush=True)
+        return
     s, r = W.SHAPES[2]
     st = W.make_store(s, args.seed, device=dev)
     store = P.cc_store_create(st.author_id, st.doc_rows)
@@ -430,12 +455,7 @@ def main():
                "candidates_per_request": singles[0][0].cand_idx.numel()}
 
     if args.calibration_copy:
-        src = torch.empty(1 << 28, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(4):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        calibration_copy(torch, dev)
 
     cpu = None
     if not args.no_cpu_baseline:

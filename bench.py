@@ -140,6 +140,22 @@ def all_configs(torch, P, W, dev, seed, only=(1, 2, 3, 4, 5), joins_only=False):
                                            b.keys, b.edge_rows, out, hit, extra_keys=ex)
             entry = "cc_join_batched"
         med, mean = time_launches(torch, fn, 100 if n < 500_000 else 30)
+        if i == 2 and not joins_only:
+            # The paper's serving batch (b = 8 requests per launch, §6.3.1) of this shape.
+            b8 = W.pack(W.make_requests(st10, r, seed, n_viewers=8))
+            n8 = b8.cand_idx.numel()
+            out8 = torch.empty(n8, wd + we, dtype=torch.uint8, device=dev)
+            hit8 = torch.empty(n8, 1, dtype=torch.int8, device=dev)
+            fn8 = lambda: P.cc_join_batched(store, b8.cand_offsets, b8.cand_idx, b8.key_offsets,
+                                            b8.keys, b8.edge_rows, out8, hit8)
+            m8, mean8 = time_launches(torch, fn8, 100)
+            alg8 = algorithmic_bytes(torch, st10, b8, wd, we, 1, P.cc_store_layout(store)[0])
+            res["2-batch8"] = {"entry": "cc_join_batched", "viewers": 8, "candidates": n8,
+                               "ms_median": m8, "ms_mean": mean8,
+                               "candidates_per_s": n8 / (m8 / 1e3), "algorithmic_bytes": alg8,
+                               "hbm_gbps": alg8 / (m8 / 1e3) / 1e9,
+                               "hbm_frac_of_peak": alg8 / (m8 / 1e3) / 1e9 / PEAK_GBPS}
+            del b8, out8, hit8
         if i == 3 and not joins_only:
             # The same requests written into the padded [B, n_max] layout of the paper's batching
             # (pad rows and the valid mask are extra output bytes).

@@ -46,7 +46,7 @@ struct JoinArgs {
     int32_t lds_keys;            // capacity of the dynamic LDS key table
     int32_t fence_stride;        // 0 = chosen per viewer segment
     int32_t fence_budget;        // fences staged per candidate of a segment (automatic stride)
-    bool one_wave;               // automatic grid: one resident wave, not 1.5
+    bool one_wave;               // automatic grid: one resident wave (long key lists)
     int32_t n_wg;                // workgroups launched (a multiple of 8); set by launch_join
     int64_t per_wg;              // candidates per workgroup (multiple of kBlock); set by launch_join
 };

@@ -507,16 +507,23 @@ hipError_t launch_one(JoinArgs &a, int32_t workgroups, int device, hipStream_t s
     });
     if (err != hipSuccess)
         return err;
-    // Grid: about 1.5 resident waves of workgroups (a slight oversubscription lets early
-    // finishers take the remaining ranges), or exactly one wave for long key lists, each
-    // owning a contiguous range of whole sub-tiles, rounded to a multiple of 8 so that each
-    // XCD gets an equal share.
+    // Grid: each workgroup owns a contiguous range of whole sub-tiles; the count is rounded to
+    // a multiple of 8 so that each XCD gets an equal share.
+    //   * Long key lists: one resident wave (the whole LDS table allows one workgroup per CU).
+    //   * At least two sub-tiles per CU: one workgroup per CU. Fewer, longer ranges pay the
+    //     fence staging and the pipeline's fill and drain once per CU; on launches of 300k to
+    //     3.2M candidates this beat every larger grid, by up to 17% at 400k.
+    //   * Smaller launches: about 1.5 resident waves, at most one workgroup per sub-tile.
     const int64_t tiles = (a.total_cand + kBlock - 1) / kBlock;
     int64_t n_wg = workgroups;
     if (n_wg <= 0) {
-        n_wg = (int64_t)cu_count(device) * resident_per_cu(fn, lds);
-        if (!a.one_wave)
-            n_wg = n_wg * 3 / 2;
+        const int64_t cus = cu_count(device);
+        if (a.one_wave)
+            n_wg = cus * resident_per_cu(fn, lds);
+        else if (tiles >= 2 * cus)
+            n_wg = cus;
+        else
+            n_wg = cus * resident_per_cu(fn, lds) * 3 / 2;
     }
     if (n_wg > tiles)
         n_wg = tiles;

@@ -3,7 +3,6 @@ a counter reset, resolve (Eq. 6) and join (Eq. 1) captured once and replayed wit
 every replay checked against the same calls made eagerly."""
 from __future__ import annotations
 
-import numpy as np
 import pytest
 import torch
 

@@ -7,7 +7,6 @@ which gives it the same answer as the full store.
 """
 from __future__ import annotations
 
-import numpy as np
 import pytest
 import torch
 

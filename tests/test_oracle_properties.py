@@ -9,7 +9,6 @@ Ids come from a small pool that includes the int64 extremes, so keys collide and
 from __future__ import annotations
 
 import numpy as np
-import pytest
 import torch
 from hypothesis import HealthCheck, given, settings, strategies as st
 

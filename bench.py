@@ -447,28 +447,55 @@ def main():
                 "hbm_gbps": alg_cold / (ms_cold / 1e3) / 1e9,
                 "hbm_frac_of_peak": alg_cold / (ms_cold / 1e3) / 1e9 / PEAK_GBPS}
 
-    # Per-request latency: single cc_join calls cycling through 64 distinct requests.
+    # Per-request latency: one request at a time on an idle stream, cycling through 64
+    # distinct requests. Each call is timed twice: HIP events around it on the stream, and host
+    # wall time from the call until the stream has finished it.
     lat = None
     if args.latency_calls:
-        singles = [(q, torch.empty(q.cand_idx.numel(), wd + we, dtype=torch.uint8, device=dev),
-                    torch.empty(q.cand_idx.numel(), 1, dtype=torch.int8, device=dev))
+        def timed_calls(calls, n):
+            ev, wall = [], []
+            for i in range(n):
+                call = calls[i % len(calls)]
+                torch.cuda.synchronize()
+                a, bb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                t0 = time.perf_counter()
+                a.record()
+                call()
+                bb.record()
+                bb.synchronize()
+                wall.append((time.perf_counter() - t0) * 1e3)
+                ev.append(a.elapsed_time(bb))
+            ev.sort()
+            wall.sort()
+            pick = lambda xs, p: xs[min(len(xs) - 1, int(p * len(xs)))]
+            return {"p50_ms": pick(ev, 0.50), "p99_ms": pick(ev, 0.99),
+                    "wall_p50_ms": pick(wall, 0.50), "wall_p99_ms": pick(wall, 0.99),
+                    "calls": n}
+
+        def single(q, o, h):
+            return lambda: P.cc_join(store, q.cand_idx, q.keys, q.edge_rows, o, h)
+        singles = [single(q, torch.empty(q.cand_idx.numel(), wd + we, dtype=torch.uint8,
+                                         device=dev),
+                          torch.empty(q.cand_idx.numel(), 1, dtype=torch.int8, device=dev))
                    for q in batches[0][0]]
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(args.latency_calls)]
-        for i in range(32):
-            q, o, h = singles[i % len(singles)]
-            P.cc_join(store, q.cand_idx, q.keys, q.edge_rows, o, h)
-        torch.cuda.synchronize()
-        for i, (a, bb) in enumerate(evs):
-            q, o, h = singles[i % len(singles)]
-            a.record()
-            P.cc_join(store, q.cand_idx, q.keys, q.edge_rows, o, h)
-            bb.record()
-        torch.cuda.synchronize()
-        ms = sorted(a.elapsed_time(bb) for a, bb in evs)
-        pick = lambda p: ms[min(len(ms) - 1, int(p * len(ms)))]
-        lat = {"p50_ms": pick(0.50), "p99_ms": pick(0.99), "calls": len(ms),
-               "candidates_per_request": singles[0][0].cand_idx.numel()}
+        timed_calls(singles, 32)                            # warm-up
+        lat = timed_calls(singles, args.latency_calls)
+        lat["candidates_per_request"] = batches[0][0][0].cand_idx.numel()
+        # The second-degree double join (100,000 candidates, 20,000 keys, two lookups), one
+        # request per launch on the same store.
+        _, r4 = W.SHAPES[4]
+        dj = []
+        for q in W.make_requests(st, r4, args.seed, n_viewers=16):
+            b1 = W.pack([q])
+            o = torch.empty(q.cand_idx.numel(), wd + 2 * we, dtype=torch.uint8, device=dev)
+            h = torch.empty(q.cand_idx.numel(), 2, dtype=torch.int8, device=dev)
+            dj.append((lambda b1=b1, o=o, h=h: P.cc_join_batched(
+                store, b1.cand_offsets, b1.cand_idx, b1.key_offsets, b1.keys, b1.edge_rows, o,
+                h, extra_keys=[b1.actor])))
+        timed_calls(dj, 16)
+        lat["double_join"] = timed_calls(dj, min(args.latency_calls, 512))
+        lat["double_join"]["candidates_per_request"] = r4.n_cand
+        del dj
 
     if args.calibration_copy:
         calibration_copy(torch, dev)

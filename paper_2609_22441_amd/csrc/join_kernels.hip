@@ -83,6 +83,26 @@ __device__ __forceinline__ void scan_window(const int64_t *gk, int64_t K, int64_
     }
 }
 
+// Inspect the W keys gk[w0 .. w0 + W), all in bounds: count those < x and note any equal to x.
+// The keys are read as W / 2 loads of 16 bytes each at the list's 8-byte alignment (global
+// loads need only dword alignment), half the load instructions of one load per key. A lane's
+// loads reach scattered lines, so the vector memory unit's cost grows with the instruction
+// count rather than the bytes.
+template <int W>
+__device__ __forceinline__ void scan_block(const int64_t *gk, int64_t w0, int64_t x, int64_t &cnt,
+                                           bool &eq) {
+    typedef long long pair_t __attribute__((ext_vector_type(2)));
+    pair_t k[W / 2];
+#pragma unroll
+    for (int t = 0; t < W / 2; ++t)
+        __builtin_memcpy(&k[t], gk + w0 + 2 * t, sizeof(pair_t));
+#pragma unroll
+    for (int t = 0; t < W / 2; ++t) {
+        cnt += (k[t].x < x ? 1 : 0) + (k[t].y < x ? 1 : 0);
+        eq |= (k[t].x == x) | (k[t].y == x);
+    }
+}
+
 // Index in [0, K) of the leftmost key equal to x, or -1.
 __device__ __forceinline__ int64_t find_key(int64_t x, const int64_t *tab, int64_t M, int S,
                                             const int64_t *gk, int64_t K) {
@@ -93,28 +113,34 @@ __device__ __forceinline__ int64_t find_key(int64_t x, const int64_t *tab, int64
         return (g < K && tab[g] == x) ? g : -1;
     if (g == 0)
         return tab[0] == x ? 0 : -1;
-    // k[(g-1)S] < x <= k[gS]: the lower bound lies in [lo, lo + len].
+    // k[(g-1)S] < x <= k[gS]: the lower bound lies in [lo, min(gS, K)].
     int64_t lo = (g - 1) * S + 1;
-    int64_t len = min(g * (int64_t)S, K) - lo;
     int64_t cnt = 0;
     bool eq = false;
-    switch (S) {
-    case 2: scan_window<2>(gk, K, lo, len, x, cnt, eq); break;
-    case 4: scan_window<4>(gk, K, lo, len, x, cnt, eq); break;
-    case 8: scan_window<8>(gk, K, lo, len, x, cnt, eq); break;
-    case 16: scan_window<16>(gk, K, lo, len, x, cnt, eq); break;
-    default: {
-        // Strides beyond 16 (only when K exceeds 16x the LDS table): narrow in global memory.
-        const int64_t *w = gk + lo;
-        while (len > kWindow) {
-            const int64_t half = len >> 1;
-            w = (w[half] < x) ? w + half : w;
-            len -= half;
+    if (S <= 16 && K >= S) {
+        // Read S keys from w0 = min(lo, K - S): the window [lo, lo + S) moved back, if needed,
+        // to end at K. Every key before lo is <= k[(g-1)S] < x, so the keys < x in the window
+        // number (lower bound - w0) either way, and a key equal to x, if any, is in the window.
+        const int64_t w0 = min(lo, K - S);
+        switch (S) {
+        case 2: scan_block<2>(gk, w0, x, cnt, eq); break;
+        case 4: scan_block<4>(gk, w0, x, cnt, eq); break;
+        case 8: scan_block<8>(gk, w0, x, cnt, eq); break;
+        default: scan_block<16>(gk, w0, x, cnt, eq); break;
         }
-        lo = w - gk;
-        scan_window<kWindow + 1>(gk, K, lo, len, x, cnt, eq);
+        return eq ? w0 + cnt : -1;
     }
+    // Strides beyond 16 (only when K exceeds 16x the LDS table), or a list shorter than a forced
+    // stride: narrow in global memory, then inspect the last few keys with clamped loads.
+    int64_t len = min(g * (int64_t)S, K) - lo;
+    const int64_t *w = gk + lo;
+    while (len > kWindow) {
+        const int64_t half = len >> 1;
+        w = (w[half] < x) ? w + half : w;
+        len -= half;
     }
+    lo = w - gk;
+    scan_window<kWindow + 1>(gk, K, lo, len, x, cnt, eq);
     return eq ? lo + cnt : -1;
 }
 

@@ -7,6 +7,7 @@
 namespace ccj {
 
 constexpr int kBlock = 256;          // threads per workgroup = candidates per sub-tile
+constexpr int kBalanceViewers = 4 * kBlock;   // CSR batches up to this size get weighted ranges
 constexpr int kWindow = 15;          // keys between two fences read from L2 in one step
 constexpr int kMaxLdsKeys = 18432;   // LDS key table limit: 144 KiB + at most 12 KiB of static
                                      // tables stays within the 160 KiB a workgroup may use
@@ -47,6 +48,7 @@ struct JoinArgs {
     int32_t fence_stride;        // 0 = chosen per viewer segment
     int32_t fence_budget;        // fences staged per candidate of a segment (automatic stride)
     bool one_wave;               // automatic grid: one resident wave (long key lists)
+    bool balanced;               // CSR ranges weighted by an estimated cost per candidate
     int32_t n_wg;                // workgroups launched (a multiple of 8); set by launch_join
     int64_t per_wg;              // candidates per workgroup (multiple of kBlock); set by launch_join
 };

@@ -172,6 +172,107 @@ __device__ __forceinline__ int64_t range_index(int b, int n) {
     return (int64_t)(b & 7) * per_xcd + (b >> 3);
 }
 
+// Estimated cost of one candidate of a viewer with K keys when the LDS table holds T keys, in
+// thousandths of the cost of a candidate of a short list. Fitted to join times of 64-viewer
+// batches whose lists all have one length (100 to 30,000 keys): a candidate of a 30,000-key
+// list costs about 25% more than one of a 100-key list, mostly from the window reads between
+// fences once K exceeds the table. Only the split of the work depends on it, never the result.
+__device__ __forceinline__ int64_t cand_cost(int64_t K, int64_t T) {
+    K = min<int64_t>(K, (int64_t)1 << 24);
+    int64_t c = 1000 + min(K, T) * 15 / 1000;
+    if (K > T)
+        c += 45 + (K - T) * 11 / 2000;
+    return c;
+}
+
+__device__ __forceinline__ int64_t wave_scan_incl(int64_t x) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int64_t y = __shfl_up(x, d);
+        if (lane >= d)
+            x += y;
+    }
+    return x;
+}
+
+// Weighted ranges for a CSR batch of at most kBalanceViewers viewers. Candidate i of viewer v
+// weighs w_v = cand_cost(K_v); with prefix weights P, logical range r of n covers the candidates
+// whose weight starts in [T_r, T_{r+1}), T_r = floor(r * W / n), W the total. Every workgroup
+// computes the same prefix, so the ranges tile the candidates. Ranges of equal weight take
+// fewer candidates of long lists, which would otherwise finish last. Returns the range and the
+// viewer holding its first candidate; s is kBlock entries of LDS scratch (unused yet).
+__device__ __forceinline__ void balanced_range(const JoinArgs &a, int64_t r, int64_t n,
+                                               int64_t *s, int64_t &begin, int64_t &end,
+                                               int32_t &v_first) {
+    constexpr int R = kBalanceViewers / kBlock;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int32_t B = a.n_viewers;
+    int64_t w[R], vb[R], c[R];
+    int64_t mine = 0;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const int64_t v = (int64_t)i * kBlock + tid;
+        w[i] = 0;
+        vb[i] = 0;
+        c[i] = 1;
+        if (v < B) {
+            vb[i] = clamp64(a.cand_offsets[v], a.total_cand);
+            const int64_t ve = clamp64(a.cand_offsets[v + 1], a.total_cand);
+            const int64_t kb = clamp64(a.key_offsets[v], a.total_keys);
+            const int64_t ke = max(kb, clamp64(a.key_offsets[v + 1], a.total_keys));
+            c[i] = cand_cost(ke - kb, a.lds_keys);
+            w[i] = max<int64_t>(ve - vb[i], 0) * c[i];
+        }
+        mine += w[i];
+    }
+    // Total weight.
+    int64_t t = mine;
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1)
+        t += __shfl_xor(t, d);
+    if (lane == 0)
+        s[wave] = t;
+    if (tid == 0) {
+        s[8] = a.total_cand;                      // range start, if no viewer holds T_r
+        s[9] = B;                                 // its viewer
+        s[10] = a.total_cand;                     // range end, if no viewer holds T_{r+1}
+    }
+    lds_barrier();
+    const int64_t W = s[0] + s[1] + s[2] + s[3];
+    const int64_t q = W / n, m = W % n;
+    const int64_t t0 = q * r + m * r / n, t1 = q * (r + 1) + m * (r + 1) / n;
+    lds_barrier();
+    // Prefix weights in viewer order, one chunk of kBlock viewers at a time.
+    int64_t carry = 0;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        if (i * kBlock >= B)                      // uniform: the same for every thread
+            break;
+        const int64_t inc = wave_scan_incl(w[i]);
+        if (lane == 63)
+            s[wave] = inc;
+        lds_barrier();
+        int64_t pre = carry + inc - w[i];
+        for (int k = 0; k < wave; ++k)
+            pre += s[k];
+        carry += s[0] + s[1] + s[2] + s[3];
+        if (w[i] > 0) {
+            if (t0 >= pre && t0 < pre + w[i]) {
+                s[8] = vb[i] + (t0 - pre + c[i] - 1) / c[i];
+                s[9] = (int64_t)i * kBlock + tid;
+            }
+            if (t1 >= pre && t1 < pre + w[i])
+                s[10] = vb[i] + (t1 - pre + c[i] - 1) / c[i];
+        }
+        lds_barrier();
+    }
+    begin = s[8];
+    v_first = (int32_t)s[9];
+    end = s[10];
+    lds_barrier();                                // s is reused by the caller
+}
+
 // Copy a full sub-tile (kBlock rows) whose widths are compile-time chunk counts. Thread tid
 // takes chunks e = i * kBlock + tid of the sub-tile's output, i.e. row e / CH, 16-byte column
 // e % CH, so each wavefront store covers 1 KiB of contiguous output (whole 128-byte lines: a
@@ -394,29 +495,34 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
     __shared__ unsigned int s_invalid;
 
     const int tid = threadIdx.x;
-    int64_t begin = range_index(blockIdx.x, gridDim.x) * a.per_wg;
-    const int64_t end = min(begin + a.per_wg, a.total_cand);
+    constexpr bool batched = BATCHED;
+    const int32_t B = batched ? a.n_viewers : 1;
+    const int64_t rng = range_index(blockIdx.x, gridDim.x);
+    int64_t begin, end;
+    int32_t v = 0;                                // first viewer that may hold `begin`
+    if (batched && a.balanced) {
+        balanced_range(a, rng, gridDim.x, s_src[0], begin, end, v);
+    } else {
+        begin = rng * a.per_wg;
+        end = min(begin + a.per_wg, a.total_cand);
+        if (batched && begin < end) {
+            // First viewer whose candidate range ends after `begin`.
+            int32_t lo = 0, hi = B;
+            while (lo < hi) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (clamp64(a.cand_offsets[mid + 1], a.total_cand) <= begin)
+                    lo = mid + 1;
+                else
+                    hi = mid;
+            }
+            v = lo;
+        }
+    }
     if (begin >= end)
         return;
     if (tid == 0)
         s_invalid = 0;
     const uint8_t *miss_row = a.def_row ? a.def_row : a.zero_row;
-
-    constexpr bool batched = BATCHED;
-    const int32_t B = batched ? a.n_viewers : 1;
-    // First viewer whose candidate range ends after `begin`.
-    int32_t v = 0;
-    if (batched) {
-        int32_t lo = 0, hi = B;
-        while (lo < hi) {
-            const int32_t mid = (lo + hi) >> 1;
-            if (clamp64(a.cand_offsets[mid + 1], a.total_cand) <= begin)
-                lo = mid + 1;
-            else
-                hi = mid;
-        }
-        v = lo;
-    }
 
     for (; v < B && begin < end; ++v) {
         int64_t vb = 0, ve = a.total_cand, kb = 0, ke = a.total_keys;
@@ -557,7 +663,8 @@ hipError_t launch_one(JoinArgs &a, int32_t workgroups, int device, hipStream_t s
         n_wg = 1;
     const int64_t tiles_per_wg = (tiles + n_wg - 1) / n_wg;
     a.per_wg = tiles_per_wg * kBlock;
-    n_wg = (a.total_cand + a.per_wg - 1) / a.per_wg;
+    if (!a.balanced)                      // equal ranges of whole sub-tiles, none left empty
+        n_wg = (a.total_cand + a.per_wg - 1) / a.per_wg;
     n_wg = (n_wg + 7) & ~int64_t(7);
     a.n_wg = (int32_t)n_wg;
     hipLaunchKernelGGL((join_kernel<D, E, L, BATCHED, A32>), dim3(a.n_wg), dim3(kBlock), lds, stream,

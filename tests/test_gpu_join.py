@@ -473,3 +473,45 @@ def test_thousands_of_small_viewers():
     tc = W.TinyCase(author, doc, W.pack(reqs), None, 1)
     for t in (None, (4, 0, 0), (0, 0, 8)):
         _tiny(tc, t, what=f"3000 viewers tuning {t}")
+
+
+def _skewed_batch(n_viewers, seed, n_lookups):
+    """Viewers with skewed work: about 10% without candidates, every 97th with 3,000, the rest
+    0 to 300; lists of 0 to 200 keys, every 50th with 9,000 to 12,000 (beyond the LDS table)."""
+    g = W.gen("cpu", seed, n_viewers)
+    n_docs, n_ids = 20_000, 40_000
+    author = torch.randint(0, n_ids, (n_docs,), generator=g)
+    doc = torch.randint(0, 256, (n_docs, 64), generator=g, dtype=torch.int64).to(torch.uint8)
+    reqs = []
+    for v in range(n_viewers):
+        big = v % 50 == 7
+        k = int(torch.randint(9_000, 12_001, (1,), generator=g)) if big else \
+            int(torch.randint(0, 201, (1,), generator=g))
+        keys = torch.sort(torch.randperm(n_ids, generator=g)[:k]).values
+        edge = torch.randint(0, 256, (k, 32), generator=g, dtype=torch.int64).to(torch.uint8)
+        if v % 10 == 3:
+            n = 0
+        elif v % 97 == 5:
+            n = 3_000
+        else:
+            n = int(torch.randint(0, 301, (1,), generator=g))
+        cand = torch.randint(-1, n_docs + 1, (n,), generator=g)
+        actor = None
+        if n_lookups == 2:
+            pick = keys[torch.randint(0, max(k, 1), (n,), generator=g)] if k else \
+                torch.full((n,), -1, dtype=torch.int64)
+            actor = torch.where(torch.rand(n, generator=g) < 0.5, pick, torch.full_like(pick, -1))
+        reqs.append(W.Request(keys, edge, cand, actor))
+    return W.TinyCase(author, doc, W.pack(reqs), None, n_lookups)
+
+
+@pytest.mark.parametrize("n_viewers", [2, 255, 256, 257, 700, 1024, 1025])
+def test_weighted_ranges_around_the_viewer_limit(n_viewers):
+    """CSR batches of up to 1,024 viewers split their candidates by estimated cost (more than
+    one 256-viewer chunk of the prefix for 257 and up); 1,025 falls back to equal ranges. Every
+    split must cover each candidate once: bit-exact with the oracle, automatic and fixed grids."""
+    note(f"weighted ranges, {n_viewers} viewers")
+    for n_lookups in (1, 2):
+        tc = _skewed_batch(n_viewers, 41, n_lookups)
+        for t in (None, (0, 0, 8), (0, 0, 1000)):
+            _tiny(tc, t, what=f"{n_viewers} viewers, {n_lookups} lookups, tuning {t}")

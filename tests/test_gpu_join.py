@@ -515,3 +515,43 @@ def test_weighted_ranges_around_the_viewer_limit(n_viewers):
         tc = _skewed_batch(n_viewers, 41, n_lookups)
         for t in (None, (0, 0, 8), (0, 0, 1000)):
             _tiny(tc, t, what=f"{n_viewers} viewers, {n_lookups} lookups, tuning {t}")
+
+
+@pytest.mark.parametrize("tuning", [None, (0, 0, 8), (4, 0, 0)])
+def test_offsets_that_break_the_rules_stay_in_bounds(tuning):
+    """Offsets that break the CSR rules (a decreasing pair, a negative entry, entries past the
+    totals) give an unspecified result, but the kernels clamp them: the call completes, and
+    every row it writes has its candidate's exact doc segment and a hit byte of 0 or 1."""
+    note(f"offsets that break the CSR rules, tuning {tuning}")
+    for seed in range(8):
+        tc = W.tiny_case(9300 + seed, max_k=120, max_n=300, max_viewers=6, n_lookups=1,
+                         dup_keys=False)
+        b = tc.batch
+        B = b.cand_offsets.numel() - 1
+        co, ko = b.cand_offsets.clone(), b.key_offsets.clone()
+        tc_n, tk_n = b.cand_idx.numel(), b.keys.numel()
+        kind = seed % 4
+        if kind == 0 and B >= 2:
+            co[1], co[2] = co[2].item() + 5, max(co[1].item() - 3, 0)
+        elif kind == 1:
+            co[B] = tc_n + 1000
+            ko[B] = tk_n + 1000
+        elif kind == 2 and B >= 2:
+            co[1] = -50
+            ko[1] = -7
+        else:
+            ko[:] = ko.flip(0)
+        bad = W.Batch(co, b.cand_idx, ko, b.keys, b.edge_rows, None)
+        wd, we = row_bytes(tc.doc_rows), row_bytes(b.edge_rows)
+        store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+        try:
+            out, hit = gpu_join(store, None, bad.to(DEV), wd, we, 1, tuning=_tuning(tuning))
+        finally:
+            P.cc_store_destroy(store)
+        doc = tc.doc_rows.numpy()
+        cand = b.cand_idx.tolist()
+        for j in np.flatnonzero(hit[:, 0] != -7):
+            assert hit[j, 0] in (0, 1), f"seed {seed}: hit byte {hit[j, 0]}"
+            c = cand[j]
+            want = doc[c] if 0 <= c < doc.shape[0] else np.zeros(wd, np.uint8)
+            assert np.array_equal(out[j, :wd], want), f"seed {seed}: doc segment of row {j}"

@@ -298,6 +298,8 @@ CC_API cc_status cc_store_create_indexed(cc_store **out_store, int64_t capacity,
  * returned with the store unchanged. Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_NOT_SUPPORTED,
  * CC_ERR_STORE_FULL, CC_ERR_DEVICE.
  */
+/* Workspace bytes cc_store_upsert needs for n_records; 0 when n_records <= 0 or > 2^30 (a
+ * batch the upsert rejects). */
 CC_API int64_t cc_upsert_workspace_bytes(int64_t n_records);
 CC_API cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc_ids,
                                  const int64_t *author_ids, const void *doc_rows, void *workspace,
@@ -354,6 +356,8 @@ CC_API cc_status cc_resolve_ids(const cc_store *store, const int64_t *doc_ids, i
  * clamped to [0, total_keys] and every access stays inside the buffers. Asynchronous on
  * `stream`. Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_DEVICE.
  */
+/* Workspace bytes cc_sort_affinity needs; 0 when there is nothing to sort or total_keys >=
+ * 2^32 (counts the sort rejects). */
 CC_API int64_t cc_sort_workspace_bytes(int64_t total_keys, int32_t n_viewers);
 CC_API cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets,
                                   const int64_t *keys_in, const void *rows_in, int32_t row_bytes,
@@ -372,8 +376,9 @@ CC_API cc_status cc_validate_keys(const int64_t *key_offsets, const int64_t *edg
                            int32_t n_viewers, int64_t total_keys, int64_t *first_bad_viewer,
                            hipStream_t stream);
 
-/* Static string naming a status code. */
-CC_API const char *cc_status_string(cc_status status);
+/* Static string naming a status code. Takes any int (a cc_status converts implicitly): a
+ * value that names no status gives "CC_UNKNOWN_STATUS". */
+CC_API const char *cc_status_string(int status);
 
 /* The hipError_t of the last CC_ERR_DEVICE returned on the calling thread (0 if none). */
 CC_API int cc_last_device_error(void);

@@ -683,7 +683,9 @@ cc_status cc_validate_keys(const int64_t *key_offsets, const int64_t *edge_keys,
     return CC_OK;
 }
 
-const char *cc_status_string(cc_status status) {
+// An int, not the enum: C callers may pass any value, and a C++ enum parameter outside the
+// enumerators' range would be undefined behaviour here.
+const char *cc_status_string(int status) {
     switch (status) {
     case CC_OK: return "CC_OK";
     case CC_ERR_INVALID_ARGUMENT: return "CC_ERR_INVALID_ARGUMENT";

@@ -424,7 +424,7 @@ hipError_t launch_resolve(const MapEntry *map, int64_t n_groups, const int64_t *
 }
 
 int64_t upsert_workspace_bytes(int64_t n) {
-    if (n <= 0)
+    if (n <= 0 || n > kMaxBatch)            // the upsert rejects larger batches
         return 0;
     const int64_t blocks = (n + kScanBlock - 1) / kScanBlock;
     return round_up(n * 8) + round_up(n * 4) + round_up((blocks + 1) * 4) + 256;

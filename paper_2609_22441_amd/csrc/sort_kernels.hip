@@ -547,10 +547,12 @@ constexpr int kRangeSlots = 1024;   // range_kernel workgroups at most
 }  // namespace
 
 int64_t sort_workspace_bytes(int64_t total, int32_t n_viewers) {
-    if (total <= 0 || n_viewers <= 0)
+    // Counts the sort rejects (total >= 2^32) need no workspace; this also keeps the products
+    // below far from overflow.
+    if (total <= 0 || n_viewers <= 0 || total >= ((int64_t)1 << 32))
         return 0;
-    return 2 * round_up(total * (int64_t)sizeof(Wide::T)) + round_up((n_viewers + 1) * 8) + 256 +
-           round_up(2 * kRangeSlots * 8);
+    return 2 * round_up(total * (int64_t)sizeof(Wide::T)) + round_up(((int64_t)n_viewers + 1) * 8) +
+           256 + round_up(2 * kRangeSlots * 8);
 }
 
 hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
@@ -563,7 +565,8 @@ hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int6
     void *buf0 = w;
     void *buf1 = w + buf_bytes;
     int64_t *tile_off = reinterpret_cast<int64_t *>(w + 2 * buf_bytes);
-    int64_t *range = reinterpret_cast<int64_t *>(w + 2 * buf_bytes + round_up((n_viewers + 1) * 8));
+    int64_t *range =
+        reinterpret_cast<int64_t *>(w + 2 * buf_bytes + round_up(((int64_t)n_viewers + 1) * 8));
     int64_t *slots = range + 32;                       // 256 bytes after range
     // Upper bound on tiles (every viewer adds at most one partial tile); larger counts are
     // covered by the kernels' grid-stride loops.

@@ -93,6 +93,7 @@ def test_sort_workspace_size():
     assert lib.cc_sort_workspace_bytes(-5, 3) == 0
     assert lib.cc_sort_workspace_bytes(100, 0) == 0
     assert lib.cc_sort_workspace_bytes(4097, 2) >= 2 * 16 * 4097 + 3 * 8   # ping-pong + plan
+    assert lib.cc_sort_workspace_bytes(1 << 32, 1) == 0             # more than the sort takes
 
 
 def test_sort_rejects_bad_arguments():
@@ -144,6 +145,7 @@ def test_upsert_and_resolve_reject_bad_arguments():
     assert lib.cc_upsert_workspace_bytes(0) == 0
     assert lib.cc_upsert_workspace_bytes(-3) == 0
     assert lib.cc_upsert_workspace_bytes(1000) >= 12 * 1000
+    assert lib.cc_upsert_workspace_bytes((1 << 30) + 1) == 0        # more than a batch takes
 
 
 def test_library_has_no_cpu_fallback(monkeypatch, tmp_path):

@@ -555,3 +555,19 @@ def test_offsets_that_break_the_rules_stay_in_bounds(tuning):
             c = cand[j]
             want = doc[c] if 0 <= c < doc.shape[0] else np.zeros(wd, np.uint8)
             assert np.array_equal(out[j, :wd], want), f"seed {seed}: doc segment of row {j}"
+
+
+def test_store_too_large_for_the_device_is_out_of_memory():
+    """A store that cannot fit returns CC_ERR_OUT_OF_MEMORY, frees what it had allocated, and
+    leaves the library usable (2^31 - 1 rows of 1 MiB: its id column fits, its rows do not)."""
+    note("store larger than device memory")
+    torch.cuda.synchronize()
+    free0, _ = torch.cuda.mem_get_info()
+    with pytest.raises(B.CCError) as err:
+        P.cc_store_create_indexed((1 << 31) - 1, 1 << 20)
+    assert err.value.status == B.CC_ERR_OUT_OF_MEMORY
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info()
+    assert abs(free1 - free0) < (64 << 20), (free0, free1)      # nothing left allocated
+    tc = W.tiny_case(77, max_viewers=3, n_lookups=1)
+    _tiny(tc, None, what="a join after the failed allocation")

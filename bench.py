@@ -354,10 +354,28 @@ def cpu_baseline(st_cpu, reqs_cpu, seconds):
                 done[0] += c
                 n_req += 1
     dt = time.perf_counter() - t0
+    # The same oracle on one thread, for the per-core rate.
+    t1, n1, c1 = time.perf_counter(), 0, 0
+    while time.perf_counter() - t1 < min(3.0, seconds):
+        c1 += one(reqs_cpu[n1 % len(reqs_cpu)])
+        n1 += 1
+    dt1 = time.perf_counter() - t1
     return {"value": done[0] / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
             "sample": f"{n_req} single-viewer requests of the benchmark workload "
                       f"({reqs_cpu[0].cand_idx.numel()} candidates each), lower-bound oracle, "
-                      f"one request per thread, {dt:.1f} s wall"}
+                      f"one request per thread, {dt:.1f} s wall; one thread: "
+                      f"{c1 / dt1 / 1e6:.1f} M candidates/s ({n1} requests, {dt1:.1f} s); "
+                      f"host CPU: {cpu_model()}"}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main():

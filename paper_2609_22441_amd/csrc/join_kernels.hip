@@ -5,10 +5,11 @@
 // search-and-copy: no matrix cores, no arithmetic on the row payloads.
 //
 // Work decomposition
-//   * The flattened candidate array [0, total_cand) is cut into n_wg contiguous ranges of
-//     per_wg candidates. Hardware dispatches workgroup b to XCD b % 8, so the range index is
-//     (b % 8) * (n_wg / 8) + b / 8: each XCD walks one contiguous eighth of the candidates,
-//     which keeps a viewer's keys and edge rows in a single XCD's L2.
+//   * The flattened candidate array [0, total_cand) is cut into n_wg contiguous ranges: of
+//     per_wg candidates each, or, for CSR batches of up to kBalanceViewers viewers, of equal
+//     estimated cost (balanced_range). Hardware dispatches workgroup b to XCD b % 8, so the
+//     range index is (b % 8) * (n_wg / 8) + b / 8: each XCD walks one contiguous eighth of the
+//     candidates, which keeps a viewer's keys and edge rows in a single XCD's L2.
 //   * A range is split at viewer boundaries into segments. For each segment the workgroup
 //     stages every S-th key of the viewer ("fences") into LDS; S = 1 stages the whole list.
 //   * Sub-tiles of kBlock candidates: each thread resolves one candidate (position check,
@@ -20,7 +21,8 @@
 //   g = #{ i : f[i] < x }            branch-free lower bound in LDS, ceil(log2 M) probes.
 //   S == 1 : the lower bound is g.
 //   S  > 1 : k[(g-1)*S] < x <= k[g*S], so the lower bound lies in [(g-1)*S+1, min(g*S, K)];
-//            read those (at most S) keys from global memory (L2) in one step and count.
+//            read S keys covering that window from global memory (L2) in one step, as
+//            16-byte loads, and count.
 //   hit    : some key equal to x in the inspected window; because keys ascend, the lower
 //            bound is then the leftmost equal key.
 #include <atomic>

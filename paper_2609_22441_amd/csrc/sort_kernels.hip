@@ -124,15 +124,20 @@ __device__ __forceinline__ int rounds_of(int64_t tiles) {
     return r;
 }
 
-// Largest v in [0, B) with tile_off[v] <= t (tile_off non-decreasing, tile_off[0] = 0).
+// Largest v in [0, B) with tile_off[v] <= t (tile_off non-decreasing, tile_off[0] = 0), found by
+// the whole workgroup (call it uniformly). Each round every thread probes one of kThreads
+// evenly spaced viewers; the probes at or below t are a prefix, and its length narrows the range
+// kThreads-fold. Up to kThreads viewers take one round of independent loads instead of a chain
+// of ~log2(B) dependent ones.
 __device__ __forceinline__ int64_t owner(const int64_t *tile_off, int64_t B, int64_t t) {
-    int64_t lo = 0, hi = B - 1;
+    int64_t lo = 0, hi = B - 1;                   // tile_off[lo] <= t; the answer is in [lo, hi]
     while (lo < hi) {
-        const int64_t mid = (lo + hi + 1) >> 1;
-        if (tile_off[mid] <= t)
-            lo = mid;
-        else
-            hi = mid - 1;
+        const int64_t step = (hi - lo + kThreads) / kThreads;
+        const int64_t v = lo + (int64_t)threadIdx.x * step;
+        const int c = __syncthreads_count(v <= hi && tile_off[v] <= t);   // >= 1 (probe lo)
+        const int64_t nlo = lo + (int64_t)(c - 1) * step;
+        hi = min(hi, nlo + step - 1);
+        lo = nlo;
     }
     return lo;
 }

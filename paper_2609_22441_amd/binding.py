@@ -374,6 +374,43 @@ def cc_join(store: int, cand_idx, edge_keys, edge_feats, out, hit_mask, default_
                          _stream(stream)), "cc_join")
 
 
+class PreparedJoin:
+    """cc_join with its arguments checked once, for serving loops that reuse the same buffers.
+
+    The constructor runs every check of cc_join on buffers sized for the largest request and keeps
+    the tensors alive. A call then writes the next request's candidates and keys into those
+    buffers' leading elements and passes only the counts: ``prepared(n_cand, n_keys)`` joins
+    cand_idx[:n_cand] against edge_keys[:n_keys] / edge_feats[:n_keys] into out[:n_cand] and
+    hit_mask[:n_cand]. Counts default to the full buffers and must not exceed them. Same C call
+    and semantics as cc_join; only the per-call Python work is smaller.
+    """
+
+    def __init__(self, store: int, cand_idx, edge_keys, edge_feats, out, hit_mask,
+                 default_row=None):
+        self._cap_n = cand_idx.numel()
+        self._cap_k = edge_keys.numel()
+        pc = _arr(cand_idx, "cand_idx", _i64())
+        pk, pf, pd, ew = _edge_args(edge_keys, edge_feats, self._cap_k, default_row)
+        po, stride = _out_rows(out, "out", self._cap_n, _doc_row_bytes(store) + ew)
+        ph = _arr(hit_mask, "hit_mask", _i8(), self._cap_n)
+        self._keep = (cand_idx, edge_keys, edge_feats, out, hit_mask, default_row)
+        self._head = (store, pc)
+        self._mid = (pk,)
+        self._tail = (pf, ew, pd, po, stride, ph)
+        self._fn = lib().cc_join
+
+    def __call__(self, n_cand: Optional[int] = None, n_keys: Optional[int] = None,
+                 stream=None) -> None:
+        n = self._cap_n if n_cand is None else n_cand
+        k = self._cap_k if n_keys is None else n_keys
+        if not (0 <= n <= self._cap_n and 0 <= k <= self._cap_k):
+            _fail("counts", f"must lie in [0, {self._cap_n}] and [0, {self._cap_k}] "
+                            f"(got {n}, {k})")
+        st = self._fn(*self._head, n, *self._mid, k, *self._tail, _stream(stream))
+        if st != CC_OK:
+            raise CCError(st, "cc_join")
+
+
 def _batched_args(store, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats,
                   default_row, extra_keys, total_cand, total_keys):
     """Checked inputs of the batched joins: (B, L, pointers..., extra array, edge width)."""

@@ -226,3 +226,37 @@ def test_store_and_map_checks(stub):
     assert [c[0] for c in stub.calls] == ["cc_store_create", "cc_resolve_ids",
                                           "cc_store_upsert", "cc_store_read"]
     assert stub.calls[0][1][5] == B.CC_SRC_HOST
+
+
+def test_prepared_join_passes_the_same_arguments_and_counts(stub):
+    a = join_args()
+    B.cc_join(1, stream=0, **a)
+    p = B.PreparedJoin(1, **a)
+    p(stream=0)
+    p(3, 2, stream=0)
+    (_, full), (_, prep), (_, part) = stub.calls
+    assert prep == full                                       # same call as cc_join
+    assert part[2] == 3 and part[4] == 2                      # n_cand, n_keys
+    assert part[:2] + part[3:4] + part[5:] == full[:2] + full[3:4] + full[5:]
+
+
+@pytest.mark.parametrize("arg,bad,exc,match", [
+    ("cand_idx", torch.zeros(10, dtype=torch.int64), ValueError, "GPU memory"),
+    ("edge_keys", g(6, dtype=torch.float64), TypeError, "int64"),
+    ("hit_mask", g(9, 1, dtype=torch.int8), ValueError, "elements"),
+    ("out", g(10, DOC_BYTES, dtype=torch.uint8), ValueError, "bytes"),
+])
+def test_prepared_join_checks_its_buffers_once(stub, arg, bad, exc, match):
+    a = join_args()
+    a[arg] = bad
+    with pytest.raises(exc, match=match):
+        B.PreparedJoin(1, **a)
+    assert stub.calls == []
+
+
+@pytest.mark.parametrize("n,k", [(11, 6), (10, 7), (-1, 0), (0, -1)])
+def test_prepared_join_counts_must_fit_the_buffers(stub, n, k):
+    p = B.PreparedJoin(1, **join_args())
+    with pytest.raises(ValueError, match="counts"):
+        p(n, k, stream=0)
+    assert stub.calls == []

@@ -47,3 +47,34 @@ def test_join_on_a_side_stream_is_ordered_with_torch_work():
         assert_same((out.cpu().numpy(), hit.cpu().numpy()), want, "side stream")
     finally:
         P.cc_store_destroy(store)
+
+
+def test_prepared_join_equals_cc_join():
+    """PreparedJoin over the leading elements of its buffers gives the bytes cc_join gives for
+    the same slices, for full, partial and empty counts; the full case also against the oracle."""
+    note("binding: prepared join")
+    tc = W.tiny_case(91, n_lookups=1, max_n=900, max_k=300, max_viewers=1)
+    b = tc.batch
+    wd, we = row_bytes(tc.doc_rows), row_bytes(b.edge_rows)
+    store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+    try:
+        cand, keys, feats = b.cand_idx.to(DEV), b.keys.to(DEV), b.edge_rows.to(DEV)
+        n_all, k_all = cand.numel(), keys.numel()
+        out = torch.full((n_all, wd + we), 0x5A, dtype=torch.uint8, device=DEV)
+        hit = torch.full((n_all, 1), -7, dtype=torch.int8, device=DEV)
+        prepared = P.PreparedJoin(store, cand, keys, feats, out, hit)
+        for n, k in ((n_all, k_all), (n_all // 2, k_all // 3), (0, k_all), (n_all, 0)):
+            out.fill_(0x5A)
+            hit.fill_(-7)
+            prepared(n, k)
+            ref_out = torch.full((n, wd + we), 0x5A, dtype=torch.uint8, device=DEV)
+            ref_hit = torch.full((n, 1), -7, dtype=torch.int8, device=DEV)
+            P.cc_join(store, cand[:n], keys[:k], feats[:k], ref_out, ref_hit)
+            torch.cuda.synchronize()
+            assert torch.equal(out[:n], ref_out) and torch.equal(hit[:n], ref_hit), (n, k)
+            assert bool((hit[n:] == -7).all()) and bool((out[n:] == 0x5A).all()), (n, k)
+            if (n, k) == (n_all, k_all):
+                want = oracle_join(tc.author_id, tc.doc_rows, b, 1)
+                assert_same((out.cpu().numpy(), hit.cpu().numpy()), want, "prepared join")
+    finally:
+        P.cc_store_destroy(store)

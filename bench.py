@@ -513,18 +513,24 @@ def main():
         # The second-degree double join (100,000 candidates, 20,000 keys, two lookups), one
         # request per launch on the same store.
         _, r4 = W.SHAPES[4]
-        dj = []
+        dj, dj_args = [], []
         for q in W.make_requests(st, r4, args.seed, n_viewers=16):
             b1 = W.pack([q])
             o = torch.empty(q.cand_idx.numel(), wd + 2 * we, dtype=torch.uint8, device=dev)
             h = torch.empty(q.cand_idx.numel(), 2, dtype=torch.int8, device=dev)
+            dj_args.append((b1, o, h))
             dj.append((lambda b1=b1, o=o, h=h: P.cc_join_batched(
                 store, b1.cand_offsets, b1.cand_idx, b1.key_offsets, b1.keys, b1.edge_rows, o,
                 h, extra_keys=[b1.actor])))
         timed_calls(dj, 16)
         lat["double_join"] = timed_calls(dj, min(args.latency_calls, 512))
         lat["double_join"]["candidates_per_request"] = r4.n_cand
-        del dj
+        djp = [P.PreparedJoinBatched(store, b1.cand_offsets, b1.cand_idx, b1.key_offsets, b1.keys,
+                                     b1.edge_rows, o, h, extra_keys=[b1.actor])
+               for b1, o, h in dj_args]
+        timed_calls(djp, 16)
+        lat["double_join"]["prepared"] = timed_calls(djp, min(args.latency_calls, 512))
+        del dj, djp, dj_args
 
     if args.calibration_copy:
         calibration_copy(torch, dev)

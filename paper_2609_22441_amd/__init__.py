@@ -8,7 +8,7 @@ only marshals arguments (device pointers, sizes, the stream) and raises ``CCErro
 non-OK status. There is no fallback: if the library is not built, every call raises.
 """
 from .binding import (  # noqa: F401
-    CCError, PreparedJoin, Tuning, cc_join, cc_join_batched, cc_join_batched_padded, cc_last_device_error,
+    CCError, PreparedJoin, PreparedJoinBatched, Tuning, cc_join, cc_join_batched, cc_join_batched_padded, cc_last_device_error,
     cc_sort_affinity, cc_sort_workspace_bytes, cc_status_string,
     cc_store_create, cc_store_destroy, cc_store_info, cc_store_invalid_count,
     cc_store_reset_invalid_count, cc_validate_keys, lib, LIB_PATH, EXPORTS,

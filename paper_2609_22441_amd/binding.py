@@ -411,6 +411,44 @@ class PreparedJoin:
             raise CCError(st, "cc_join")
 
 
+class PreparedJoinBatched:
+    """cc_join_batched with its arguments checked once (see PreparedJoin).
+
+    Buffers are sized for the largest batch. A call passes the batch's viewer count and totals:
+    ``prepared(n_viewers, total_cand, total_keys)`` joins the CSR batch described by
+    cand_offsets[:n_viewers + 1] and key_offsets[:n_viewers + 1] (device contents written by the
+    caller, as for cc_join_batched) over the leading elements of the other buffers. Counts
+    default to the full buffers and must not exceed them.
+    """
+
+    def __init__(self, store: int, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats,
+                 out, hit_mask, default_row=None, extra_keys: Optional[Sequence] = None):
+        B, L, tc, tk, pco, pc, pko, pk, pf, pd, ex, ew = _batched_args(
+            store, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats, default_row,
+            extra_keys, None, None)
+        po, stride = _out_rows(out, "out", tc, _doc_row_bytes(store) + L * ew)
+        ph = _arr(hit_mask, "hit_mask", _i8(), tc * L)
+        self._cap = (B, tc, tk)
+        self._keep = (cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats, out, hit_mask,
+                      default_row, extra_keys, ex)
+        self._a = (store, pco, pc, pko, pk, pf, ew, pd, L, ex, po, stride, ph)
+        self._fn = lib().cc_join_batched
+
+    def __call__(self, n_viewers: Optional[int] = None, total_cand: Optional[int] = None,
+                 total_keys: Optional[int] = None, stream=None) -> None:
+        B, tc, tk = self._cap
+        b = B if n_viewers is None else n_viewers
+        n = tc if total_cand is None else total_cand
+        k = tk if total_keys is None else total_keys
+        if not (0 <= b <= B and 0 <= n <= tc and 0 <= k <= tk):
+            _fail("counts", f"must lie in [0, {B}], [0, {tc}] and [0, {tk}] (got {b}, {n}, {k})")
+        store, pco, pc, pko, pk, pf, ew, pd, L, ex, po, stride, ph = self._a
+        st = self._fn(store, b, pco, pc, n, pko, pk, k, pf, ew, pd, L, ex, po, stride, ph,
+                      _stream(stream))
+        if st != CC_OK:
+            raise CCError(st, "cc_join_batched")
+
+
 def _batched_args(store, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats,
                   default_row, extra_keys, total_cand, total_keys):
     """Checked inputs of the batched joins: (B, L, pointers..., extra array, edge width)."""

@@ -260,3 +260,28 @@ def test_prepared_join_counts_must_fit_the_buffers(stub, n, k):
     with pytest.raises(ValueError, match="counts"):
         p(n, k, stream=0)
     assert stub.calls == []
+
+
+def test_prepared_batched_join_passes_the_same_arguments_and_counts(stub):
+    a = batched_args(lookups=2)
+    B.cc_join_batched(1, stream=0, **a)
+    p = B.PreparedJoinBatched(1, **a)
+    p(stream=0)
+    p(2, 7, 5, stream=0)
+    (_, full), (_, prep), (_, part) = stub.calls
+    same = lambda x: list(x) if hasattr(x, "_length_") else x   # ctypes arrays by contents
+    assert [same(x) for x in prep] == [same(x) for x in full]
+    assert part[1] == 2 and part[4] == 7 and part[7] == 5     # viewers, candidates, keys
+    with pytest.raises(ValueError, match="counts"):
+        p(4, 7, 5, stream=0)                                    # more viewers than the offsets
+    with pytest.raises(ValueError, match="counts"):
+        p(2, 13, 5, stream=0)
+    assert len(stub.calls) == 3
+
+
+def test_prepared_batched_join_checks_its_buffers_once(stub):
+    a = batched_args(lookups=2)
+    a["extra_keys"] = [g(11)]
+    with pytest.raises(ValueError, match="elements"):
+        B.PreparedJoinBatched(1, **a)
+    assert stub.calls == []

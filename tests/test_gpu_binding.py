@@ -78,3 +78,39 @@ def test_prepared_join_equals_cc_join():
                 assert_same((out.cpu().numpy(), hit.cpu().numpy()), want, "prepared join")
     finally:
         P.cc_store_destroy(store)
+
+
+def test_prepared_batched_join_equals_cc_join_batched():
+    """PreparedJoinBatched on its first b viewers gives the bytes cc_join_batched gives for the
+    same CSR prefix, two lookups, b from all viewers down to none."""
+    note("binding: prepared batched join")
+    tc = W.tiny_case(93, n_lookups=2, max_n=400, max_k=200, max_viewers=5)
+    b = tc.batch
+    wd, we = row_bytes(tc.doc_rows), row_bytes(b.edge_rows)
+    store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+    try:
+        d = b.to(DEV)
+        n_all = d.cand_idx.numel()
+        out = torch.full((n_all, wd + 2 * we), 0x5A, dtype=torch.uint8, device=DEV)
+        hit = torch.full((n_all, 2), -7, dtype=torch.int8, device=DEV)
+        prepared = P.PreparedJoinBatched(store, d.cand_offsets, d.cand_idx, d.key_offsets, d.keys,
+                                         d.edge_rows, out, hit, extra_keys=[d.actor])
+        co, ko = b.cand_offsets.tolist(), b.key_offsets.tolist()
+        for nv in range(len(co) - 1, -1, -1):
+            n, k = co[nv], ko[nv]
+            out.fill_(0x5A)
+            hit.fill_(-7)
+            prepared(nv, n, k)
+            ref_out = torch.full((n, wd + 2 * we), 0x5A, dtype=torch.uint8, device=DEV)
+            ref_hit = torch.full((n, 2), -7, dtype=torch.int8, device=DEV)
+            P.cc_join_batched(store, d.cand_offsets[:nv + 1], d.cand_idx[:n],
+                              d.key_offsets[:nv + 1], d.keys[:k], d.edge_rows[:k], ref_out,
+                              ref_hit, extra_keys=[d.actor[:n]])
+            torch.cuda.synchronize()
+            assert torch.equal(out[:n], ref_out) and torch.equal(hit[:n], ref_hit), nv
+            assert bool((hit[n:] == -7).all()), nv
+            if nv == len(co) - 1:
+                want = oracle_join(tc.author_id, tc.doc_rows, b, 2)
+                assert_same((out.cpu().numpy(), hit.cpu().numpy()), want, "prepared batched")
+    finally:
+        P.cc_store_destroy(store)

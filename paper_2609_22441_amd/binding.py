@@ -382,7 +382,9 @@ class PreparedJoin:
     buffers' leading elements and passes only the counts: ``prepared(n_cand, n_keys)`` joins
     cand_idx[:n_cand] against edge_keys[:n_keys] / edge_feats[:n_keys] into out[:n_cand] and
     hit_mask[:n_cand]. Counts default to the full buffers and must not exceed them. Same C call
-    and semantics as cc_join; only the per-call Python work is smaller.
+    and semantics as cc_join; only the per-call Python work is smaller. The object keeps its
+    tensors referenced and their device pointers fixed: resizing a buffer in place
+    (``Tensor.resize_``, ``set_``) would leave it with a stale pointer, so build a new one instead.
     """
 
     def __init__(self, store: int, cand_idx, edge_keys, edge_feats, out, hit_mask,

@@ -150,3 +150,20 @@ def test_thousands_of_small_viewers():
     keys = torch.randint(-50, 50, (n,), generator=g)
     rows = torch.randint(0, 256, (n, 16), generator=g, dtype=torch.int64).to(torch.uint8)
     _check(ko, keys, rows, "5000 viewers")
+
+
+@pytest.mark.parametrize("max_keys", [0, 20_000])
+def test_many_viewers_with_merge_rounds(max_keys):
+    """1,300 viewers (more than one round of the workgroup-wide viewer search) where every 50th
+    has 5,000 to 20,000 records, so the merge rounds also look up viewers past the first 512;
+    the rest hold 0 to 60 records. Packed elements; without and with the max_keys hint."""
+    note(f"sort: 1,300 viewers with merge rounds, max_keys {max_keys}")
+    g = W.gen("cpu", 23, 5)
+    sizes = torch.randint(0, 61, (1300,), generator=g)
+    sizes[::50] = torch.randint(5_000, 20_001, (26,), generator=g)
+    sizes[3::97] = 0
+    ko = torch.cat([torch.zeros(1, dtype=torch.int64), torch.cumsum(sizes, 0)])
+    n = int(ko[-1])
+    keys = torch.randint(0, 3_000, (n,), generator=g)            # many equal keys: stability
+    rows = torch.randint(0, 256, (n, 32), generator=g, dtype=torch.int64).to(torch.uint8)
+    _check(ko, keys, rows, f"1300 viewers, max_keys {max_keys}", max_keys=max_keys)

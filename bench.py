@@ -8,7 +8,9 @@ only the store's hot columns can stay in the caches between steps.
 
 Reported:
   value           joined candidates/s over the K timed steps (inputs resident in HBM)
-  p50/p99         per-request latency of single cc_join calls (hip events on the stream)
+  p50/p99         per-request latency of single cc_join calls (hip events on the stream);
+                  latency.prepared: the same requests through PreparedJoin; latency.double_join:
+                  two-lookup requests (plain and PreparedJoinBatched)
   roofline        algorithmic bytes per launch / mean launch time, against 8 TB/s
   cold            the same step with the caches flushed (1 GiB read) before each launch
   cpu_baseline    the CPU oracle on the host cores, on a bounded sample of the same requests

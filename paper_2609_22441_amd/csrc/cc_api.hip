@@ -190,10 +190,9 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
     a.fence_stride = stride;
     a.fence_budget = budget;
     a.one_wave = one_wave;
-    // Weighted ranges for CSR batches that a workgroup can scan in one pass (the padded layout
-    // keeps equal ranges: its candidates past n_max are skipped, which the weights ignore).
-    a.balanced = cand_offsets != nullptr && n_max == 0 && n_viewers > 1 &&
-                 n_viewers <= ccj::kBalanceViewers;
+    // Weighted ranges for CSR batches of 2 to kBalanceViewers viewers (each workgroup scans
+    // every viewer's offsets once).
+    a.balanced = cand_offsets != nullptr && n_viewers > 1 && n_viewers <= ccj::kBalanceViewers;
     // The LDS table never needs more entries than the largest viewer has keys.
     a.lds_keys = (int32_t)(total_keys < lds_cap ? (total_keys > 0 ? total_keys : 1) : lds_cap);
 

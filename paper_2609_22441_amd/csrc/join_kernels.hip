@@ -199,7 +199,8 @@ __device__ __forceinline__ int64_t wave_scan_incl(int64_t x) {
 }
 
 // Weighted ranges for a CSR batch of at most kBalanceViewers viewers. Candidate i of viewer v
-// weighs w_v = cand_cost(K_v); with prefix weights P, logical range r of n covers the candidates
+// weighs w_v = cand_cost(K_v) (in the padded layout only its first n_max candidates, the ones
+// joined, count); with prefix weights P, logical range r of n covers the candidates
 // whose weight starts in [T_r, T_{r+1}), T_r = floor(r * W / n), W the total. Every workgroup
 // computes the same prefix, so the ranges tile the candidates. Ranges of equal weight take
 // fewer candidates of long lists, which would otherwise finish last. Returns the range and the
@@ -224,7 +225,10 @@ __device__ __forceinline__ void balanced_range(const JoinArgs &a, int64_t r, int
             const int64_t kb = clamp64(a.key_offsets[v], a.total_keys);
             const int64_t ke = max(kb, clamp64(a.key_offsets[v + 1], a.total_keys));
             c[i] = cand_cost(ke - kb, a.lds_keys);
-            w[i] = max<int64_t>(ve - vb[i], 0) * c[i];
+            int64_t nv = max<int64_t>(ve - vb[i], 0);
+            if (a.n_max > 0)                      // the padded layout joins the first n_max
+                nv = min(nv, a.n_max);
+            w[i] = nv * c[i];
         }
         mine += w[i];
     }

@@ -51,6 +51,9 @@ def parse():
                     help="also time each of the five workload shapes (adds a 'configs' field)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (known bytes) for counter scaling")
+    ap.add_argument("--only-sorts", default="",
+                    help="time only the record sorts of these workload shapes (2, 3 and/or 5): "
+                         "for counter passes on the sort")
     ap.add_argument("--only-workloads", default="",
                     help="time only the joins of these workload shapes (e.g. 3,5), without the "
                          "benchmark step, the sort or the id map: for per-workload counter passes")
@@ -100,9 +103,10 @@ def calibration_copy(torch, dev):
     del src, dst
 
 
-def all_configs(torch, P, W, dev, seed, only=(1, 2, 3, 4, 5), joins_only=False):
+def all_configs(torch, P, W, dev, seed, only=(1, 2, 3, 4, 5), joins_only=False, sorts_only=False):
     """Per-launch time and algorithmic bandwidth of each workload shape at full size (only the
-    join launches of the listed shapes when joins_only)."""
+    join launches of the listed shapes when joins_only; only their record sorts when
+    sorts_only)."""
     res = {}
     st10 = None
     for i in (1, 2, 3, 4, 5):
@@ -141,8 +145,9 @@ def all_configs(torch, P, W, dev, seed, only=(1, 2, 3, 4, 5), joins_only=False):
             fn = lambda: P.cc_join_batched(store, b.cand_offsets, b.cand_idx, b.key_offsets,
                                            b.keys, b.edge_rows, out, hit, extra_keys=ex)
             entry = "cc_join_batched"
-        med, mean = time_launches(torch, fn, 100 if n < 500_000 else 30)
-        if i == 2 and not joins_only:
+        if not sorts_only:
+            med, mean = time_launches(torch, fn, 100 if n < 500_000 else 30)
+        if i == 2 and not joins_only and not sorts_only:
             # The paper's serving batch (b = 8 requests per launch, §6.3.1) of this shape.
             b8 = W.pack(W.make_requests(st10, r, seed, n_viewers=8))
             n8 = b8.cand_idx.numel()
@@ -158,7 +163,7 @@ def all_configs(torch, P, W, dev, seed, only=(1, 2, 3, 4, 5), joins_only=False):
                                "hbm_gbps": alg8 / (m8 / 1e3) / 1e9,
                                "hbm_frac_of_peak": alg8 / (m8 / 1e3) / 1e9 / PEAK_GBPS}
             del b8, out8, hit8
-        if i == 3 and not joins_only:
+        if i == 3 and not joins_only and not sorts_only:
             # The same requests written into the padded [B, n_max] layout of the paper's batching
             # (pad rows and the valid mask are extra output bytes).
             n_max = r.n_cand
@@ -200,14 +205,15 @@ def all_configs(torch, P, W, dev, seed, only=(1, 2, 3, 4, 5), joins_only=False):
                                 "hbm_frac_of_peak": alg_s / (sm / 1e3) / 1e9 / PEAK_GBPS}
             del k_in, r_in, k_out, r_out, ws
         P.cc_store_destroy(store)
-        res[str(i)] = {"entry": entry, "viewers": r.n_viewers, "candidates": n,
-                       "keys": b.keys.numel(), "lookups": L, "ms_median": med, "ms_mean": mean,
-                       "candidates_per_s": n / (med / 1e3), "algorithmic_bytes": alg,
-                       "hbm_gbps": alg / (med / 1e3) / 1e9,
-                       "hbm_frac_of_peak": alg / (med / 1e3) / 1e9 / PEAK_GBPS}
+        if not sorts_only:
+            res[str(i)] = {"entry": entry, "viewers": r.n_viewers, "candidates": n,
+                           "keys": b.keys.numel(), "lookups": L, "ms_median": med,
+                           "ms_mean": mean, "candidates_per_s": n / (med / 1e3),
+                           "algorithmic_bytes": alg, "hbm_gbps": alg / (med / 1e3) / 1e9,
+                           "hbm_frac_of_peak": alg / (med / 1e3) / 1e9 / PEAK_GBPS}
         del out, hit, b, reqs
         torch.cuda.empty_cache()
-    if not joins_only:
+    if not joins_only and not sorts_only:
         res.update(index_workloads(torch, P, W, dev, seed))
     return res
 
@@ -397,13 +403,14 @@ def main():
         __graft_entry__.build()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    if args.only_workloads:
-        ids = tuple(int(x) for x in args.only_workloads.split(","))
-        res = all_configs(torch, P, W, dev, args.seed, only=ids, joins_only=True)
+    if args.only_workloads or args.only_sorts:
+        ids = tuple(int(x) for x in (args.only_workloads or args.only_sorts).split(","))
+        res = all_configs(torch, P, W, dev, args.seed, only=ids,
+                          joins_only=bool(args.only_workloads), sorts_only=bool(args.only_sorts))
         if args.calibration_copy:
             calibration_copy(torch, dev)
-        print(json.dumps({"metric": METRIC, "only_workloads": list(ids), "configs": res}),
-              flush=True)
+        key = "only_workloads" if args.only_workloads else "only_sorts"
+        print(json.dumps({"metric": METRIC, key: list(ids), "configs": res}), flush=True)
         return
     s, r = W.SHAPES[2]
     st = W.make_store(s, args.seed, device=dev)

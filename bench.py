@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--only-sorts", default="",
                     help="time only the record sorts of these workload shapes (2, 3 and/or 5): "
                          "for counter passes on the sort")
+    ap.add_argument("--only-index", action="store_true",
+                    help="run only the id-map part (index build, resolve, ingestion batches): for "
+                         "counter passes on those kernels")
     ap.add_argument("--only-workloads", default="",
                     help="time only the joins of these workload shapes (e.g. 3,5), without the "
                          "benchmark step, the sort or the id map: for per-workload counter passes")
@@ -403,6 +406,12 @@ def main():
         __graft_entry__.build()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.only_index:
+        res = index_workloads(torch, P, W, dev, args.seed)
+        if args.calibration_copy:
+            calibration_copy(torch, dev)
+        print(json.dumps({"metric": METRIC, "only_index": True, "configs": res}), flush=True)
+        return
     if args.only_workloads or args.only_sorts:
         ids = tuple(int(x) for x in (args.only_workloads or args.only_sorts).split(","))
         res = all_configs(torch, P, W, dev, args.seed, only=ids,

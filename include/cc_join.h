@@ -52,7 +52,9 @@ typedef enum cc_status {
     CC_ERR_DEVICE = 3,             /* a HIP call failed; see cc_last_device_error()         */
     CC_ERR_UNSORTED_KEYS = 4,      /* only from cc_validate_keys                            */
     CC_ERR_NOT_SUPPORTED = 5,      /* no usable gfx950 device, or a store without an id map */
-    CC_ERR_STORE_FULL = 6          /* an ingestion batch does not fit; the store is unchanged */
+    CC_ERR_STORE_FULL = 6,         /* an ingestion batch does not fit; the store is unchanged */
+    CC_ERR_TOO_LARGE = 7           /* a size exceeds the fixed scratch of an allocation-free
+                                      entry point; nothing enqueued                          */
 } cc_status;
 
 /* Where cc_store_create reads its source arrays from. */
@@ -364,6 +366,29 @@ CC_API cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets,
                                   int64_t total_keys, int64_t max_keys, int64_t *keys_out,
                                   void *rows_out, void *workspace, int64_t workspace_bytes,
                                   hipStream_t stream);
+
+/*
+ * cc_sort_affinity_noalloc -- cc_sort_affinity for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, hosts that forbid allocation): the same
+ * sort, whose workspace is a fixed device array that the library holds on each device it runs
+ * on until the process ends, instead of a caller-provided buffer. The call allocates nothing
+ * and never synchronises; its first call on a device resolves that device's array once.
+ *
+ * Limits: total_keys <= CC_SORT_NOALLOC_MAX_RECORDS and n_viewers <=
+ * CC_SORT_NOALLOC_MAX_VIEWERS; larger calls return CC_ERR_TOO_LARGE before anything is
+ * enqueued. The array is shared by every call on one device and keeps the last call's
+ * contents (nothing in it needs clearing between calls): calls that overlap on one device,
+ * from any threads or streams, race and must be serialised by the caller.
+ * Other arguments, the result and the errors are those of cc_sort_affinity, on the current
+ * HIP device.
+ */
+#define CC_SORT_NOALLOC_MAX_RECORDS (1 << 20)
+#define CC_SORT_NOALLOC_MAX_VIEWERS (1 << 16)
+CC_API cc_status cc_sort_affinity_noalloc(int32_t n_viewers, const int64_t *key_offsets,
+                                          const int64_t *keys_in, const void *rows_in,
+                                          int32_t row_bytes, int64_t total_keys,
+                                          int64_t max_keys, int64_t *keys_out, void *rows_out,
+                                          hipStream_t stream);
 
 /*
  * cc_validate_keys -- debug helper: check that each viewer's keys are strictly increasing

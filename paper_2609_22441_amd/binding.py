@@ -19,6 +19,7 @@ EXPORTS = (
     "cc_store_create", "cc_store_destroy", "cc_store_info", "cc_store_invalid_count",
     "cc_store_reset_invalid_count", "cc_join", "cc_join_batched", "cc_join_batched_tuned",
     "cc_join_batched_padded", "cc_sort_workspace_bytes", "cc_sort_affinity",
+    "cc_sort_affinity_noalloc",
     "cc_store_create_indexed", "cc_upsert_workspace_bytes", "cc_store_upsert", "cc_store_read",
     "cc_store_layout",
     "cc_resolve_ids",
@@ -26,7 +27,8 @@ EXPORTS = (
 )
 
 CC_OK, CC_ERR_INVALID_ARGUMENT, CC_ERR_OUT_OF_MEMORY, CC_ERR_DEVICE = 0, 1, 2, 3
-CC_ERR_UNSORTED_KEYS, CC_ERR_NOT_SUPPORTED, CC_ERR_STORE_FULL = 4, 5, 6
+CC_ERR_UNSORTED_KEYS, CC_ERR_NOT_SUPPORTED, CC_ERR_STORE_FULL, CC_ERR_TOO_LARGE = 4, 5, 6, 7
+SORT_NOALLOC_MAX_RECORDS, SORT_NOALLOC_MAX_VIEWERS = 1 << 20, 1 << 16
 CC_SRC_HOST, CC_SRC_DEVICE = 1, 2
 
 
@@ -72,6 +74,7 @@ def lib():
             "cc_join_batched_padded": [vp, i32, vp, vp, i64, vp, vp, i64, vp, i32, vp, i32,
                                        ctypes.POINTER(vp), i64, vp, i64, vp, vp, vp],
             "cc_sort_affinity": [i32, vp, vp, vp, i32, i64, i64, vp, vp, vp, i64, vp],
+            "cc_sort_affinity_noalloc": [i32, vp, vp, vp, i32, i64, i64, vp, vp, vp],
             "cc_store_create_indexed": [ctypes.POINTER(vp), i64, i32, vp],
             "cc_store_upsert": [vp, i64, vp, vp, vp, vp, i64, P64, P64, vp],
             "cc_resolve_ids": [vp, vp, i64, vp, vp],
@@ -526,6 +529,23 @@ def cc_sort_affinity(key_offsets, keys_in, rows_in, keys_out, rows_out, workspac
     ws_bytes = workspace.numel() * workspace.element_size()
     _check(lib().cc_sort_affinity(B, pko, pki, pri, rb, tk, max_keys, pk, pr, pw, ws_bytes,
                                   _stream(stream)), "cc_sort_affinity")
+
+
+def cc_sort_affinity_noalloc(key_offsets, keys_in, rows_in, keys_out, rows_out,
+                             max_keys: int = 0, total_keys: Optional[int] = None,
+                             stream=None) -> None:
+    """cc_sort_affinity with the library's fixed per-device scratch instead of a workspace (for
+    callers that cannot allocate; calls on one device must not overlap)."""
+    B = key_offsets.numel() - 1
+    tk = keys_in.numel() if total_keys is None else int(total_keys)
+    rb = _row_bytes(rows_in)
+    pko = _arr(key_offsets, "key_offsets", _i64(), 1)
+    pki = _arr(keys_in, "keys_in", _i64(), tk)
+    pri = _rows(rows_in, "rows_in", tk)
+    pk = _arr(keys_out, "keys_out", _i64(), tk)
+    pr = _rows(rows_out, "rows_out", tk, rb)
+    _check(lib().cc_sort_affinity_noalloc(B, pko, pki, pri, rb, tk, max_keys, pk, pr,
+                                          _stream(stream)), "cc_sort_affinity_noalloc")
 
 
 def cc_validate_keys(key_offsets, edge_keys, total_keys: Optional[int] = None, stream=None):

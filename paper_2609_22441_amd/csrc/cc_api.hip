@@ -646,6 +646,41 @@ cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets, const 
     return e == hipSuccess ? CC_OK : device_error(e);
 }
 
+cc_status cc_sort_affinity_noalloc(int32_t n_viewers, const int64_t *key_offsets,
+                                   const int64_t *keys_in, const void *rows_in, int32_t row_bytes,
+                                   int64_t total_keys, int64_t max_keys, int64_t *keys_out,
+                                   void *rows_out, hipStream_t stream) {
+    if (n_viewers < 0 || total_keys < 0 || max_keys < 0)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (row_bytes <= 0 || (row_bytes & 15) || row_bytes > ccj::kMaxRowBytes)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_viewers > 0 && !key_offsets)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (total_keys > ccj::kSortScratchRecords || n_viewers > ccj::kSortScratchViewers)
+        return CC_ERR_TOO_LARGE;
+    if (total_keys == 0 || n_viewers == 0)
+        return CC_OK;
+    if (!keys_in || !rows_in || !keys_out || !rows_out)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (!aligned(key_offsets, 8) || !aligned(keys_in, 8) || !aligned(keys_out, 8) ||
+        !aligned(rows_in, 16) || !aligned(rows_out, 16))
+        return CC_ERR_INVALID_ARGUMENT;
+    const int64_t kbytes = total_keys * 8, rbytes = total_keys * (int64_t)row_bytes;
+    if (overlaps(keys_out, kbytes, keys_in, kbytes) || overlaps(keys_out, kbytes, rows_in, rbytes) ||
+        overlaps(rows_out, rbytes, keys_in, kbytes) || overlaps(rows_out, rbytes, rows_in, rbytes) ||
+        overlaps(keys_out, kbytes, rows_out, rbytes))
+        return CC_ERR_INVALID_ARGUMENT;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    void *scratch = nullptr;
+    if (e == hipSuccess)
+        e = ccj::sort_scratch(dev, &scratch);
+    if (e == hipSuccess)
+        e = ccj::launch_sort(n_viewers, key_offsets, keys_in, rows_in, row_bytes, total_keys,
+                             max_keys, keys_out, rows_out, scratch, stream);
+    return e == hipSuccess ? CC_OK : device_error(e);
+}
+
 cc_status cc_validate_keys(const int64_t *key_offsets, const int64_t *edge_keys,
                            int32_t n_viewers, int64_t total_keys, int64_t *first_bad_viewer,
                            hipStream_t stream) {
@@ -693,6 +728,7 @@ const char *cc_status_string(int status) {
     case CC_ERR_UNSORTED_KEYS: return "CC_ERR_UNSORTED_KEYS";
     case CC_ERR_NOT_SUPPORTED: return "CC_ERR_NOT_SUPPORTED";
     case CC_ERR_STORE_FULL: return "CC_ERR_STORE_FULL";
+    case CC_ERR_TOO_LARGE: return "CC_ERR_TOO_LARGE";
     }
     return "CC_UNKNOWN_STATUS";
 }

@@ -67,6 +67,16 @@ hipError_t launch_pad_fill(const JoinArgs &args, int n_lookups, int8_t *valid_ma
 // Workspace bytes of the affinity-record sort for `total` records in `n_viewers` viewers.
 int64_t sort_workspace_bytes(int64_t total, int32_t n_viewers);
 
+// Largest call of the allocation-free sort: its workspace is a fixed device array of
+// sort_workspace_bytes(kSortScratchRecords, kSortScratchViewers) bytes (about 32.5 MiB).
+constexpr int64_t kSortScratchRecords = (int64_t)1 << 20;
+constexpr int32_t kSortScratchViewers = 1 << 16;
+constexpr int kMaxScratchDevices = 64;
+
+// Device address of the allocation-free sort's fixed scratch on `device`, which must be the
+// current device. Resolved on the first call per device, then cached.
+hipError_t sort_scratch(int device, void **ptr);
+
 // Enqueue the per-viewer stable sort of affinity records (keys + rows) into keys_out/rows_out.
 // max_keys > 0 bounds the records of any one viewer (fewer merge rounds); 0 = unknown.
 hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,

@@ -30,6 +30,8 @@
 // conflicts come from the data-dependent merge-path probes, which no static layout removes.
 #include <stdint.h>
 
+#include <mutex>
+
 #include <hip/hip_runtime.h>
 
 #include "join_internal.h"
@@ -545,9 +547,22 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const void *src, void *
         merge_body(Wide{}, lds, s_split, src, dst, off, B, tile_off, r, o);
 }
 
-int64_t round_up(int64_t x) { return (x + 255) & ~int64_t(255); }
+constexpr int64_t round_up(int64_t x) { return (x + 255) & ~int64_t(255); }
 
 constexpr int kRangeSlots = 1024;   // range_kernel workgroups at most
+
+// Workspace layout: two ping-pong element arrays, the per-viewer tile offsets, the key range
+// (256 bytes) and the range kernel's per-workgroup slots.
+constexpr int64_t workspace_bytes(int64_t total, int64_t n_viewers) {
+    return 2 * round_up(total * (int64_t)sizeof(Wide::T)) + round_up((n_viewers + 1) * 8) + 256 +
+           round_up(2 * kRangeSlots * 8);
+}
+
+// Fixed device scratch of the allocation-free sort (cc_sort_affinity_noalloc): the workspace of
+// the largest call it accepts. One copy per device, resolved once per device below; in host
+// code `scratch` names a host-side stand-in, so only the resolved address is ever passed on.
+constexpr int64_t kScratchBytes = workspace_bytes(kSortScratchRecords, kSortScratchViewers);
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 
 }  // namespace
 
@@ -556,8 +571,25 @@ int64_t sort_workspace_bytes(int64_t total, int32_t n_viewers) {
     // below far from overflow.
     if (total <= 0 || n_viewers <= 0 || total >= ((int64_t)1 << 32))
         return 0;
-    return 2 * round_up(total * (int64_t)sizeof(Wide::T)) + round_up(((int64_t)n_viewers + 1) * 8) +
-           256 + round_up(2 * kRangeSlots * 8);
+    return workspace_bytes(total, n_viewers);
+}
+
+hipError_t sort_scratch(int device, void **ptr) {
+    static std::mutex mu;
+    static void *addr[kMaxScratchDevices] = {};
+    if (device < 0 || device >= kMaxScratchDevices)
+        return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[device]) {
+        // The caller has made `device` current: the symbol resolves to that device's copy.
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess)
+            return e;
+        addr[device] = p;
+    }
+    *ptr = addr[device];
+    return hipSuccess;
 }
 
 hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,

@@ -96,6 +96,36 @@ def test_sort_workspace_size():
     assert lib.cc_sort_workspace_bytes(1 << 32, 1) == 0             # more than the sort takes
 
 
+def test_sort_noalloc_rejects_bad_arguments_and_sizes_past_its_scratch():
+    lib = B.lib()
+    base = dict(nv=1, off=0x1000, kin=0x2000, rin=0x10000, rb=32, tk=1000, mk=0, kout=0x30000,
+                rout=0x100000)
+
+    def call(**kw):
+        a = dict(base, **kw)
+        return lib.cc_sort_affinity_noalloc(a["nv"], a["off"], a["kin"], a["rin"], a["rb"],
+                                            a["tk"], a["mk"], a["kout"], a["rout"], None)
+
+    assert B.SORT_NOALLOC_MAX_RECORDS == 1 << 20 and B.SORT_NOALLOC_MAX_VIEWERS == 1 << 16
+    big = dict(kin=None, rin=None, kout=None, rout=None)
+    assert call(tk=B.SORT_NOALLOC_MAX_RECORDS + 1, **big) == B.CC_ERR_TOO_LARGE
+    assert call(nv=B.SORT_NOALLOC_MAX_VIEWERS + 1, **big) == B.CC_ERR_TOO_LARGE
+    assert call(tk=1 << 32, **big) == B.CC_ERR_TOO_LARGE
+    assert P.cc_status_string(B.CC_ERR_TOO_LARGE) == "CC_ERR_TOO_LARGE"
+    assert call(rb=24) == 1                      # row width not a multiple of 16
+    assert call(rb=(1 << 20) + 16) == 1          # row wider than 1 MiB
+    assert call(tk=-1) == 1
+    assert call(nv=-1) == 1
+    assert call(mk=-1) == 1
+    assert call(off=None) == 1
+    assert call(kin=None) == 1
+    assert call(rout=0x100008) == 1              # misaligned rows
+    assert call(kout=0x2004) == 1                # misaligned keys
+    assert call(kout=0x2000) == 1                # output keys alias the input keys
+    assert call(rout=0x10000 + 64) == 1          # output rows overlap the input rows
+    assert call(tk=0, **big) == 0                # no work: nothing touches a device
+
+
 def test_sort_rejects_bad_arguments():
     lib = B.lib()
     ws = lib.cc_sort_workspace_bytes(1000, 1)

@@ -51,3 +51,37 @@ def test_more_than_one_gpu_is_refused():
     assert p.returncode == 2
     assert "one GPU" in p.stderr
     assert p.stdout == ""
+
+
+def test_cpu_threads_follow_the_job_share(monkeypatch):
+    import os
+    avail = len(os.sched_getaffinity(0))
+    monkeypatch.delenv("OMP_NUM_THREADS", raising=False)
+    assert bench.cpu_threads() == (avail, avail, "affinity mask")
+    if avail > 1:
+        monkeypatch.setenv("OMP_NUM_THREADS", "1")
+        assert bench.cpu_threads() == (1, avail, "OMP_NUM_THREADS")
+    monkeypatch.setenv("OMP_NUM_THREADS", str(avail + 5))
+    assert bench.cpu_threads()[0] == avail
+
+
+def test_cpu_baseline_reports_both_thread_counts(monkeypatch):
+    monkeypatch.setenv("OMP_NUM_THREADS", "2")
+    calls = []
+
+    def task(n):
+        def run():
+            calls.append(n)
+            return n
+        return run
+    tasks = {"1": [task(10)], "2": [task(50), task(60)], "4": [task(7)], "4x64": [task(7)]}
+    res = bench.cpu_baseline(tasks, 0.01)
+    threads = res["threads"]
+    assert res["cores"] == threads and threads <= 2
+    assert set(res["per_workload"]) == {"1", "2", "4"}
+    for leg in res["per_workload"].values():
+        assert set(leg) == {"threads_1", f"threads_{threads}"}
+        assert all(x["candidates_per_s"] > 0 and x["requests"] >= 1 for x in leg.values())
+    assert res["value"] == res["per_workload"]["2"][f"threads_{threads}"]["candidates_per_s"]
+    assert res["value_1_thread"] == res["per_workload"]["2"]["threads_1"]["candidates_per_s"]
+    assert res["host_cpus_in_affinity"] >= threads

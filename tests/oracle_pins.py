@@ -7,8 +7,10 @@ are independent of the oracle's code:
 * ``pin_golden``      -- the hand-worked Eq. 1 example in ``tests/golden/eq1_worked.json``;
 * ``pin_scan``        -- a pure-Python scan of Eq. 1 on tiny random inputs (the naive O(N K)
                          scan of §3.1), including duplicates, int64 extremes, invalid positions;
-* ``pin_alg1``        -- NumPy's stable ``argsort`` + ``searchsorted(side="left")`` route through
-                         the four steps of Alg. 1, given the keys in shuffled order;
+* ``pin_alg1``        -- a first-record map built from NumPy's stable ``argsort`` and
+                         ``np.unique`` (each id gets the row of its first record once records
+                         are stably sorted, the record Eq. 1 picks after Alg. 1 Step 1), given
+                         the keys in shuffled order;
 * ``pin_invariants``  -- properties of the result on generated workloads: hit iff the key is
                          in the viewer's key set, miss rows equal the default row, valid doc
                          segments equal the store row, equivariance under a permutation of the
@@ -140,22 +142,23 @@ def pin_scan(lib, seeds=range(60)):
 
 
 # --------------------------------------------------------------------------------------------
-def alg1_numpy(d, a, F):
-    """Alg. 1 for one viewer with NumPy library routines (valid for K >= 1).
+def first_record_rows(query_ids, record_ids, record_rows):
+    """Eq. 1 for one viewer whose affinity records arrive in any order, from library routines.
 
-    Step 1 sorts the affinity records (stable, so equal keys keep their input order),
-    Step 2 is searchsorted (leftmost insertion point), Step 3 clamps and validates,
-    Step 4 fills zeros and gathers the matched rows.
+    A query id receives the row of the first record carrying that id, where "first" is the
+    order a stable sort by id leaves (records with equal ids keep their input order); a query
+    id that no record carries receives the zero row. The map id -> first record comes from a
+    stable argsort and np.unique's first-occurrence indices; membership from np.isin.
+    Returns (rows [n, row_bytes], found [n] bool).
     """
-    K = a.shape[0]
-    idx = np.argsort(a, kind="stable")
-    a_sorted, F_sorted = a[idx], F[idx]
-    pos = np.searchsorted(a_sorted, d, side="left")
-    pos_safe = np.minimum(pos, K - 1)
-    valid = (pos < K) & (a_sorted[pos_safe] == d)
-    O = np.zeros((d.shape[0], F.shape[1]), dtype=F.dtype)
-    O[valid] = F_sorted[pos_safe[valid]]
-    return O, valid
+    by_id = np.argsort(record_ids, kind="stable")
+    distinct, first_in_sorted = np.unique(record_ids[by_id], return_index=True)
+    first_record = dict(zip(distinct.tolist(), by_id[first_in_sorted].tolist()))
+    found = np.isin(query_ids, distinct)
+    rows = np.zeros((query_ids.shape[0], record_rows.shape[1]), dtype=record_rows.dtype)
+    which = [first_record[q] for q in query_ids[found].tolist()]
+    rows[found] = record_rows[np.asarray(which, dtype=np.int64)]
+    return rows, found
 
 
 def pin_alg1(lib, seeds=range(40)):
@@ -178,7 +181,7 @@ def pin_alg1(lib, seeds=range(40)):
         shuffled_keys = np.empty_like(keys)
         shuffled_edge = np.empty_like(edge)
         shuffled_keys[slot], shuffled_edge[slot] = keys, edge
-        O, valid = alg1_numpy(d, shuffled_keys, shuffled_edge)
+        O, valid = first_record_rows(d, shuffled_keys, shuffled_edge)
         out, hit, _ = oracle.join(tc.author_id, tc.doc_rows, b.cand_offsets, b.cand_idx,
                                   b.key_offsets, b.keys, b.edge_rows, lib=lib, fill=FILL)
         wd = tc.doc_rows.shape[1]
@@ -329,13 +332,14 @@ def pin_sort(lib):
             order = sorted(range(int(ko[v + 1] - ko[v])), key=lambda i: int(kn[sl][i]))
             assert ks[sl].tolist() == [int(kn[sl][i]) for i in order], f"sort keys, seed {seed}"
             assert np.array_equal(rs[sl], rn[sl][order]), f"sort rows, seed {seed}"
-        # whole Alg. 1 on one viewer: shuffled records -> sort -> join == NumPy Alg. 1
+        # whole Alg. 1 on one viewer: shuffled records -> sort -> join == the NumPy first-record
+        # map on the shuffled records
         v0 = slice(ko[0], ko[1])
         if ko[1] > ko[0]:
             cand = b.cand_idx[b.cand_offsets[0]:b.cand_offsets[1]].numpy()
             ok = (cand >= 0) & (cand < tc.author_id.numel())
             d = tc.author_id.numpy()[np.where(ok, cand, 0)]
-            O, valid = alg1_numpy(d, kn[v0], rn[v0])
+            O, valid = first_record_rows(d, kn[v0], rn[v0])
             out, hit, _ = oracle.join_single(tc.author_id, tc.doc_rows, cand, ks[v0], rs[v0],
                                              lib=lib, fill=FILL)
             wd = tc.doc_rows.shape[1]

@@ -109,7 +109,10 @@ CC_API cc_status cc_store_layout(const cc_store *store, int32_t *author_id_bytes
                                  int64_t *capacity);
 
 /* Read the number of invalid candidate positions (outside [0, n_docs)) that joins on this
- * store have met since creation or the last reset. Synchronises `stream` (debug/metrics). */
+ * store have met since creation or the last reset. The id -> position resolution of §6.3.1
+ * (Eq. 6) returns -1 for a document id that is not in the index; such positions reach the join
+ * as candidates and are counted here (their output rows are defined in cc_join_batched).
+ * Synchronises `stream` (debug/metrics). Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_DEVICE. */
 CC_API cc_status cc_store_invalid_count(const cc_store *store, int64_t *count, hipStream_t stream);
 
 /* Reset that counter to zero, ordered on `stream` (no synchronisation). A kernel clears it, so
@@ -395,7 +398,9 @@ CC_API cc_status cc_sort_affinity_noalloc(int32_t n_viewers, const int64_t *key_
  * (the precondition under which the join result is unique, §3.1 Alg. 1 Step 1 output).
  * Synchronises `stream`. Returns CC_OK, or CC_ERR_UNSORTED_KEYS with *first_bad_viewer set to
  * the lowest offending viewer (otherwise it is set to -1). Offsets must satisfy the rules of
- * cc_join_batched (they are clamped to total_keys).
+ * cc_join_batched (they are clamped to total_keys). The result flag lives in an 8-byte device
+ * buffer that the library allocates on the first call per device and keeps; calls are
+ * serialised by the library (one at a time per process).
  */
 CC_API cc_status cc_validate_keys(const int64_t *key_offsets, const int64_t *edge_keys,
                            int32_t n_viewers, int64_t total_keys, int64_t *first_bad_viewer,

@@ -3,6 +3,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 
 #include <hip/hip_runtime.h>
@@ -695,10 +696,22 @@ cc_status cc_validate_keys(const int64_t *key_offsets, const int64_t *edge_keys,
         return CC_ERR_INVALID_ARGUMENT;
     if (n_viewers == 0 || total_keys == 0)
         return CC_OK;
-    unsigned long long *d_bad = nullptr;
-    hipError_t e = hipMalloc(&d_bad, sizeof(*d_bad));
+    // One flag buffer per device, allocated on the first call there and kept; the lock
+    // serialises the calls that share it (each call synchronises before it returns).
+    static std::mutex mu;
+    static unsigned long long *flag[ccj::kMaxScratchDevices] = {};
+    std::lock_guard<std::mutex> lock(mu);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess)
         return device_error(e);
+    if (dev < 0 || dev >= ccj::kMaxScratchDevices)
+        return device_error(hipErrorInvalidDevice);
+    if (!flag[dev] && (e = hipMalloc(&flag[dev], sizeof(unsigned long long))) != hipSuccess) {
+        flag[dev] = nullptr;
+        return device_error(e);
+    }
+    unsigned long long *d_bad = flag[dev];
     unsigned long long bad = ~0ull;
     e = hipMemcpyAsync(d_bad, &bad, sizeof(bad), hipMemcpyHostToDevice, stream);
     if (e == hipSuccess)
@@ -707,7 +720,6 @@ cc_status cc_validate_keys(const int64_t *key_offsets, const int64_t *edge_keys,
         e = hipMemcpyAsync(&bad, d_bad, sizeof(bad), hipMemcpyDeviceToHost, stream);
     if (e == hipSuccess)
         e = hipStreamSynchronize(stream);
-    (void)hipFree(d_bad);
     if (e != hipSuccess)
         return device_error(e);
     if (bad != ~0ull) {

@@ -348,3 +348,84 @@ def test_batch_of_one_repeated_id():
         ix.resolve(torch.tensor([1234567, 7654321]), "repeated id")
     finally:
         ix.close()
+
+
+# ---- the map's probe limit: ids chosen to share one home group ----
+
+_M64 = (1 << 64) - 1
+_C1, _C2 = 0xBF58476D1CE4E5B9, 0x94D049BB133111EB     # SplitMix64's output-function multipliers
+
+
+def _mix(z):
+    """SplitMix64's output function (the map's published mixer), on Python ints mod 2^64."""
+    z = ((z ^ (z >> 30)) * _C1) & _M64
+    z = ((z ^ (z >> 27)) * _C2) & _M64
+    return z ^ (z >> 31)
+
+
+def _unxorshift(y, s):
+    x = y
+    for _ in range(64 // s + 1):
+        x = y ^ (x >> s)
+    return x
+
+
+def _unmix(z):
+    """The inverse of _mix: every step of the mixer is a bijection on 64-bit words."""
+    z = _unxorshift(z, 31)
+    z = (z * pow(_C2, -1, 1 << 64)) & _M64
+    z = _unxorshift(z, 27)
+    z = (z * pow(_C1, -1, 1 << 64)) & _M64
+    return _unxorshift(z, 30)
+
+
+def _colliding_ids(n, groups, home):
+    """n distinct int64 ids whose home group (mixer output mod groups) is `home`."""
+    out = []
+    for k in range(1, n + 1):
+        u = _unmix(home + k * groups)
+        assert _mix(u) % groups == home
+        out.append(u - (1 << 64) if u >= 1 << 63 else u)
+    assert I64_MIN not in out and len(set(out)) == n
+    return out
+
+
+def test_probe_limit_refuses_the_batch_and_keeps_the_store():
+    """An id that cannot be placed within the map's 64 probe groups (256 entries) fails its
+    batch with CC_ERR_STORE_FULL and the store stays as it was: positions, rows and the map.
+    The oracle has no probe limit (it accepts such batches), so the refused batches are
+    checked against the oracle state from before them."""
+    cap, rb = 300, 16
+    groups = 256                  # the map of a 300-document store: 2 * 300 entries -> 256 groups
+    ids = _colliding_ids(257, groups, home=17)
+    idx = DeviceIndex(cap, rb)
+    g = torch.Generator().manual_seed(5)
+    rows = lambda n: torch.randint(0, 256, (n, rb), generator=g, dtype=torch.int64).to(torch.uint8)
+    # 256 colliding ids fill the 64 groups their probes may visit: accepted.
+    note("probe limit: 256 colliding ids")
+    assert idx.upsert(ids[:256], list(range(256)), rows(256)) == (256, 0)
+    idx.check_state("after the 256 colliding ids")
+    # One more colliding id (plus an ordinary new id and an update of a stored id): refused.
+    other = 123456789
+    batch = [ids[3], other, ids[256]]
+    ws = torch.empty(P.cc_upsert_workspace_bytes(3), dtype=torch.uint8, device=DEV)
+    note("probe limit: the 257th colliding id")
+    with pytest.raises(P.CCError) as e:
+        P.cc_store_upsert(idx.store, torch.tensor(batch, device=DEV),
+                          torch.tensor([7, 8, 9], device=DEV), rows(3).to(DEV), ws)
+    assert e.value.status == P.CC_ERR_STORE_FULL
+    idx.check_state("after the refused batch")
+    pos = idx.resolve(ids + [other], "after the refused batch")
+    assert pos[:256].tolist() == list(range(256)) and pos[256] == -1 and pos[257] == -1
+    # On an empty store, 257 colliding ids in one batch: refused, nothing stored.
+    fresh = DeviceIndex(cap, rb)
+    with pytest.raises(P.CCError) as e:
+        P.cc_store_upsert(fresh.store, torch.tensor(ids, device=DEV),
+                          torch.arange(257, device=DEV), rows(257).to(DEV),
+                          torch.empty(P.cc_upsert_workspace_bytes(257), dtype=torch.uint8,
+                                      device=DEV))
+    assert e.value.status == P.CC_ERR_STORE_FULL
+    fresh.check_state("after the refused first batch")
+    assert (fresh.resolve(ids, "refused first batch") == -1).all()
+    idx.close()
+    fresh.close()

@@ -350,8 +350,10 @@ CC_API cc_status cc_resolve_ids(const cc_store *store, const int64_t *doc_ids, i
  *   row_bytes      positive multiple of 16, at most 2^20 (1 MiB).
  *   total_keys     host copy of key_offsets[B]; < 2^32.
  *   max_keys       host upper bound on any one viewer's record count (fewer merge passes), or
- *                  0 if unknown. The output of a viewer with more records than max_keys is
- *                  unspecified (every access still stays inside the buffers).
+ *                  0 if unknown. A viewer with more records than a nonzero max_keys is not
+ *                  sorted: its keys and rows are copied to the output in their input order
+ *                  (cc_validate_keys reports it unless its input was already in order); every
+ *                  other viewer is sorted as usual.
  *   keys_out       [total_keys] int64 device (sorted keys, same CSR offsets).
  *   rows_out       [total_keys][row_bytes] device (rows in the sorted order).
  *   workspace      device scratch of at least cc_sort_workspace_bytes(total_keys, n_viewers)

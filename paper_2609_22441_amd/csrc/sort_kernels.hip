@@ -226,6 +226,7 @@ __device__ __forceinline__ void store_regs(typename F::T *s, const typename F::T
 }
 
 struct SortOut {
+    int64_t limit;          // viewers with more records are copied through in input order
     int64_t total;
     const chunk_t *rows_in;
     int32_t row_chunks;
@@ -373,6 +374,17 @@ __global__ __launch_bounds__(kRangeThreads) void range_kernel(const int64_t *__r
     }
 }
 
+// Records [base, base + n) go to the output unchanged (keys and rows, in input order).
+__device__ __forceinline__ void copy_through(const int64_t *__restrict__ keys, int64_t base, int n,
+                                             const SortOut &o) {
+    for (int i = threadIdx.x; i < n; i += kThreads)
+        o.keys_out[base + i] = keys[base + i];
+    const int64_t c0 = base * o.row_chunks;
+    const int n_chunks = n * o.row_chunks;
+    for (int g = threadIdx.x; g < n_chunks; g += kThreads)
+        o.rows_out[c0 + g] = o.rows_in[c0 + g];
+}
+
 template <typename F>
 __device__ __forceinline__ void block_sort_body(const F &fm, char *lds,
                                                 const int64_t *__restrict__ keys,
@@ -391,6 +403,10 @@ __device__ __forceinline__ void block_sort_body(const F &fm, char *lds,
         const int64_t base = kb + (t - tile_off[v]) * kTile;
         const int n = (int)(min<int64_t>(base + kTile, ke) - base);
         const bool last = tile_off[v + 1] - tile_off[v] == 1;
+        if (ke - kb > o.limit) {                         // larger than the caller's bound
+            copy_through(keys, base, n, o);
+            continue;
+        }
 #pragma unroll
         for (int m = 0; m < kEpt; ++m) {
             const int i = m * kThreads + tid;
@@ -489,6 +505,8 @@ __device__ __forceinline__ void merge_body(const F &fm, char *lds, int64_t *s_sp
         const bool last = r == rounds_of(nt) - 1;
         int64_t kb, ke;
         segment(off, o.total, v, kb, ke);
+        if (ke - kb > o.limit)
+            continue;                                    // copied through by the block sort
         const int64_t n_seg = ke - kb;
         const int64_t run = (int64_t)kTile << r;
         const int64_t out0 = (t - tile_off[v]) * kTile;  // position within the viewer
@@ -620,8 +638,8 @@ hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int6
     while (((int64_t)1 << pbits) < largest)
         ++pbits;
     const Codec c{range, pbits};
-    const SortOut o{total, static_cast<const chunk_t *>(rows_in), row_bytes / 16, keys_out,
-                    static_cast<chunk_t *>(rows_out)};
+    const SortOut o{largest, total, static_cast<const chunk_t *>(rows_in), row_bytes / 16,
+                    keys_out, static_cast<chunk_t *>(rows_out)};
     int64_t n_slots = (total + kRangeThreads * kRangeUnroll - 1) / (kRangeThreads * kRangeUnroll);
     if (n_slots > kRangeSlots)
         n_slots = kRangeSlots;

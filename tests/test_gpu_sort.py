@@ -167,3 +167,24 @@ def test_many_viewers_with_merge_rounds(max_keys):
     keys = torch.randint(0, 3_000, (n,), generator=g)            # many equal keys: stability
     rows = torch.randint(0, 256, (n, 32), generator=g, dtype=torch.int64).to(torch.uint8)
     _check(ko, keys, rows, f"1300 viewers, max_keys {max_keys}", max_keys=max_keys)
+
+
+@pytest.mark.parametrize("max_keys", [1, 4095, 6000, 20_000])
+def test_viewers_above_the_max_keys_bound_are_copied_through(max_keys):
+    """A max_keys hint below some viewer's record count: that viewer is copied to the output in
+    input order (keys and rows), every other viewer is sorted as usual."""
+    sizes = [5000, 20_000, 300, 0, 6001, 1]
+    ko = torch.tensor([0] + np.cumsum(sizes).tolist(), dtype=torch.int64)
+    g = torch.Generator().manual_seed(max_keys)
+    n = int(ko[-1])
+    keys = torch.randint(-500, 500, (n,), generator=g)
+    rows = torch.randint(0, 256, (n, 48), generator=g, dtype=torch.int64).to(torch.uint8)
+    note(f"sort: viewers {sizes}, max_keys {max_keys}")
+    gk, gr = _gpu_sort(ko, keys, rows, max_keys)
+    wk, wr = oracle.sort_affinity(ko, keys, rows)
+    kn, rn = keys.numpy(), oracle.as_bytes(rows)
+    for v, size in enumerate(sizes):
+        sl = slice(int(ko[v]), int(ko[v + 1]))
+        want_k, want_r = (kn[sl], rn[sl]) if size > max_keys else (wk[sl], wr[sl])
+        assert np.array_equal(gk[sl], want_k), f"viewer {v} ({size} records): keys"
+        assert np.array_equal(gr[sl], want_r), f"viewer {v} ({size} records): rows"

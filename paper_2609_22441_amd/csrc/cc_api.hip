@@ -141,7 +141,7 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
     // while a longer window between fences costs every lookup another dependent line.
     int32_t lds_cap = ccj::kDefaultLdsKeys, stride = 0, wgs = 0;
     const int32_t budget = 16;
-    bool one_wave = false;
+    bool one_wave = false, lds_auto = true;
     const int64_t viewers = cand_offsets ? n_viewers : 1;
     if (viewers > 0 && total_keys / viewers > ccj::kLongListKeys) {
         lds_cap = ccj::kMaxLdsKeys;
@@ -153,8 +153,10 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
             return CC_ERR_INVALID_ARGUMENT;
         if (tuning->fence_stride & (tuning->fence_stride - 1))
             return CC_ERR_INVALID_ARGUMENT;
-        if (tuning->lds_keys)
+        if (tuning->lds_keys) {
             lds_cap = tuning->lds_keys;
+            lds_auto = false;
+        }
         stride = tuning->fence_stride;
         wgs = tuning->workgroups;
     }
@@ -191,6 +193,7 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
     a.fence_stride = stride;
     a.fence_budget = budget;
     a.one_wave = one_wave;
+    a.lds_auto = lds_auto && !one_wave;
     // Weighted ranges for CSR batches of 2 to kBalanceViewers viewers (each workgroup scans
     // every viewer's offsets once).
     a.balanced = cand_offsets != nullptr && n_viewers > 1 && n_viewers <= ccj::kBalanceViewers;

@@ -12,6 +12,9 @@ constexpr int kWindow = 15;          // keys between two fences read from L2 in 
 constexpr int kMaxLdsKeys = 18432;   // LDS key table limit: 144 KiB + at most 12 KiB of static
                                      // tables stays within the 160 KiB a workgroup may use
 constexpr int kDefaultLdsKeys = 8192;   // 64 KiB: within the register-limited occupancy
+// Table capacity when the grid is one workgroup per CU (occupancy is then set by the grid, not
+// by LDS): lists of up to 16,384 keys are staged whole, with no window read per lookup.
+constexpr int kWideLdsKeys = 16384;
 // Average key-list length above which a launch uses the whole LDS table and one resident wave
 // of workgroups (one per CU): the larger table keeps each lookup's window of keys within one
 // 64-byte sector, and one wave leaves no half-empty last wave.
@@ -48,6 +51,7 @@ struct JoinArgs {
     int32_t fence_stride;        // 0 = chosen per viewer segment
     int32_t fence_budget;        // fences staged per candidate of a segment (automatic stride)
     bool one_wave;               // automatic grid: one resident wave (long key lists)
+    bool lds_auto;               // lds_keys chosen by the library (not by a tuning)
     bool balanced;               // CSR ranges weighted by an estimated cost per candidate
     int32_t n_wg;                // workgroups launched (a multiple of 8); set by launch_join
     int64_t per_wg;              // candidates per workgroup (multiple of kBlock); set by launch_join

@@ -93,6 +93,17 @@ def test_workload4_double_join(store10m):
     assert 0.6 < hit[:, 0].mean() < 0.8 and 0.45 < hit[:, 1].mean() < 0.55
 
 
+@pytest.mark.timeout(300)
+def test_workload4_batched_as_benchmarked(store10m):
+    """64 second-degree requests in one launch (6.4M candidates, two lookups each into 20,000
+    keys per viewer): the launch the benchmark times, with the same inputs."""
+    st, h, cpu = store10m
+    _, r = W.SHAPES[4]
+    reqs = W.make_requests(st, r, 2, n_viewers=64)
+    _, hit = _check(st, h, cpu, reqs, 2, what="workload 4 x64 batched")
+    assert 0.6 < hit[:, 0].mean() < 0.8 and 0.45 < hit[:, 1].mean() < 0.55
+
+
 @pytest.mark.timeout(900)
 def test_workload5_large_scale():
     s, r = W.SHAPES[5]

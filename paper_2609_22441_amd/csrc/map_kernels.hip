@@ -60,10 +60,18 @@ __device__ __forceinline__ int64_t global_id() {
     return (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
 }
 
-// Workspace: slot int64[n] | rank int32[n] | partial int32[blocks + 1] | counts int64[4].
+// Workspace: slot int64[n] | rank int32[n] | posv int32[n] | last uint8[n] |
+// partial int32[blocks + 1] | counts int64[4].
+//   slot   map entry of record i (-1: reserved id or not placed)
+//   posv   the entry's position field once every record has claimed (read once, by the scan's
+//          first pass): a stored position >= 0, or -(3 + first record) for an id new in this
+//          batch, or kNoPos when slot < 0
+//   last   1 when record i is the last record with its id (it carries the row to store)
 struct Ws {
     int64_t *slot;
     int32_t *rank;
+    int32_t *posv;
+    uint8_t *last;
     int32_t *partial;
     int64_t *counts;     // {n_new, n_rejected, n_unplaced, n_wide_authors}
     int64_t blocks;
@@ -79,6 +87,10 @@ Ws carve(void *workspace, int64_t n) {
     w += round_up(n * 8);
     s.rank = reinterpret_cast<int32_t *>(w);
     w += round_up(n * 4);
+    s.posv = reinterpret_cast<int32_t *>(w);
+    w += round_up(n * 4);
+    s.last = w;
+    w += round_up(n);
     s.partial = reinterpret_cast<int32_t *>(w);
     w += round_up((s.blocks + 1) * 4);
     s.counts = reinterpret_cast<int64_t *>(w);
@@ -154,50 +166,82 @@ __global__ void counts_init_kernel(int64_t *counts) {
         counts[threadIdx.x] = 0;
 }
 
+// One record per quad of lanes: each lane reads one entry of the probed group (the quad reads
+// the group's 64 contiguous bytes in one instruction) and the quad votes. A group holding the id
+// ends the probe; otherwise the quad claims the group's first free entry with one
+// compare-and-swap (entries before it are occupied, so the occupied entries stay a prefix of
+// the probe order). A failed swap that returns another id means that entry was just taken:
+// the group is read again, at most kGroup times in all. A group with no free entry sends the
+// probe on to the next one. Then one lane records the first and last record of the entry.
 __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t mask,
                                                          const int64_t *__restrict__ ids,
                                                          int64_t n, Ws w) {
-    for (int64_t i = global_id(); i < n; i += grid_stride()) {
+    const int lane = threadIdx.x & 63;
+    const int sub = lane & (kGroup - 1);
+    const int quad0 = lane & ~(kGroup - 1);
+    const int64_t stride = grid_stride() / kGroup;
+    for (int64_t i = global_id() / kGroup; i < n; i += stride) {      // uniform per quad
         const int64_t key = ids[i];
-        int64_t found = -1;
         if (key == kEmptyKey) {
-            atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[1]), 1ULL);
-            w.slot[i] = -1;
+            if (sub == 0) {
+                atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[1]), 1ULL);
+                w.slot[i] = -1;
+            }
             continue;
         }
         uint64_t g = mix((uint64_t)key) & mask;
-        for (uint64_t probe = 0; probe < kMaxProbeGroups && probe <= mask && found < 0; ++probe) {
-            for (int e = 0; e < kGroup; ++e) {
-                MapEntry *m = map + g * kGroup + e;
-                int64_t k = load_key(m);
-                if (k == kEmptyKey) {
-                    k = (int64_t)atomicCAS(reinterpret_cast<unsigned long long *>(&m->key),
-                                           (unsigned long long)kEmptyKey,
-                                           (unsigned long long)key);
-                    if (k == kEmptyKey)
-                        k = key;                               // claimed by this record
-                }
-                if (k == key) {
-                    found = (int64_t)(g * kGroup + e);
-                    break;
-                }
+        int64_t found = -1;
+        bool stored = false;              // the id was stored by an earlier batch
+        uint64_t probe = 0;
+        int retries = 0;
+        while (probe < kMaxProbeGroups && probe <= mask) {
+            MapEntry *grp = map + g * kGroup;
+            const int64_t k = load_key(grp + sub);
+            const unsigned hit = (unsigned)(__ballot(k == key) >> quad0) & 0xF;
+            if (hit) {
+                found = (int64_t)(g * kGroup) + __builtin_ctz(hit);
+                // A position >= 0 was committed by an earlier batch and does not change during
+                // this one (only entries claimed in this batch carry pending values).
+                stored = __shfl(grp[sub].pos, quad0 + __builtin_ctz(hit)) >= 0;
+                break;
             }
-            g = (g + 1) & mask;
+            const unsigned emp = (unsigned)(__ballot(k == kEmptyKey) >> quad0) & 0xF;
+            if (!emp || retries == kGroup) {
+                g = (g + 1) & mask;
+                ++probe;
+                retries = 0;
+                continue;
+            }
+            const int e = __builtin_ctz(emp);
+            unsigned long long got = 0;
+            if (sub == e)
+                got = atomicCAS(reinterpret_cast<unsigned long long *>(&grp[e].key),
+                                (unsigned long long)kEmptyKey, (unsigned long long)key);
+            got = __shfl(got, quad0 + e);
+            if ((int64_t)got == kEmptyKey || (int64_t)got == key) {
+                found = (int64_t)(g * kGroup) + e;         // claimed now, or by the same id
+                break;
+            }
+            ++retries;                                     // another id took entry e
         }
-        w.slot[i] = found;
-        if (found < 0) {
-            atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[2]), 1ULL);
-            continue;
+        if (sub == 0) {
+            w.slot[i] = found;
+            if (found < 0) {
+                atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[2]), 1ULL);
+            } else {
+                // Atomics on device memory are performed past the per-XCD L2 caches, so each
+                // costs a memory round trip: a stored entry's position needs none.
+                if (!stored)
+                    atomicMax(&map[found].pos, -(3 + (int32_t)i));
+                atomicMax(&map[found].aux, (int32_t)i);
+            }
         }
-        atomicMax(&map[found].pos, -(3 + (int32_t)i));   // no effect on a stored entry (pos >= 0)
-        atomicMax(&map[found].aux, (int32_t)i);
     }
 }
 
-// Record i is the first occurrence of an id that is new in this batch.
-__device__ __forceinline__ int32_t first_new(const MapEntry *map, const Ws &w, int64_t i) {
-    const int64_t s = w.slot[i];
-    return (s >= 0 && map[s].pos == -(3 + (int32_t)i)) ? 1 : 0;
+// Record i is the first occurrence of an id that is new in this batch (posv already read).
+__device__ __forceinline__ int32_t first_new(const Ws &w, int64_t i) {
+    return w.posv[i] == -(3 + (int32_t)i) ? 1 : 0;
 }
 
 __device__ __forceinline__ int32_t block_sum(int32_t v, int32_t *lds) {
@@ -214,6 +258,9 @@ __device__ __forceinline__ int32_t block_sum(int32_t v, int32_t *lds) {
     return t;
 }
 
+// First pass of the scan, and the one pass that reads the claimed entries: every record keeps
+// its entry's position field and whether it is the id's last record, so that later passes
+// read the workspace in order instead of the map at random.
 __global__ __launch_bounds__(kThreads) void scan_reduce_kernel(const MapEntry *map, int64_t n,
                                                                Ws w) {
     __shared__ int32_t lds[kThreads / 64];
@@ -221,8 +268,19 @@ __global__ __launch_bounds__(kThreads) void scan_reduce_kernel(const MapEntry *m
     int32_t v = 0;
     for (int k = 0; k < kScanPer; ++k) {
         const int64_t i = base + k * kThreads + threadIdx.x;
-        if (i < n)
-            v += first_new(map, w, i);
+        if (i < n) {
+            const int64_t s = w.slot[i];
+            int32_t pv = kNoPos;
+            uint8_t last = 0;
+            if (s >= 0) {
+                const MapEntry e = map[s];
+                pv = e.pos;
+                last = e.aux == (int32_t)i ? 1 : 0;
+            }
+            w.posv[i] = pv;
+            w.last[i] = last;
+            v += pv == -(3 + (int32_t)i) ? 1 : 0;
+        }
     }
     const int32_t t = block_sum(v, lds);
     if (threadIdx.x == 0)
@@ -260,8 +318,7 @@ __global__ __launch_bounds__(kThreads) void scan_partials_kernel(Ws w) {
 }
 
 // rank[i] = number of first occurrences of new ids before record i.
-__global__ __launch_bounds__(kThreads) void scan_apply_kernel(const MapEntry *map, int64_t n,
-                                                              Ws w) {
+__global__ __launch_bounds__(kThreads) void scan_apply_kernel(int64_t n, Ws w) {
     __shared__ int32_t s[kThreads];
     const int tid = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * kScanBlock + (int64_t)tid * kScanPer;
@@ -270,7 +327,7 @@ __global__ __launch_bounds__(kThreads) void scan_apply_kernel(const MapEntry *ma
 #pragma unroll
     for (int k = 0; k < kScanPer; ++k) {
         const int64_t i = base + k;
-        f[k] = i < n ? first_new(map, w, i) : 0;
+        f[k] = i < n ? first_new(w, i) : 0;
         v += f[k];
     }
     s[tid] = v;
@@ -311,8 +368,9 @@ __global__ void rollback_kernel(MapEntry *map, int64_t n, Ws w, int64_t n_old, i
     }
 }
 
-// The last occurrence of each id writes its row (one 16-byte chunk per thread) and author id.
-__global__ __launch_bounds__(kThreads) void scatter_kernel(const MapEntry *map, int64_t n, Ws w,
+// The last occurrence of each id writes its row (one 16-byte chunk per thread) and author id,
+// at the stored position or at n_old + the rank of the id's first record.
+__global__ __launch_bounds__(kThreads) void scatter_kernel(int64_t n, Ws w,
                                                            int64_t n_old, int64_t capacity,
                                                            const int64_t *__restrict__ author_in,
                                                            const chunk_t *__restrict__ rows_in,
@@ -326,13 +384,10 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const MapEntry *map, 
     for (int64_t g = global_id(); g < total; g += grid_stride()) {
         const int64_t i = g / chunks;
         const int32_t q = (int32_t)(g - i * chunks);
-        const int64_t s = w.slot[i];
-        if (s < 0)
-            continue;
-        const MapEntry e = map[s];
-        if (e.aux != (int32_t)i)
+        if (!w.last[i])
             continue;                             // a later record carries this id's row
-        const int64_t target = e.pos >= 0 ? (int64_t)e.pos : n_old + w.rank[-(int64_t)e.pos - 3];
+        const int32_t pv = w.posv[i];
+        const int64_t target = pv >= 0 ? (int64_t)pv : n_old + w.rank[-(int64_t)pv - 3];
         rows[target * chunks + q] = rows_in[i * chunks + q];
         if (q == 0) {
             const int64_t x = author_in[i];
@@ -344,6 +399,9 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const MapEntry *map, 
     }
 }
 
+// The map changes only now, after the rows are written: the first record of a new id stores
+// its position, the last record of every id clears the entry's pending mark. Nothing is read
+// from the map.
 __global__ void commit_kernel(MapEntry *map, int64_t n, Ws w, int64_t n_old, int64_t capacity) {
     if (!batch_fits(w, n_old, capacity))
         return;
@@ -351,9 +409,16 @@ __global__ void commit_kernel(MapEntry *map, int64_t n, Ws w, int64_t n_old, int
         const int64_t s = w.slot[i];
         if (s < 0)
             continue;
-        if (map[s].pos == -(3 + (int32_t)i))      // only the id's first occurrence writes pos
-            map[s].pos = (int32_t)(n_old + w.rank[i]);
-        map[s].aux = -1;
+        const bool first = first_new(w, i) != 0, last = w.last[i] != 0;
+        const int32_t pos = (int32_t)(n_old + w.rank[i]);
+        if (first && last) {
+            typedef int pair_t __attribute__((ext_vector_type(2)));
+            *reinterpret_cast<pair_t *>(&map[s].pos) = pair_t{pos, -1};
+        } else if (first) {
+            map[s].pos = pos;
+        } else if (last) {
+            map[s].aux = -1;
+        }
     }
 }
 
@@ -427,7 +492,7 @@ int64_t upsert_workspace_bytes(int64_t n) {
     if (n <= 0 || n > kMaxBatch)            // the upsert rejects larger batches
         return 0;
     const int64_t blocks = (n + kScanBlock - 1) / kScanBlock;
-    return round_up(n * 8) + round_up(n * 4) + round_up((blocks + 1) * 4) + 256;
+    return round_up(n * 8) + 2 * round_up(n * 4) + round_up(n) + round_up((blocks + 1) * 4) + 256;
 }
 
 int64_t *upsert_counts(void *workspace, int64_t n) { return carve(workspace, n).counts; }
@@ -440,8 +505,8 @@ hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *i
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || n <= 0)
         return e;
-    hipLaunchKernelGGL(claim_kernel, dim3(grid_for(n, kThreads)), dim3(kThreads), 0, stream, map,
-                       mask, ids, n, w);
+    hipLaunchKernelGGL(claim_kernel, dim3(grid_for(n * kGroup, kThreads)), dim3(kThreads), 0,
+                       stream, map, mask, ids, n, w);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
     hipLaunchKernelGGL(scan_reduce_kernel, dim3((unsigned)w.blocks), dim3(kThreads), 0, stream,
@@ -452,7 +517,7 @@ hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *i
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
     hipLaunchKernelGGL(scan_apply_kernel, dim3((unsigned)w.blocks), dim3(kThreads), 0, stream,
-                       map, n, w);
+                       n, w);
     return hipGetLastError();
 }
 
@@ -465,7 +530,7 @@ hipError_t launch_upsert_finish(MapEntry *map, int64_t n, void *workspace, int64
     const Ws w = carve(workspace, n);
     const int32_t chunks = row_bytes / 16;
     hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(n * chunks, kThreads)), dim3(kThreads), 0,
-                       stream, map, n, w, n_old, capacity, author_in,
+                       stream, n, w, n_old, capacity, author_in,
                        static_cast<const chunk_t *>(rows_in), chunks, author, author32,
                        reinterpret_cast<chunk_t *>(rows));
     hipError_t e = hipGetLastError();

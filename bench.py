@@ -58,7 +58,8 @@ def parse(argv=None):
                     help="skip the per-workload entries (headline step and latency only)")
     ap.add_argument("--seed", type=int, default=2)
     ap.add_argument("--all-configs", action="store_true",
-                    help="also the padded layout, the id map, ingestion and the merge-path probe")
+                    help="also the padded layout, the id map, ingestion, the merge-path probe "
+                         "and a reference device copy")
     ap.add_argument("--only-headline", action="store_true",
                     help="only the headline steps (warm-up, cold steps, warm steps): for counter "
                          "passes on the headline launch")
@@ -239,6 +240,22 @@ def merge_path_probe(torch, P, st, b, dev):
                                                         max_keys=mk), 30)
     return {"entry": "cc_sort_affinity", "what": "candidates sorted by author id, per viewer",
             "records": n, "row_bytes": 16, "ms_median": t["median"], "ms_mean": t["mean"]}
+
+
+def reference_copy(torch, dev, flush):
+    """A reference point on this GPU: a plain 1 GiB device copy with PyTorch's own kernel
+    (streaming reads and writes, the best access pattern there is)."""
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    tc = time_launches(torch, lambda: dst.copy_(src), 20, flush=flush)
+    tw = time_launches(torch, lambda: dst.copy_(src), 20)
+    nbytes = 2 * (1 << 30)
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"reference-copy": {"entry": "torch copy_ (PyTorch's own kernel)", "bytes": nbytes,
+                               "ms_median": tc["median"], "ms_median_warm": tw["median"],
+                               "gbps": nbytes / (tc["median"] / 1e3) / 1e9,
+                               "gbps_warm": nbytes / (tw["median"] / 1e3) / 1e9}}
 
 
 def workload_entries(torch, P, W, dev, seed, flush, only=None, sorts=True, sorts_only=False,
@@ -612,7 +629,14 @@ def headline(torch, P, W, dev, args, flush):
     e1.record()
     torch.cuda.synchronize()
     ms_warm = e0.elapsed_time(e1) / args.steps
-    res = {"store": store, "st": st, "batches": batches, "wd": wd, "we": we, "total": total,
+    # Reference: the same launches with every key list empty (no search, no edge rows: the
+    # candidate positions, author ids, doc rows and output rows only).
+    nk = torch.zeros(REQS_PER_STEP + 1, dtype=torch.int64, device=dev)
+    no_keys = time_launches(torch, lambda: P.cc_join_batched(
+        store, batches[0][1].cand_offsets, batches[0][1].cand_idx, nk, batches[0][1].keys[:0],
+        batches[0][1].edge_rows[:0], out, hit), 20, flush=flush)
+    res = {"no_keys_ms": no_keys["median"], "store": store, "st": st, "batches": batches,
+           "wd": wd, "we": we, "total": total,
            "ms_step": ms_step, "ms_median": cold_sorted[len(cold) // 2],
            "ms_p99": cold_sorted[min(len(cold) - 1, int(0.99 * len(cold)))],
            "ms_warm": ms_warm, "wall": wall, "alg8": alg8_mean, "alg_stored": alg_st_mean}
@@ -740,6 +764,7 @@ def main(argv=None):
                                    cpu=tasks)
         if args.all_configs:
             configs.update(index_workloads(torch, P, W, dev, args.seed))
+            configs.update(reference_copy(torch, dev, flush))
         if tasks:
             cpu = cpu_baseline(tasks, args.cpu_seconds)
     line = {
@@ -771,6 +796,8 @@ def main(argv=None):
         "ms_per_step_p99": h["ms_p99"],
         "warm": {"ms_per_step": h["ms_warm"], "candidates_per_s": total / (h["ms_warm"] / 1e3),
                  "hbm_gbps": warm_gbps, "frac": warm_gbps / PEAK_GBPS},
+        "no_keys_reference": {"ms_median": h["no_keys_ms"],
+                              "what": "the same launch with every key list empty (cold)"},
         "latency": lat,
         "p99_ms": None if lat is None else lat["p99_ms"],
         "roofline": {

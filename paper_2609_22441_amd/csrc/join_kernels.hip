@@ -175,15 +175,21 @@ __device__ __forceinline__ int64_t range_index(int b, int n) {
 }
 
 // Estimated cost of one candidate of a viewer with K keys when the LDS table holds T keys, in
-// thousandths of the cost of a candidate of a short list. Fitted to join times of 64-viewer
-// batches whose lists all have one length (100 to 30,000 keys): a candidate of a 30,000-key
-// list costs about 25% more than one of a 100-key list, mostly from the window reads between
-// fences once K exceeds the table. Only the split of the work depends on it, never the result.
+// units of about 1/60 ns (a candidate of a 3,000-key list costs about 1,050). Fitted to
+// per-workgroup clocks of ragged 64-viewer batches (1.92M candidates, K from 100 to 30,000):
+// a candidate costs about 17% less when its list is short (its viewer's in-network candidates
+// then come from few authors, whose rows stay in the caches), grows with log K while the list
+// fits the table, and steps up by about 20% once K exceeds it (each lookup then reads a key
+// window from L2). Only the split of the work depends on it, never the result.
 __device__ __forceinline__ int64_t cand_cost(int64_t K, int64_t T) {
-    K = min<int64_t>(K, (int64_t)1 << 24);
-    int64_t c = 1000 + min(K, T) * 15 / 1000;
+    K = K < 1 ? 1 : min<int64_t>(K, (int64_t)1 << 24);
+    const int64_t k = min(K, T < 1 ? (int64_t)1 : T);
+    // 16 * log2(k), linear between powers of two.
+    const int l = 63 - __clzll((unsigned long long)k);
+    const int64_t l16 = 16 * l + (((k - ((int64_t)1 << l)) << 4) >> l);
+    int64_t c = 830 + 45 * max<int64_t>(l16 - 106, 0) / 16;      // 106 = 16 * log2(100)
     if (K > T)
-        c += 45 + (K - T) * 11 / 2000;
+        c += 100 + (K - T) * 11 / 2000;
     return c;
 }
 
@@ -203,8 +209,10 @@ __device__ __forceinline__ int64_t wave_scan_incl(int64_t x) {
 // joined, count); with prefix weights P, logical range r of n covers the candidates
 // whose weight starts in [T_r, T_{r+1}), T_r = floor(r * W / n), W the total. Every workgroup
 // computes the same prefix, so the ranges tile the candidates. Ranges of equal weight take
-// fewer candidates of long lists, which would otherwise finish last. Returns the range and the
-// viewer holding its first candidate; s is kBlock entries of LDS scratch (unused yet).
+// fewer candidates of long lists, which would otherwise finish last. (A cost for starting a
+// viewer, charged to the range that holds its first candidate, helped ragged batches by 1% but
+// slowed batches of equal viewers, whose ranges start exactly at viewer starts, by 2%.) Returns
+// the range and the viewer holding its first candidate; s is kBlock entries of LDS scratch.
 __device__ __forceinline__ void balanced_range(const JoinArgs &a, int64_t r, int64_t n,
                                                int64_t *s, int64_t &begin, int64_t &end,
                                                int32_t &v_first) {

@@ -228,12 +228,29 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
             w.slot[i] = found;
             if (found < 0) {
                 atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[2]), 1ULL);
-            } else {
+            } else if (stored) {
                 // Atomics on device memory are performed past the per-XCD L2 caches, so each
                 // costs a memory round trip: a stored entry's position needs none.
-                if (!stored)
-                    atomicMax(&map[found].pos, -(3 + (int32_t)i));
                 atomicMax(&map[found].aux, (int32_t)i);
+            } else {
+                // A new id's first and last record: while the entry still holds its values
+                // from between batches (no position, aux -1), one 64-bit compare-and-swap sets
+                // both; only when another record of the id got there first do the two maxima
+                // fold this record in. Between batches pos and aux always hold those values
+                // (map init, commit and rollback restore them), and they are below any value a
+                // record writes, so the swap sets exactly what the maxima would.
+                const unsigned long long idle =
+                    (unsigned long long)(uint32_t)kNoPos | ((unsigned long long)(uint32_t)-1 << 32);
+                const unsigned long long mine =
+                    (unsigned long long)(uint32_t)(-(3 + (int32_t)i)) |
+                    ((unsigned long long)(uint32_t)(int32_t)i << 32);
+                static_assert(offsetof(MapEntry, aux) == offsetof(MapEntry, pos) + 4,
+                              "pos and aux share one 8-byte word");
+                if (atomicCAS(reinterpret_cast<unsigned long long *>(&map[found].pos), idle,
+                              mine) != idle) {
+                    atomicMax(&map[found].pos, -(3 + (int32_t)i));
+                    atomicMax(&map[found].aux, (int32_t)i);
+                }
             }
         }
     }

@@ -60,24 +60,27 @@ __device__ __forceinline__ int64_t global_id() {
     return (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
 }
 
-// Workspace: slot int64[n] | rank int32[n] | posv int32[n] | last uint8[n] |
+// Workspace: slot int64[n] | rank int32[n] | posv int32[n] | last uint8[n] | dup uint8[n] |
 // partial int32[blocks + 1] | counts int64[4].
 //   slot   map entry of record i (-1: reserved id or not placed)
-//   posv   the entry's position field once every record has claimed (read once, by the scan's
-//          first pass): a stored position >= 0, or -(3 + first record) for an id new in this
-//          batch, or kNoPos when slot < 0
+//   posv   the entry's position field once every record has claimed: a stored position >= 0,
+//          or -(3 + first record) for an id new in this batch, or kNoPos when slot < 0
 //   last   1 when record i is the last record with its id (it carries the row to store)
+//   dup    1 when another record of the batch has record i's id. The claim writes posv and
+//          last as they are for an id without repeats; the scan's first pass reads the map
+//          entry only for the records marked here.
 struct Ws {
     int64_t *slot;
     int32_t *rank;
     int32_t *posv;
     uint8_t *last;
+    uint8_t *dup;
     int32_t *partial;
     int64_t *counts;     // {n_new, n_rejected, n_unplaced, n_wide_authors}
     int64_t blocks;
 };
 
-int64_t round_up(int64_t x) { return (x + 255) & ~int64_t(255); }
+__host__ __device__ int64_t round_up(int64_t x) { return (x + 255) & ~int64_t(255); }
 
 Ws carve(void *workspace, int64_t n) {
     uint8_t *w = static_cast<uint8_t *>(workspace);
@@ -90,6 +93,8 @@ Ws carve(void *workspace, int64_t n) {
     s.posv = reinterpret_cast<int32_t *>(w);
     w += round_up(n * 4);
     s.last = w;
+    w += round_up(n);
+    s.dup = w;
     w += round_up(n);
     s.partial = reinterpret_cast<int32_t *>(w);
     w += round_up((s.blocks + 1) * 4);
@@ -161,9 +166,13 @@ __global__ __launch_bounds__(kThreads) void resolve_kernel(const MapEntry *__res
     }
 }
 
-__global__ void counts_init_kernel(int64_t *counts) {
-    if (threadIdx.x < 4)
+// Clears the batch's counts and its repeat marks (round_up(n) bytes, 16 at a time).
+__global__ void counts_init_kernel(int64_t *counts, uint8_t *dup, int64_t n) {
+    if (blockIdx.x == 0 && threadIdx.x < 4)
         counts[threadIdx.x] = 0;
+    const int64_t chunks = round_up(n) / 16;
+    for (int64_t c = global_id(); c < chunks; c += grid_stride())
+        reinterpret_cast<chunk_t *>(dup)[c] = chunk_t{0u, 0u, 0u, 0u};
 }
 
 // One record per quad of lanes: each lane reads one entry of the probed group (the quad reads
@@ -192,6 +201,7 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
         uint64_t g = mix((uint64_t)key) & mask;
         int64_t found = -1;
         bool stored = false;              // the id was stored by an earlier batch
+        int32_t stored_pos = kNoPos;      // its position then
         uint64_t probe = 0;
         int retries = 0;
         while (probe < kMaxProbeGroups && probe <= mask) {
@@ -202,7 +212,8 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
                 found = (int64_t)(g * kGroup) + __builtin_ctz(hit);
                 // A position >= 0 was committed by an earlier batch and does not change during
                 // this one (only entries claimed in this batch carry pending values).
-                stored = __shfl(grp[sub].pos, quad0 + __builtin_ctz(hit)) >= 0;
+                stored_pos = __shfl(grp[sub].pos, quad0 + __builtin_ctz(hit));
+                stored = stored_pos >= 0;
                 break;
             }
             const unsigned emp = (unsigned)(__ballot(k == kEmptyKey) >> quad0) & 0xF;
@@ -230,8 +241,16 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
                 atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[2]), 1ULL);
             } else if (stored) {
                 // Atomics on device memory are performed past the per-XCD L2 caches, so each
-                // costs a memory round trip: a stored entry's position needs none.
-                atomicMax(&map[found].aux, (int32_t)i);
+                // costs a memory round trip: a stored entry's position needs none. The old
+                // last record comes back: -1 while this is the id's only record so far,
+                // otherwise a record of the same id, which this one marks with itself.
+                w.posv[i] = stored_pos;
+                w.last[i] = 1;
+                const int32_t prev = atomicMax(&map[found].aux, (int32_t)i);
+                if (prev >= 0) {
+                    w.dup[i] = 1;
+                    w.dup[prev] = 1;
+                }
             } else {
                 // A new id's first and last record: while the entry still holds its values
                 // from between batches (no position, aux -1), one 64-bit compare-and-swap sets
@@ -246,10 +265,23 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
                     ((unsigned long long)(uint32_t)(int32_t)i << 32);
                 static_assert(offsetof(MapEntry, aux) == offsetof(MapEntry, pos) + 4,
                               "pos and aux share one 8-byte word");
-                if (atomicCAS(reinterpret_cast<unsigned long long *>(&map[found].pos), idle,
-                              mine) != idle) {
+                w.posv[i] = -(3 + (int32_t)i);
+                w.last[i] = 1;
+                const unsigned long long old =
+                    atomicCAS(reinterpret_cast<unsigned long long *>(&map[found].pos), idle, mine);
+                if (old != idle) {
+                    // A repeat: mark it and the records whose indices the entry already holds
+                    // (the first swap's record is among them for the first repeat to arrive,
+                    // so every record of a repeated id ends up marked).
                     atomicMax(&map[found].pos, -(3 + (int32_t)i));
                     atomicMax(&map[found].aux, (int32_t)i);
+                    const int32_t p = (int32_t)(uint32_t)old;
+                    const int32_t q = (int32_t)(uint32_t)(old >> 32);
+                    w.dup[i] = 1;
+                    if (p <= -3 && -(int64_t)p - 3 < n)
+                        w.dup[-(int64_t)p - 3] = 1;
+                    if (q >= 0 && q < n)
+                        w.dup[q] = 1;
                 }
             }
         }
@@ -288,14 +320,17 @@ __global__ __launch_bounds__(kThreads) void scan_reduce_kernel(const MapEntry *m
         if (i < n) {
             const int64_t s = w.slot[i];
             int32_t pv = kNoPos;
-            uint8_t last = 0;
-            if (s >= 0) {
+            if (s < 0) {
+                w.posv[i] = kNoPos;
+                w.last[i] = 0;
+            } else if (w.dup[i]) {
                 const MapEntry e = map[s];
                 pv = e.pos;
-                last = e.aux == (int32_t)i ? 1 : 0;
+                w.posv[i] = pv;
+                w.last[i] = e.aux == (int32_t)i ? 1 : 0;
+            } else {
+                pv = w.posv[i];                   // as the claim wrote it: no repeats
             }
-            w.posv[i] = pv;
-            w.last[i] = last;
             v += pv == -(3 + (int32_t)i) ? 1 : 0;
         }
     }
@@ -509,7 +544,8 @@ int64_t upsert_workspace_bytes(int64_t n) {
     if (n <= 0 || n > kMaxBatch)            // the upsert rejects larger batches
         return 0;
     const int64_t blocks = (n + kScanBlock - 1) / kScanBlock;
-    return round_up(n * 8) + 2 * round_up(n * 4) + round_up(n) + round_up((blocks + 1) * 4) + 256;
+    return round_up(n * 8) + 2 * round_up(n * 4) + 2 * round_up(n) + round_up((blocks + 1) * 4) +
+           256;
 }
 
 int64_t *upsert_counts(void *workspace, int64_t n) { return carve(workspace, n).counts; }
@@ -518,7 +554,8 @@ hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *i
                                void *workspace, hipStream_t stream) {
     const Ws w = carve(workspace, n);
     const uint64_t mask = (uint64_t)(n_groups - 1);
-    hipLaunchKernelGGL(counts_init_kernel, dim3(1), dim3(64), 0, stream, w.counts);
+    hipLaunchKernelGGL(counts_init_kernel, dim3(grid_for(round_up(n > 0 ? n : 0) / 16, kThreads)),
+                       dim3(kThreads), 0, stream, w.counts, w.dup, n > 0 ? n : 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || n <= 0)
         return e;

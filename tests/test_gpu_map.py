@@ -116,6 +116,32 @@ def test_random_batches(cap):
         ix.close()
 
 
+def test_heavily_repeated_ids():
+    """Ids repeated up to thousands of times in one batch, shuffled among singletons, first as
+    new ids and then as stored ones: every repeat must leave the first record's rank and the
+    last record's row, as in the sequential replay (the claim marks repeats and only they read
+    the map again)."""
+    note("map: heavily repeated ids")
+    rng = np.random.default_rng(77)
+    ix = DeviceIndex(300_000, 32)
+    universe = W.doc_ids(torch.arange(400_000), 5).numpy()
+    try:
+        for b in range(4):
+            hot = universe[rng.integers(0, 50, 40)]                   # few ids, many records
+            counts = rng.integers(1, 3000, hot.size)
+            reps = np.repeat(hot, counts)
+            singles = universe[rng.integers(50 + b * 60_000, 50 + (b + 1) * 60_000, 50_000)]
+            ids = np.concatenate([reps, singles])
+            ids = ids[rng.permutation(ids.size)]
+            authors = rng.integers(-(1 << 40), 1 << 40, ids.size)
+            rows = rng.integers(0, 256, (ids.size, 32)).astype(np.uint8)
+            ix.upsert(ids, authors, torch.from_numpy(rows))
+            ix.check_state(f"repeats batch {b}")
+            ix.resolve(np.concatenate([hot, singles[:1000]]), f"repeats batch {b}")
+    finally:
+        ix.close()
+
+
 def test_full_store_is_unchanged_and_exact_fit_is_accepted():
     note("map: store full, then exact fit")
     ix = DeviceIndex(100, 16)

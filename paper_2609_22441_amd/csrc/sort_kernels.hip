@@ -247,8 +247,10 @@ __device__ __forceinline__ void emit(const F &fm, const typename F::T *s, int n,
             dst[pos + i] = s[pidx(i)];
         return;
     }
+    // The sorted keys and rows are not read again by this call: non-temporal stores keep them
+    // from evicting the lines of rows still to be gathered.
     for (int i = tid; i < n; i += kThreads)
-        o.keys_out[pos + i] = fm.key(s[pidx(i)]);
+        __builtin_nontemporal_store(fm.key(s[pidx(i)]), o.keys_out + pos + i);
     constexpr int U = 8;
     const int row_chunks = o.row_chunks;
     const int n_chunks = n * row_chunks;
@@ -270,7 +272,7 @@ __device__ __forceinline__ void emit(const F &fm, const typename F::T *s, int n,
 #pragma unroll
         for (int u = 0; u < U; ++u)
             if (dst_i[u] >= 0)
-                o.rows_out[dst_i[u]] = c[u];
+                __builtin_nontemporal_store(c[u], o.rows_out + dst_i[u]);
     }
 }
 

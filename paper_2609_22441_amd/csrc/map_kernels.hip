@@ -15,10 +15,11 @@
 //
 // Ingestion batch of n records (§6.2: identify new vs. stored ids, prefix-sum positions for the
 // new ones, scatter rows, update the map only after the rows are written):
-//   claim:   every record finds or claims its id's entry; atomic maxima leave in the entry the
-//            first record index (pos = -(3 + i), only while the entry is pending) and the last
-//            record index (aux); an exclusive scan over "record i is the first occurrence of a
-//            new id" gives each new id its rank, in batch order.
+//   claim:   every record finds or claims its id's entry, which then holds the first record
+//            index (pos = -(3 + i), only while the entry is pending) and the last record index
+//            (aux): one 64-bit compare-and-swap sets both for a new id, atomic maxima fold in
+//            its repeats; an exclusive scan over "record i is the first occurrence of a new id"
+//            gives each new id its rank, in batch order.
 //   apply:   the last occurrence of every id copies its row and author id to the stored
 //            position or to n_old + rank; then the first occurrence commits pos and every
 //            record clears aux.
@@ -181,7 +182,8 @@ __global__ void counts_init_kernel(int64_t *counts, uint8_t *dup, int64_t n) {
 // compare-and-swap (entries before it are occupied, so the occupied entries stay a prefix of
 // the probe order). A failed swap that returns another id means that entry was just taken:
 // the group is read again, at most kGroup times in all. A group with no free entry sends the
-// probe on to the next one. Then one lane records the first and last record of the entry.
+// probe on to the next one. Then one lane records the first and last record in the entry and
+// writes the record's workspace fields as they are for an id without repeats (see Ws).
 __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t mask,
                                                          const int64_t *__restrict__ ids,
                                                          int64_t n, Ws w) {

@@ -349,11 +349,11 @@ CC_API cc_status cc_resolve_ids(const cc_store *store, const int64_t *doc_ids, i
  *   rows_in        [total_keys][row_bytes] device.
  *   row_bytes      positive multiple of 16, at most 2^20 (1 MiB).
  *   total_keys     host copy of key_offsets[B]; < 2^32.
- *   max_keys       host upper bound on any one viewer's record count (fewer merge passes), or
- *                  0 if unknown. A viewer with more records than a nonzero max_keys is not
- *                  sorted: its keys and rows are copied to the output in their input order
- *                  (cc_validate_keys reports it unless its input was already in order); every
- *                  other viewer is sorted as usual.
+ *   max_keys       host upper bound on any one viewer's record count (fewer merge rounds and
+ *                  narrower sort elements), or 0 if unknown. A viewer with more records than a
+ *                  nonzero max_keys is not sorted: its keys and rows are copied to the output
+ *                  in their input order (cc_validate_keys reports it unless its input was
+ *                  already in order); every other viewer is sorted as usual.
  *   keys_out       [total_keys] int64 device (sorted keys, same CSR offsets).
  *   rows_out       [total_keys][row_bytes] device (rows in the sorted order).
  *   workspace      device scratch of at least cc_sort_workspace_bytes(total_keys, n_viewers)
@@ -371,6 +371,31 @@ CC_API cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets,
                                   int64_t total_keys, int64_t max_keys, int64_t *keys_out,
                                   void *rows_out, void *workspace, int64_t workspace_bytes,
                                   hipStream_t stream);
+
+/*
+ * cc_sort_affinity_method -- cc_sort_affinity with the sorting method named by the caller
+ * (cc_sort_affinity is CC_SORT_AUTO). Every method gives the same output; they differ in speed:
+ *   CC_SORT_MERGE  per-tile sorts in LDS, then merge rounds within each viewer (a number of
+ *                  kernels that grows with log2 of the largest viewer); the last round writes
+ *                  the keys and copies the rows. Fewer launches: the faster method for small
+ *                  calls.
+ *   CC_SORT_RADIX  least-significant-digit radix passes of up to 9 bits over the span of the
+ *                  call's keys (decoupled look-back between a viewer's tiles), then one gather
+ *                  of the rows. Moves fewer bytes per record: the faster method for large calls.
+ *   CC_SORT_AUTO   CC_SORT_RADIX from CC_SORT_RADIX_MIN_RECORDS records on, else CC_SORT_MERGE.
+ * Arguments, workspace and errors are those of cc_sort_affinity; a method other than these three
+ * is CC_ERR_INVALID_ARGUMENT.
+ */
+#define CC_SORT_AUTO 0
+#define CC_SORT_MERGE 1
+#define CC_SORT_RADIX 2
+#define CC_SORT_RADIX_MIN_RECORDS (1 << 20)
+CC_API cc_status cc_sort_affinity_method(int32_t method, int32_t n_viewers,
+                                         const int64_t *key_offsets, const int64_t *keys_in,
+                                         const void *rows_in, int32_t row_bytes,
+                                         int64_t total_keys, int64_t max_keys, int64_t *keys_out,
+                                         void *rows_out, void *workspace, int64_t workspace_bytes,
+                                         hipStream_t stream);
 
 /*
  * cc_sort_affinity_noalloc -- cc_sort_affinity for callers that cannot allocate device memory

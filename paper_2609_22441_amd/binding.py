@@ -19,7 +19,7 @@ EXPORTS = (
     "cc_store_create", "cc_store_destroy", "cc_store_info", "cc_store_invalid_count",
     "cc_store_reset_invalid_count", "cc_join", "cc_join_batched", "cc_join_batched_tuned",
     "cc_join_batched_padded", "cc_sort_workspace_bytes", "cc_sort_affinity",
-    "cc_sort_affinity_noalloc",
+    "cc_sort_affinity_method", "cc_sort_affinity_noalloc",
     "cc_store_create_indexed", "cc_upsert_workspace_bytes", "cc_store_upsert", "cc_store_read",
     "cc_store_layout",
     "cc_resolve_ids",
@@ -74,6 +74,7 @@ def lib():
             "cc_join_batched_padded": [vp, i32, vp, vp, i64, vp, vp, i64, vp, i32, vp, i32,
                                        ctypes.POINTER(vp), i64, vp, i64, vp, vp, vp],
             "cc_sort_affinity": [i32, vp, vp, vp, i32, i64, i64, vp, vp, vp, i64, vp],
+            "cc_sort_affinity_method": [i32, i32, vp, vp, vp, i32, i64, i64, vp, vp, vp, i64, vp],
             "cc_sort_affinity_noalloc": [i32, vp, vp, vp, i32, i64, i64, vp, vp, vp],
             "cc_store_create_indexed": [ctypes.POINTER(vp), i64, i32, vp],
             "cc_store_upsert": [vp, i64, vp, vp, vp, vp, i64, P64, P64, vp],
@@ -514,9 +515,15 @@ def cc_sort_workspace_bytes(total_keys: int, n_viewers: int) -> int:
     return lib().cc_sort_workspace_bytes(total_keys, n_viewers)
 
 
+SORT_AUTO, SORT_MERGE, SORT_RADIX = 0, 1, 2
+
+
 def cc_sort_affinity(key_offsets, keys_in, rows_in, keys_out, rows_out, workspace,
-                     max_keys: int = 0, total_keys: Optional[int] = None, stream=None) -> None:
-    """Stable per-viewer sort of affinity records (Alg. 1 Step 1; see include/cc_join.h)."""
+                     max_keys: int = 0, total_keys: Optional[int] = None, stream=None,
+                     method: int = SORT_AUTO) -> None:
+    """Stable per-viewer sort of affinity records (Alg. 1 Step 1; see include/cc_join.h).
+    `method` is CC_SORT_AUTO (cc_sort_affinity), CC_SORT_MERGE or CC_SORT_RADIX
+    (cc_sort_affinity_method)."""
     B = key_offsets.numel() - 1
     tk = keys_in.numel() if total_keys is None else int(total_keys)
     rb = _row_bytes(rows_in)
@@ -527,8 +534,13 @@ def cc_sort_affinity(key_offsets, keys_in, rows_in, keys_out, rows_out, workspac
     pr = _rows(rows_out, "rows_out", tk, rb)
     pw = _arr(workspace, "workspace")
     ws_bytes = workspace.numel() * workspace.element_size()
-    _check(lib().cc_sort_affinity(B, pko, pki, pri, rb, tk, max_keys, pk, pr, pw, ws_bytes,
-                                  _stream(stream)), "cc_sort_affinity")
+    if method == SORT_AUTO:
+        _check(lib().cc_sort_affinity(B, pko, pki, pri, rb, tk, max_keys, pk, pr, pw, ws_bytes,
+                                      _stream(stream)), "cc_sort_affinity")
+    else:
+        _check(lib().cc_sort_affinity_method(int(method), B, pko, pki, pri, rb, tk, max_keys, pk,
+                                             pr, pw, ws_bytes, _stream(stream)),
+               "cc_sort_affinity_method")
 
 
 def cc_sort_affinity_noalloc(key_offsets, keys_in, rows_in, keys_out, rows_out,

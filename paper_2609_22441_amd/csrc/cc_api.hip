@@ -11,6 +11,11 @@
 #include "cc_join.h"
 #include "join_internal.h"
 
+static_assert(CC_SORT_AUTO == ccj::kSortAuto && CC_SORT_MERGE == ccj::kSortMerge &&
+                  CC_SORT_RADIX == ccj::kSortRadix &&
+                  CC_SORT_RADIX_MIN_RECORDS == ccj::kSortRadixMinRecords,
+              "sort method values of the header and the kernels agree");
+
 struct cc_store {
     int device;
     int64_t n_docs;
@@ -621,10 +626,13 @@ int64_t cc_sort_workspace_bytes(int64_t total_keys, int32_t n_viewers) {
 }
 
 
-cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
-                           const void *rows_in, int32_t row_bytes, int64_t total_keys,
-                           int64_t max_keys, int64_t *keys_out, void *rows_out, void *workspace,
-                           int64_t workspace_bytes, hipStream_t stream) {
+cc_status cc_sort_affinity_method(int32_t method, int32_t n_viewers, const int64_t *key_offsets,
+                                  const int64_t *keys_in, const void *rows_in, int32_t row_bytes,
+                                  int64_t total_keys, int64_t max_keys, int64_t *keys_out,
+                                  void *rows_out, void *workspace, int64_t workspace_bytes,
+                                  hipStream_t stream) {
+    if (method != CC_SORT_AUTO && method != CC_SORT_MERGE && method != CC_SORT_RADIX)
+        return CC_ERR_INVALID_ARGUMENT;
     if (n_viewers < 0 || total_keys < 0 || total_keys >= ((int64_t)1 << 32) || max_keys < 0)
         return CC_ERR_INVALID_ARGUMENT;
     if (row_bytes <= 0 || (row_bytes & 15) || row_bytes > ccj::kMaxRowBytes)
@@ -646,8 +654,18 @@ cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets, const 
         overlaps(keys_out, kbytes, rows_out, rbytes))
         return CC_ERR_INVALID_ARGUMENT;
     hipError_t e = ccj::launch_sort(n_viewers, key_offsets, keys_in, rows_in, row_bytes,
-                                    total_keys, max_keys, keys_out, rows_out, workspace, stream);
+                                    total_keys, max_keys, keys_out, rows_out, workspace, method,
+                                    stream);
     return e == hipSuccess ? CC_OK : device_error(e);
+}
+
+cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
+                           const void *rows_in, int32_t row_bytes, int64_t total_keys,
+                           int64_t max_keys, int64_t *keys_out, void *rows_out, void *workspace,
+                           int64_t workspace_bytes, hipStream_t stream) {
+    return cc_sort_affinity_method(CC_SORT_AUTO, n_viewers, key_offsets, keys_in, rows_in,
+                                   row_bytes, total_keys, max_keys, keys_out, rows_out, workspace,
+                                   workspace_bytes, stream);
 }
 
 cc_status cc_sort_affinity_noalloc(int32_t n_viewers, const int64_t *key_offsets,
@@ -681,7 +699,7 @@ cc_status cc_sort_affinity_noalloc(int32_t n_viewers, const int64_t *key_offsets
         e = ccj::sort_scratch(dev, &scratch);
     if (e == hipSuccess)
         e = ccj::launch_sort(n_viewers, key_offsets, keys_in, rows_in, row_bytes, total_keys,
-                             max_keys, keys_out, rows_out, scratch, stream);
+                             max_keys, keys_out, rows_out, scratch, ccj::kSortAuto, stream);
     return e == hipSuccess ? CC_OK : device_error(e);
 }
 

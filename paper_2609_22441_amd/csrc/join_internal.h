@@ -72,7 +72,7 @@ hipError_t launch_pad_fill(const JoinArgs &args, int n_lookups, int8_t *valid_ma
 int64_t sort_workspace_bytes(int64_t total, int32_t n_viewers);
 
 // Largest call of the allocation-free sort: its workspace is a fixed device array of
-// sort_workspace_bytes(kSortScratchRecords, kSortScratchViewers) bytes (about 32.5 MiB).
+// sort_workspace_bytes(kSortScratchRecords, kSortScratchViewers) bytes.
 constexpr int64_t kSortScratchRecords = (int64_t)1 << 20;
 constexpr int32_t kSortScratchViewers = 1 << 16;
 constexpr int kMaxScratchDevices = 64;
@@ -81,11 +81,20 @@ constexpr int kMaxScratchDevices = 64;
 // current device. Resolved on the first call per device, then cached.
 hipError_t sort_scratch(int device, void **ptr);
 
-// Enqueue the per-viewer stable sort of affinity records (keys + rows) into keys_out/rows_out.
-// max_keys > 0 bounds the records of any one viewer (fewer merge rounds); 0 = unknown.
+// Sort methods (the values of CC_SORT_AUTO, CC_SORT_MERGE, CC_SORT_RADIX) and the call size
+// from which the automatic choice takes the radix method.
+constexpr int32_t kSortAuto = 0;
+constexpr int32_t kSortMerge = 1;
+constexpr int32_t kSortRadix = 2;
+constexpr int64_t kSortRadixMinRecords = (int64_t)1 << 20;
+
+// Enqueue the per-viewer stable sort of affinity records (keys + rows) into keys_out/rows_out
+// with `method` (kSortAuto: by call size). max_keys > 0 bounds the records of any one viewer;
+// 0 = unknown.
 hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
                        const void *rows_in, int32_t row_bytes, int64_t total, int64_t max_keys,
-                       int64_t *keys_out, void *rows_out, void *workspace, hipStream_t stream);
+                       int64_t *keys_out, void *rows_out, void *workspace, int32_t method,
+                       hipStream_t stream);
 
 // Enqueue a kernel that sets *counter (device) to zero.
 hipError_t launch_clear_counter(unsigned long long *counter, hipStream_t stream);

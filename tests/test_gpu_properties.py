@@ -72,10 +72,11 @@ def test_ingestion_and_resolution_equal_the_oracle(capacity, batches, queries):
 @SETTINGS
 @given(st.lists(st.lists(st.sampled_from(ID_POOL + list(range(-5, 40))), max_size=40),
                 min_size=1, max_size=5),
-       st.sampled_from([16, 32, 64]), st.booleans())
-def test_sort_equals_the_oracle(viewers, row_bytes, hint):
-    """Alg. 1 Step 1 on the device against the oracle's stable sort; the pool's int64 extremes
-    force the wide element form, small ids alone allow the packed one."""
+       st.sampled_from([16, 32, 64]), st.booleans(),
+       st.sampled_from([P.SORT_AUTO, P.SORT_MERGE, P.SORT_RADIX]))
+def test_sort_equals_the_oracle(viewers, row_bytes, hint, method):
+    """Alg. 1 Step 1 on the device against the oracle's stable sort, with each sort method; the
+    pool's int64 extremes force the wide element form, small ids alone allow the packed one."""
     keys = torch.tensor([k for v in viewers for k in v], dtype=torch.int64)
     ko = torch.tensor(np.cumsum([0] + [len(v) for v in viewers]), dtype=torch.int64)
     n = keys.numel()
@@ -88,7 +89,7 @@ def test_sort_equals_the_oracle(viewers, row_bytes, hint):
                      device=DEV)
     mk = max(len(v) for v in viewers) if hint else 0
     P.cc_sort_affinity(ko.to(DEV), keys.to(DEV), rows.to(DEV), k_out, r_out, ws, max_keys=mk,
-                       total_keys=n)
+                       total_keys=n, method=method)
     torch.cuda.synchronize()
     assert np.array_equal(k_out.cpu().numpy()[:n], want_k)
     assert np.array_equal(r_out.cpu().numpy()[:n], want_r)

@@ -25,23 +25,28 @@ def _shuffle_within(key_offsets, keys, rows, seed):
     return k, r
 
 
-def _gpu_sort(ko, keys, rows, max_keys=0):
+METHODS = (P.SORT_MERGE, P.SORT_RADIX)
+
+
+def _gpu_sort(ko, keys, rows, max_keys=0, method=P.SORT_AUTO):
     n = keys.numel()
     ws = torch.empty(max(16, P.cc_sort_workspace_bytes(n, ko.numel() - 1)), dtype=torch.uint8,
                      device=DEV)
     ko_d, k_d, r_d = ko.to(DEV), keys.to(DEV), rows.to(DEV)
     k_out = torch.full_like(k_d, -7)
     r_out = torch.full_like(r_d, 0xCD) if r_d.dtype == torch.uint8 else torch.empty_like(r_d)
-    P.cc_sort_affinity(ko_d, k_d, r_d, k_out, r_out, ws, max_keys=max_keys)
+    P.cc_sort_affinity(ko_d, k_d, r_d, k_out, r_out, ws, max_keys=max_keys, method=method)
     torch.cuda.synchronize()
     return k_out.cpu().numpy(), oracle.as_bytes(r_out.cpu())
 
 
 def _check(ko, keys, rows, what, max_keys=0):
-    gk, gr = _gpu_sort(ko, keys, rows, max_keys)
+    """Both sort methods (merge rounds; radix passes and a row gather) against the oracle."""
     wk, wr = oracle.sort_affinity(ko, keys, rows)
-    assert np.array_equal(gk, wk), f"{what}: keys"
-    assert np.array_equal(gr, wr), f"{what}: rows"
+    for method in METHODS:
+        gk, gr = _gpu_sort(ko, keys, rows, max_keys, method)
+        assert np.array_equal(gk, wk), f"{what}, method {method}: keys"
+        assert np.array_equal(gr, wr), f"{what}, method {method}: rows"
 
 
 def test_tiny_sorts_with_duplicates_and_empty_viewers():
@@ -180,11 +185,12 @@ def test_viewers_above_the_max_keys_bound_are_copied_through(max_keys):
     keys = torch.randint(-500, 500, (n,), generator=g)
     rows = torch.randint(0, 256, (n, 48), generator=g, dtype=torch.int64).to(torch.uint8)
     note(f"sort: viewers {sizes}, max_keys {max_keys}")
-    gk, gr = _gpu_sort(ko, keys, rows, max_keys)
     wk, wr = oracle.sort_affinity(ko, keys, rows)
     kn, rn = keys.numpy(), oracle.as_bytes(rows)
-    for v, size in enumerate(sizes):
-        sl = slice(int(ko[v]), int(ko[v + 1]))
-        want_k, want_r = (kn[sl], rn[sl]) if size > max_keys else (wk[sl], wr[sl])
-        assert np.array_equal(gk[sl], want_k), f"viewer {v} ({size} records): keys"
-        assert np.array_equal(gr[sl], want_r), f"viewer {v} ({size} records): rows"
+    for method in METHODS:
+        gk, gr = _gpu_sort(ko, keys, rows, max_keys, method)
+        for v, size in enumerate(sizes):
+            sl = slice(int(ko[v]), int(ko[v + 1]))
+            want_k, want_r = (kn[sl], rn[sl]) if size > max_keys else (wk[sl], wr[sl])
+            assert np.array_equal(gk[sl], want_k), f"method {method}, viewer {v} ({size}): keys"
+            assert np.array_equal(gr[sl], want_r), f"method {method}, viewer {v} ({size}): rows"

@@ -993,20 +993,6 @@ __device__ __forceinline__ int64_t radix_excl_scan(int64_t x, int64_t *s_w) {
     return base + inc - x;
 }
 
-// Lanes of this wavefront holding a valid record whose digit (< kRadix) equals this lane's:
-// one ballot per digit bit (bits above the call's digit width are zero in every lane and keep
-// the mask). Invalid lanes are excluded by the first ballot and never added back.
-__device__ __forceinline__ uint64_t peers_of(uint32_t d, bool valid) {
-    uint64_t m = __ballot(valid);
-#pragma unroll
-    for (int b = 0; b < kDigitBits; ++b) {
-        const bool bit = (d >> b) & 1u;
-        const uint64_t ones = __ballot(bit);
-        m &= bit ? ones : ~ones;
-    }
-    return m;
-}
-
 static_assert(kRadix == kThreads, "one thread per digit value");
 
 struct PassShared {
@@ -1016,9 +1002,11 @@ struct PassShared {
     int32_t start[kRadix];          // first tile-sorted index of each digit value
     int64_t scan_a[kRadix / 64], scan_b[kRadix / 64];
     int64_t tile;
+    int64_t desc[3];                // the tile's segment start and end, and its viewer's first tile
 };
 
-// Digit pass p over tile t of the multi-tile list (called by the whole workgroup).
+// Digit pass p over tile t of the multi-tile list (called by the whole workgroup), whose
+// descriptor is in sh.desc.
 template <typename F>
 __device__ __forceinline__ void pass_tile(const F &fm, const Digits &dg, int p, char *lds,
                                           PassShared &sh, const int64_t *__restrict__ keys,
@@ -1036,9 +1024,9 @@ __device__ __forceinline__ void pass_tile(const F &fm, const Digits &dg, int p, 
     {
         // The tile's segment, from the descriptor the histogram kernel wrote.
         TileAt a;
-        a.kb = mt.desc[t * 4];
-        a.ke = mt.desc[t * 4 + 1];
-        a.t0 = mt.desc[t * 4 + 2];
+        a.kb = sh.desc[0];
+        a.ke = sh.desc[1];
+        a.t0 = sh.desc[2];
         a.base = a.kb + (t - a.t0) * (E * kThreads);
         a.n = (int)clampk(a.ke - a.base, E * kThreads);
         if (a.ke - a.kb > o.limit)
@@ -1062,17 +1050,24 @@ __device__ __forceinline__ void pass_tile(const F &fm, const Digits &dg, int p, 
                     e[m] = i < a.n ? in[i] : F::pad();
             }
         }
-        for (int j = lane; j < kRadix; j += 64)
+        // Per wavefront: its digit counts, and one 64-bit lane-mask word per digit value (in the
+        // tile's LDS area, free until the scatter).
+        uint64_t *flags = reinterpret_cast<uint64_t *>(lds) + w * kRadix;
+        for (int j = lane; j < kRadix; j += 64) {
             sh.cnt[w][j] = 0;
+            flags[j] = 0;
+        }
         // The viewer's records of each smaller digit value: where the digit's records start.
         const uint32_t h =
             tid < kRadix ? mt.hist[(a.t0 * kMaxPasses + p) * kRadix + tid] : 0u;
         const int64_t vstart = radix_excl_scan(h, sh.scan_a);    // has a barrier
 
         // Rank within the wavefront: records of equal digit before this one in earlier rounds
-        // (the wavefront's running count) and in this round (lower lanes). The lowest lane of
-        // each digit group advances the count after every lane of the group has read it (the
-        // wavefront's LDS accesses complete in order).
+        // (the wavefront's running count) and in this round (lower lanes). The lanes of a round
+        // OR their bits into the wavefront's word for their digit and read it back: the lanes
+        // holding that digit (the wavefront's LDS accesses complete in order, so every OR of
+        // the round precedes every read). The lowest lane of each digit group then advances
+        // the count and clears the word, after every lane of the group has read both.
         // rd[m] = (rank << 16) | digit: one register per record, pinned here so that the
         // compiler does not keep the masks and partial counts it derives from alive until the
         // scatter below.
@@ -1081,13 +1076,21 @@ __device__ __forceinline__ void pass_tile(const F &fm, const Digits &dg, int p, 
         for (int m = 0; m < E; ++m) {
             const bool valid = (w * E + m) * 64 + lane < a.n;
             const uint32_t d = fm.digit(e[m], shift, dg.mask);
-            const uint64_t peers = peers_of(d, valid);
-            const uint32_t before = (uint32_t)__popcll(peers & below_me);
+            uint64_t peers = 0;
             uint32_t c = 0;
-            if (valid)
+            if (valid) {
+                __hip_atomic_fetch_or(&flags[d], ((uint64_t)1) << lane, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_WAVEFRONT);
+                peers = __hip_atomic_load(&flags[d], __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_WAVEFRONT);
                 c = sh.cnt[w][d];
-            if (valid && before == 0)
+            }
+            const uint32_t before = (uint32_t)__popcll(peers & below_me);
+            if (valid && before == 0) {
                 sh.cnt[w][d] = (uint16_t)(c + (uint32_t)__popcll(peers));
+                __hip_atomic_store(&flags[d], (uint64_t)0, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_WAVEFRONT);
+            }
             uint32_t x = ((c + before) << 16) | d;
             asm volatile("" : "+v"(x));
             rd[m] = x;
@@ -1160,9 +1163,25 @@ __device__ __forceinline__ void pass_body(const F &fm, const Digits &dg, int p, 
                                           const void *src_v, void *dst_v, const int64_t *off,
                                           int32_t B, const Multi &mt, const SortOut &o) {
     const int64_t n_mt = min(mt.mt_off[B], mt.mt_cap);
+    auto fetch_desc = [&](int64_t t) {
+        const int64_t *d = mt.desc + t * 4;
+        sh.desc[0] = d[0];
+        sh.desc[1] = d[1];
+        sh.desc[2] = d[2];
+    };
     if constexpr (!LOOP) {
-        if (threadIdx.x == 0)
-            sh.tile = blockIdx.x < n_mt ? (int64_t)atomicAdd(&mt.counters[p], 1u) : n_mt;
+        if (threadIdx.x == 0) {
+            // Claims come in dispatch order as a rule, so the descriptor of tile blockIdx.x is
+            // read while the claim is in flight, and replaced when the claim differs.
+            int64_t t = n_mt;
+            if (blockIdx.x < n_mt) {
+                fetch_desc(blockIdx.x);
+                t = (int64_t)atomicAdd(&mt.counters[p], 1u);
+                if (t != (int64_t)blockIdx.x)
+                    fetch_desc(t);
+            }
+            sh.tile = t;
+        }
         lds_sync();
         const int64_t t = sh.tile;
         if (t < n_mt)                                    // uniform
@@ -1170,8 +1189,12 @@ __device__ __forceinline__ void pass_body(const F &fm, const Digits &dg, int p, 
     } else {
         for (;;) {
             lds_sync();                                  // every thread is done with sh and lds
-            if (threadIdx.x == 0)
-                sh.tile = (int64_t)atomicAdd(&mt.counters[p], 1u);
+            if (threadIdx.x == 0) {
+                const int64_t t = (int64_t)atomicAdd(&mt.counters[p], 1u);
+                if (t < n_mt)
+                    fetch_desc(t);
+                sh.tile = t;
+            }
             lds_sync();
             const int64_t t = sh.tile;
             if (t >= n_mt)

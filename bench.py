@@ -202,9 +202,10 @@ class JoinCase:
         return e
 
 
-def sort_entry(torch, P, b, we, dev, tag):
+def sort_entry(torch, P, b, we, dev, tag, n_authors):
     """Alg. 1 Step 1 on a batch's records, shuffled within each viewer: the sort that precedes
-    the join when affinity records arrive unsorted."""
+    the join when affinity records arrive unsorted. The keys are author ids below n_authors, a
+    bound the caller knows, passed as the span bound key_bits."""
     ko = b.key_offsets
     nk = b.keys.numel()
     perm = torch.argsort(torch.rand(nk, device=dev) + 2.0 * torch.repeat_interleave(
@@ -213,10 +214,12 @@ def sort_entry(torch, P, b, we, dev, tag):
     k_out, r_out = torch.empty_like(k_in), torch.empty_like(r_in)
     ws = torch.empty(P.cc_sort_workspace_bytes(nk, ko.numel() - 1), dtype=torch.uint8, device=dev)
     mk = int((ko[1:] - ko[:-1]).max())
+    kb = max(1, (n_authors - 1).bit_length())
     t = time_launches(torch, lambda: P.cc_sort_affinity(ko, k_in, r_in, k_out, r_out, ws,
-                                                        max_keys=mk), 30)
+                                                        max_keys=mk, key_bits=kb), 30)
     alg = nk * (16 + 2 * we)
-    return {"entry": "cc_sort_affinity", "workload": tag, "viewers": ko.numel() - 1,
+    return {"entry": "cc_sort_affinity_method", "workload": tag, "viewers": ko.numel() - 1,
+            "method": "radix" if nk >= P.SORT_RADIX_MIN_RECORDS else "merge", "key_bits": kb,
             "records": nk, "row_bytes": we, "ms_median": t["median"], "ms_mean": t["mean"],
             "records_per_s": nk / (t["median"] / 1e3), "algorithmic_bytes": alg,
             "hbm_gbps": alg / (t["median"] / 1e3) / 1e9,
@@ -236,9 +239,10 @@ def merge_path_probe(torch, P, st, b, dev):
     k_out, r_out = torch.empty_like(keys), torch.empty_like(rows)
     ws = torch.empty(P.cc_sort_workspace_bytes(n, co.numel() - 1), dtype=torch.uint8, device=dev)
     mk = int((co[1:] - co[:-1]).max())
+    kb = max(1, (st.spec.n_authors - 1).bit_length())
     t = time_launches(torch, lambda: P.cc_sort_affinity(co, keys, rows, k_out, r_out, ws,
-                                                        max_keys=mk), 30)
-    return {"entry": "cc_sort_affinity", "what": "candidates sorted by author id, per viewer",
+                                                        max_keys=mk, key_bits=kb), 30)
+    return {"entry": "cc_sort_affinity_method", "what": "candidates sorted by author id, per viewer",
             "records": n, "row_bytes": 16, "ms_median": t["median"], "ms_mean": t["mean"]}
 
 
@@ -323,8 +327,8 @@ def workload_entries(torch, P, W, dev, seed, flush, only=None, sorts=True, sorts
                 res["3-padded"] = padded_entry(torch, P, c, r3.n_cand, 128, 64, dev)
             if sorts and tag in ("2x8", "3") and want(tag):
                 bs = c.b if tag == "3" else W.pack(W.make_requests(st, r2, seed, n_viewers=64))
-                res[("2" if tag == "2x8" else "3") + "-sort"] = sort_entry(torch, P, bs, 64, dev,
-                                                                          tag)
+                res[("2" if tag == "2x8" else "3") + "-sort"] = sort_entry(
+                    torch, P, bs, 64, dev, tag, st.spec.n_authors)
             del c
             torch.cuda.empty_cache()
         if cpu is not None and "4" in cpu and want("4x64"):
@@ -357,7 +361,7 @@ def workload_entries(torch, P, W, dev, seed, flush, only=None, sorts=True, sorts
         if not sorts_only:
             res["5"] = c.entry(torch, flush, 40)
         if sorts:
-            res["5-sort"] = sort_entry(torch, P, c.b, 128, dev, "5")
+            res["5-sort"] = sort_entry(torch, P, c.b, 128, dev, "5", s.n_authors)
         P.cc_store_destroy(store)
         del c
         torch.cuda.empty_cache()

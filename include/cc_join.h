@@ -373,8 +373,9 @@ CC_API cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets,
                                   hipStream_t stream);
 
 /*
- * cc_sort_affinity_method -- cc_sort_affinity with the sorting method named by the caller
- * (cc_sort_affinity is CC_SORT_AUTO). Every method gives the same output; they differ in speed:
+ * cc_sort_affinity_method -- cc_sort_affinity with the sorting method named by the caller, and
+ * an optional bound on the keys' span (cc_sort_affinity is CC_SORT_AUTO with key_bits 0). Every
+ * method gives the same output; they differ in speed:
  *   CC_SORT_MERGE  per-tile sorts in LDS, then merge rounds within each viewer (a number of
  *                  kernels that grows with log2 of the largest viewer); the last round writes
  *                  the keys and copies the rows. Fewer launches: the faster method for small
@@ -383,14 +384,22 @@ CC_API cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets,
  *                  call's keys (decoupled look-back between a viewer's tiles), then one gather
  *                  of the rows. Moves fewer bytes per record: the faster method for large calls.
  *   CC_SORT_AUTO   CC_SORT_RADIX from CC_SORT_RADIX_MIN_RECORDS records on, else CC_SORT_MERGE.
- * Arguments, workspace and errors are those of cc_sort_affinity; a method other than these three
- * is CC_ERR_INVALID_ARGUMENT.
+ *   key_bits       0, or an upper bound on the bit length of (largest key - smallest key) over
+ *                  the call (at most 64): the radix method then launches only the passes such a
+ *                  span needs (ceil(key_bits / 9), e.g. 3 for author ids below 2^27), where it
+ *                  otherwise launches all 8 and lets the unneeded ones return at once. A call
+ *                  whose keys span more bits than key_bits still writes, for every viewer, a
+ *                  permutation of its records with their rows (memory-safe), in an order that
+ *                  is then unspecified (cc_validate_keys flags it). The merge method ignores
+ *                  key_bits.
+ * Other arguments, the workspace and the errors are those of cc_sort_affinity; a method other
+ * than these three, or key_bits outside [0, 64], is CC_ERR_INVALID_ARGUMENT.
  */
 #define CC_SORT_AUTO 0
 #define CC_SORT_MERGE 1
 #define CC_SORT_RADIX 2
 #define CC_SORT_RADIX_MIN_RECORDS (1 << 20)
-CC_API cc_status cc_sort_affinity_method(int32_t method, int32_t n_viewers,
+CC_API cc_status cc_sort_affinity_method(int32_t method, int32_t key_bits, int32_t n_viewers,
                                          const int64_t *key_offsets, const int64_t *keys_in,
                                          const void *rows_in, int32_t row_bytes,
                                          int64_t total_keys, int64_t max_keys, int64_t *keys_out,

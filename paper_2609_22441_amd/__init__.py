@@ -10,7 +10,7 @@ non-OK status. There is no fallback: if the library is not built, every call rai
 from .binding import (  # noqa: F401
     CCError, PreparedJoin, PreparedJoinBatched, Tuning, cc_join, cc_join_batched, cc_join_batched_padded, cc_last_device_error,
     cc_sort_affinity, cc_sort_affinity_noalloc, cc_sort_workspace_bytes, cc_status_string,
-    SORT_AUTO, SORT_MERGE, SORT_RADIX,
+    SORT_AUTO, SORT_MERGE, SORT_RADIX, SORT_RADIX_MIN_RECORDS,
     cc_store_create, cc_store_destroy, cc_store_info, cc_store_invalid_count,
     cc_store_reset_invalid_count, cc_validate_keys, lib, LIB_PATH, EXPORTS,
     cc_store_create_indexed, cc_upsert_workspace_bytes, cc_store_upsert, cc_resolve_ids,

@@ -74,7 +74,8 @@ def lib():
             "cc_join_batched_padded": [vp, i32, vp, vp, i64, vp, vp, i64, vp, i32, vp, i32,
                                        ctypes.POINTER(vp), i64, vp, i64, vp, vp, vp],
             "cc_sort_affinity": [i32, vp, vp, vp, i32, i64, i64, vp, vp, vp, i64, vp],
-            "cc_sort_affinity_method": [i32, i32, vp, vp, vp, i32, i64, i64, vp, vp, vp, i64, vp],
+            "cc_sort_affinity_method": [i32, i32, i32, vp, vp, vp, i32, i64, i64, vp, vp, vp, i64,
+                                        vp],
             "cc_sort_affinity_noalloc": [i32, vp, vp, vp, i32, i64, i64, vp, vp, vp],
             "cc_store_create_indexed": [ctypes.POINTER(vp), i64, i32, vp],
             "cc_store_upsert": [vp, i64, vp, vp, vp, vp, i64, P64, P64, vp],
@@ -516,14 +517,15 @@ def cc_sort_workspace_bytes(total_keys: int, n_viewers: int) -> int:
 
 
 SORT_AUTO, SORT_MERGE, SORT_RADIX = 0, 1, 2
+SORT_RADIX_MIN_RECORDS = 1 << 20       # CC_SORT_AUTO takes the radix method from this many records
 
 
 def cc_sort_affinity(key_offsets, keys_in, rows_in, keys_out, rows_out, workspace,
                      max_keys: int = 0, total_keys: Optional[int] = None, stream=None,
-                     method: int = SORT_AUTO) -> None:
+                     method: int = SORT_AUTO, key_bits: int = 0) -> None:
     """Stable per-viewer sort of affinity records (Alg. 1 Step 1; see include/cc_join.h).
-    `method` is CC_SORT_AUTO (cc_sort_affinity), CC_SORT_MERGE or CC_SORT_RADIX
-    (cc_sort_affinity_method)."""
+    With the defaults this is cc_sort_affinity; a `method` (CC_SORT_MERGE, CC_SORT_RADIX) or a
+    `key_bits` bound on the keys' span calls cc_sort_affinity_method."""
     B = key_offsets.numel() - 1
     tk = keys_in.numel() if total_keys is None else int(total_keys)
     rb = _row_bytes(rows_in)
@@ -534,12 +536,12 @@ def cc_sort_affinity(key_offsets, keys_in, rows_in, keys_out, rows_out, workspac
     pr = _rows(rows_out, "rows_out", tk, rb)
     pw = _arr(workspace, "workspace")
     ws_bytes = workspace.numel() * workspace.element_size()
-    if method == SORT_AUTO:
+    if method == SORT_AUTO and key_bits == 0:
         _check(lib().cc_sort_affinity(B, pko, pki, pri, rb, tk, max_keys, pk, pr, pw, ws_bytes,
                                       _stream(stream)), "cc_sort_affinity")
     else:
-        _check(lib().cc_sort_affinity_method(int(method), B, pko, pki, pri, rb, tk, max_keys, pk,
-                                             pr, pw, ws_bytes, _stream(stream)),
+        _check(lib().cc_sort_affinity_method(int(method), int(key_bits), B, pko, pki, pri, rb, tk,
+                                             max_keys, pk, pr, pw, ws_bytes, _stream(stream)),
                "cc_sort_affinity_method")
 
 

@@ -626,12 +626,14 @@ int64_t cc_sort_workspace_bytes(int64_t total_keys, int32_t n_viewers) {
 }
 
 
-cc_status cc_sort_affinity_method(int32_t method, int32_t n_viewers, const int64_t *key_offsets,
-                                  const int64_t *keys_in, const void *rows_in, int32_t row_bytes,
-                                  int64_t total_keys, int64_t max_keys, int64_t *keys_out,
-                                  void *rows_out, void *workspace, int64_t workspace_bytes,
-                                  hipStream_t stream) {
+cc_status cc_sort_affinity_method(int32_t method, int32_t key_bits, int32_t n_viewers,
+                                  const int64_t *key_offsets, const int64_t *keys_in,
+                                  const void *rows_in, int32_t row_bytes, int64_t total_keys,
+                                  int64_t max_keys, int64_t *keys_out, void *rows_out,
+                                  void *workspace, int64_t workspace_bytes, hipStream_t stream) {
     if (method != CC_SORT_AUTO && method != CC_SORT_MERGE && method != CC_SORT_RADIX)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (key_bits < 0 || key_bits > 64)
         return CC_ERR_INVALID_ARGUMENT;
     if (n_viewers < 0 || total_keys < 0 || total_keys >= ((int64_t)1 << 32) || max_keys < 0)
         return CC_ERR_INVALID_ARGUMENT;
@@ -655,7 +657,7 @@ cc_status cc_sort_affinity_method(int32_t method, int32_t n_viewers, const int64
         return CC_ERR_INVALID_ARGUMENT;
     hipError_t e = ccj::launch_sort(n_viewers, key_offsets, keys_in, rows_in, row_bytes,
                                     total_keys, max_keys, keys_out, rows_out, workspace, method,
-                                    stream);
+                                    key_bits, stream);
     return e == hipSuccess ? CC_OK : device_error(e);
 }
 
@@ -663,7 +665,7 @@ cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets, const 
                            const void *rows_in, int32_t row_bytes, int64_t total_keys,
                            int64_t max_keys, int64_t *keys_out, void *rows_out, void *workspace,
                            int64_t workspace_bytes, hipStream_t stream) {
-    return cc_sort_affinity_method(CC_SORT_AUTO, n_viewers, key_offsets, keys_in, rows_in,
+    return cc_sort_affinity_method(CC_SORT_AUTO, 0, n_viewers, key_offsets, keys_in, rows_in,
                                    row_bytes, total_keys, max_keys, keys_out, rows_out, workspace,
                                    workspace_bytes, stream);
 }
@@ -699,7 +701,7 @@ cc_status cc_sort_affinity_noalloc(int32_t n_viewers, const int64_t *key_offsets
         e = ccj::sort_scratch(dev, &scratch);
     if (e == hipSuccess)
         e = ccj::launch_sort(n_viewers, key_offsets, keys_in, rows_in, row_bytes, total_keys,
-                             max_keys, keys_out, rows_out, scratch, ccj::kSortAuto, stream);
+                             max_keys, keys_out, rows_out, scratch, ccj::kSortAuto, 0, stream);
     return e == hipSuccess ? CC_OK : device_error(e);
 }
 

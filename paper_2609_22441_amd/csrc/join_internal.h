@@ -90,11 +90,11 @@ constexpr int64_t kSortRadixMinRecords = (int64_t)1 << 20;
 
 // Enqueue the per-viewer stable sort of affinity records (keys + rows) into keys_out/rows_out
 // with `method` (kSortAuto: by call size). max_keys > 0 bounds the records of any one viewer;
-// 0 = unknown.
+// key_bits > 0 bounds the bit length of (largest key - smallest key); 0 = unknown.
 hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
                        const void *rows_in, int32_t row_bytes, int64_t total, int64_t max_keys,
                        int64_t *keys_out, void *rows_out, void *workspace, int32_t method,
-                       hipStream_t stream);
+                       int32_t key_bits, hipStream_t stream);
 
 // Enqueue a kernel that sets *counter (device) to zero.
 hipError_t launch_clear_counter(unsigned long long *counter, hipStream_t stream);

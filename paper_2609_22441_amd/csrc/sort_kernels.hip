@@ -61,6 +61,7 @@ typedef unsigned int chunk_t __attribute__((ext_vector_type(4)));
 struct Codec {
     const int64_t *range;   // {min key, max key} in the workspace
     int32_t pbits;
+    int32_t max_passes;     // digit passes launched (from the caller's bound on the key span)
 };
 
 struct Wide {
@@ -124,7 +125,9 @@ __device__ __forceinline__ bool use_packed(const Codec &c, int64_t &kmin) {
 
 // The call's digits: P passes of D <= kDigitBits bits over the bit length of kmax - kmin (one
 // pass of one always-zero bit when every key is equal). P * D >= kbits and (P - 1) * D < kbits;
-// P <= kMaxPasses for 64-bit spans.
+// P <= kMaxPasses for 64-bit spans. When the keys span more bits than the launched passes
+// cover (a caller's bound that does not hold), those passes take full-width digits: the low
+// max_passes * kDigitBits bits of key - kmin are ordered, the rest are not.
 struct Digits {
     int P, D;
     uint32_t mask;
@@ -135,6 +138,8 @@ __device__ __forceinline__ Digits digits_of(const Codec &c) {
     const uint64_t span = kmax < kmin ? 0 : (uint64_t)kmax - (uint64_t)kmin;
     const int kbits = span ? 64 - __clzll(span) : 0;
     const int P = kbits ? (kbits + kDigitBits - 1) / kDigitBits : 1;
+    if (P > c.max_passes)
+        return Digits{c.max_passes, kDigitBits, (1u << kDigitBits) - 1};
     const int D = kbits ? (kbits + P - 1) / P : 1;
     return Digits{P, D, (1u << D) - 1};
 }
@@ -1314,7 +1319,7 @@ hipError_t sort_scratch(int device, void **ptr) {
 hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int64_t *keys_in,
                        const void *rows_in, int32_t row_bytes, int64_t total, int64_t max_keys,
                        int64_t *keys_out, void *rows_out, void *workspace, int32_t method,
-                       hipStream_t stream) {
+                       int32_t key_bits, hipStream_t stream) {
     if (total <= 0 || n_viewers <= 0)
         return hipSuccess;
     if (method == kSortAuto)
@@ -1332,7 +1337,10 @@ hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int6
     int32_t pbits = 1;
     while (((int64_t)1 << pbits) < largest)
         ++pbits;
-    const Codec c{range, pbits};
+    // Digit passes to launch: enough for a key span of key_bits bits (64 when unknown).
+    const int bits = key_bits > 0 && key_bits < 64 ? key_bits : 64;
+    const int passes = (bits + kDigitBits - 1) / kDigitBits;
+    const Codec c{range, pbits, passes < kMaxPasses ? passes : kMaxPasses};
     const SortOut o{largest, total, static_cast<const chunk_t *>(rows_in), row_bytes / 16,
                     keys_out, static_cast<chunk_t *>(rows_out),
                     reinterpret_cast<uint32_t *>(w + l.perm)};
@@ -1402,7 +1410,7 @@ hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int6
                            key_offsets, n_viewers, mt, o, c);
         e = hipGetLastError();
     }
-    for (int p = 0; e == hipSuccess && p < kMaxPasses; ++p) {
+    for (int p = 0; e == hipSuccess && p < c.max_passes; ++p) {
         const void *src = (p & 1) ? buf0 : buf1;     // written by pass p - 1
         void *dst = (p & 1) ? buf1 : buf0;
         if (p < kDirectPasses)

@@ -155,6 +155,37 @@ def test_sort_rejects_bad_arguments():
     assert call(tk=0, kin=None, rin=None, kout=None, rout=None, w=None, wb=0) == 0   # no work
 
 
+def test_sort_method_rejects_bad_arguments():
+    """cc_sort_affinity_method: an unknown method or a key_bits bound outside [0, 64] is refused
+    before anything is enqueued; the other checks are cc_sort_affinity's."""
+    lib = B.lib()
+    ws = lib.cc_sort_workspace_bytes(1000, 1)
+    base = dict(m=2, kb=26, nv=1, off=0x1000, kin=0x2000, rin=0x10000, rb=32, tk=1000, mk=0,
+                kout=0x30000, rout=0x100000, w=0x200000, wb=ws)
+
+    def call(**kw):
+        a = dict(base, **kw)
+        return lib.cc_sort_affinity_method(a["m"], a["kb"], a["nv"], a["off"], a["kin"], a["rin"],
+                                           a["rb"], a["tk"], a["mk"], a["kout"], a["rout"],
+                                           a["w"], a["wb"], None)
+
+    header = (ROOT / "include" / "cc_join.h").read_text()
+    for name, value in (("CC_SORT_AUTO", B.SORT_AUTO), ("CC_SORT_MERGE", B.SORT_MERGE),
+                        ("CC_SORT_RADIX", B.SORT_RADIX),
+                        ("CC_SORT_RADIX_MIN_RECORDS", B.SORT_RADIX_MIN_RECORDS)):
+        m = re.search(rf"#define {name} \(?(\d+)(?: << (\d+)\))?", header)
+        assert m, name                           # the binding's constants are the header's
+        assert int(m.group(1)) << int(m.group(2) or 0) == value, name
+    assert call(m=3) == 1 and call(m=-1) == 1    # no such method
+    assert call(kb=-1) == 1 and call(kb=65) == 1
+    assert call(rb=24) == 1                      # the checks of cc_sort_affinity apply
+    assert call(wb=ws - 1) == 1
+    for m in (0, 1, 2):                          # no work: nothing touches a device
+        for kb in (0, 1, 64):
+            assert call(m=m, kb=kb, tk=0, kin=None, rin=None, kout=None, rout=None, w=None,
+                        wb=0) == 0
+
+
 def test_indexed_store_rejects_bad_arguments():
     lib = B.lib()
     h = ctypes.c_void_p(99)

@@ -28,14 +28,15 @@ def _shuffle_within(key_offsets, keys, rows, seed):
 METHODS = (P.SORT_MERGE, P.SORT_RADIX)
 
 
-def _gpu_sort(ko, keys, rows, max_keys=0, method=P.SORT_AUTO):
+def _gpu_sort(ko, keys, rows, max_keys=0, method=P.SORT_AUTO, key_bits=0):
     n = keys.numel()
     ws = torch.empty(max(16, P.cc_sort_workspace_bytes(n, ko.numel() - 1)), dtype=torch.uint8,
                      device=DEV)
     ko_d, k_d, r_d = ko.to(DEV), keys.to(DEV), rows.to(DEV)
     k_out = torch.full_like(k_d, -7)
     r_out = torch.full_like(r_d, 0xCD) if r_d.dtype == torch.uint8 else torch.empty_like(r_d)
-    P.cc_sort_affinity(ko_d, k_d, r_d, k_out, r_out, ws, max_keys=max_keys, method=method)
+    P.cc_sort_affinity(ko_d, k_d, r_d, k_out, r_out, ws, max_keys=max_keys, method=method,
+                       key_bits=key_bits)
     torch.cuda.synchronize()
     return k_out.cpu().numpy(), oracle.as_bytes(r_out.cpu())
 
@@ -194,3 +195,46 @@ def test_viewers_above_the_max_keys_bound_are_copied_through(max_keys):
             want_k, want_r = (kn[sl], rn[sl]) if size > max_keys else (wk[sl], wr[sl])
             assert np.array_equal(gk[sl], want_k), f"method {method}, viewer {v} ({size}): keys"
             assert np.array_equal(gr[sl], want_r), f"method {method}, viewer {v} ({size}): rows"
+
+
+@pytest.mark.parametrize("key_bits", [9, 18, 26, 27, 64])
+def test_radix_passes_bounded_by_key_bits(key_bits):
+    """A key_bits bound that holds launches only the passes it needs (1 to 3 here, 8 at 64):
+    the output is still the oracle's. Viewers of several tiles, keys spanning just under
+    2^min(key_bits, 26), with repeats."""
+    note(f"sort: radix with key_bits {key_bits}")
+    g = W.gen("cpu", 40 + key_bits, 3)
+    sizes = torch.tensor([30_000, 9_000, 100, 17_000, 4097])
+    ko = torch.cat([torch.zeros(1, dtype=torch.int64), torch.cumsum(sizes, 0)])
+    n = int(ko[-1])
+    span = 1 << min(key_bits, 26)
+    keys = 1_000_000_000 + torch.randint(0, span, (n,), generator=g)
+    keys[::5] = 1_000_000_000 + span - 1                         # the span is exact, repeats
+    rows = torch.randint(0, 256, (n, 32), generator=g, dtype=torch.int64).to(torch.uint8)
+    gk, gr = _gpu_sort(ko, keys, rows, 0, P.SORT_RADIX, key_bits)
+    wk, wr = oracle.sort_affinity(ko, keys, rows)
+    assert np.array_equal(gk, wk), "keys"
+    assert np.array_equal(gr, wr), "rows"
+
+
+def test_radix_with_a_key_bits_bound_that_does_not_hold():
+    """Keys spanning 40 bits under a 9-bit bound: every viewer still gets a permutation of its
+    own records, each key with its own row (the order is unspecified), and nothing outside the
+    outputs changes."""
+    note("sort: radix with a key_bits bound that does not hold")
+    g = W.gen("cpu", 41, 3)
+    sizes = torch.tensor([20_000, 3_000, 12_000])
+    ko = torch.cat([torch.zeros(1, dtype=torch.int64), torch.cumsum(sizes, 0)])
+    n = int(ko[-1])
+    keys = torch.randint(0, 1 << 40, (n,), generator=g)
+    rows = torch.zeros(n, 16, dtype=torch.uint8)
+    rows.view(torch.int64)[:, 0] = keys                          # each row names its key
+    rows.view(torch.int64)[:, 1] = torch.arange(n)
+    gk, gr = _gpu_sort(ko, keys, rows, 0, P.SORT_RADIX, 9)
+    gr64 = gr.view(np.int64).reshape(n, 2)
+    assert np.array_equal(gr64[:, 0], gk), "every key travels with its own row"
+    for v in range(len(sizes)):
+        lo, hi = int(ko[v]), int(ko[v + 1])
+        src = gr64[lo:hi, 1]
+        assert np.array_equal(np.sort(src), np.arange(lo, hi)), f"viewer {v}: a permutation"
+

@@ -476,7 +476,8 @@ struct Multi {
     int64_t mt_cap;
     uint32_t *hist;        // [mt_cap][kMaxPasses][kRadix]
     uint64_t *status;      // [2][mt_cap][kRadix]
-    uint32_t *counters;    // [kMaxPasses] tile claims
+    uint32_t *counters;    // [kMaxPasses] tile claims of the looping passes
+    uint32_t *vclaim;      // [mt_cap][kMaxPasses] tile claims per viewer (row = first tile)
 };
 
 template <typename F>
@@ -894,6 +895,8 @@ __global__ __launch_bounds__(kThreads) void hist_kernel(const int64_t *__restric
         const TileAt a = tile_at(off, B, mt, o.total, t, tile);
         if (tid < 3)
             mt.desc[t * 4 + tid] = tid == 0 ? a.kb : (tid == 1 ? a.ke : a.t0);
+        if (t == a.t0 && tid < kMaxPasses)
+            mt.vclaim[t * kMaxPasses + tid] = 0;         // the viewer's claim counters
         if (a.ke - a.kb > o.limit) {
             copy_through(keys, a.base, a.n, o);
             continue;
@@ -1159,9 +1162,10 @@ __device__ __forceinline__ void pass_tile(const F &fm, const Digits &dg, int p, 
 }
 
 // Tiles of digit pass p, taken in claim order. LOOP = false: one tile per workgroup, the first
-// n_mt workgroups claiming the n_mt tiles and the rest of the grid (sized for the list's
-// capacity) leaving without a claim. LOOP = true: a smaller grid whose workgroups claim tiles
-// until none is left (a workgroup claims its next tile only after publishing the last one).
+// n_mt workgroups claiming the n_mt tiles (from per-viewer counters, so that only a viewer's
+// workgroups contend) and the rest of the grid (sized for the list's capacity) leaving without
+// a claim. LOOP = true: a smaller grid whose workgroups claim tiles from one counter until none
+// is left (a workgroup claims its next tile only after publishing the last one).
 template <typename F, bool LOOP>
 __device__ __forceinline__ void pass_body(const F &fm, const Digits &dg, int p, char *lds,
                                           PassShared &sh, const int64_t *__restrict__ keys,
@@ -1176,14 +1180,14 @@ __device__ __forceinline__ void pass_body(const F &fm, const Digits &dg, int p, 
     };
     if constexpr (!LOOP) {
         if (threadIdx.x == 0) {
-            // Claims come in dispatch order as a rule, so the descriptor of tile blockIdx.x is
-            // read while the claim is in flight, and replaced when the claim differs.
+            // Workgroup b < n_mt takes a tile of the viewer that tile b belongs to, in that
+            // viewer's claim order: as many workgroups as the viewer has tiles claim from its
+            // counter, and every tile shares the viewer's descriptor.
             int64_t t = n_mt;
             if (blockIdx.x < n_mt) {
                 fetch_desc(blockIdx.x);
-                t = (int64_t)atomicAdd(&mt.counters[p], 1u);
-                if (t != (int64_t)blockIdx.x)
-                    fetch_desc(t);
+                const int64_t t0 = sh.desc[2];
+                t = t0 + (int64_t)atomicAdd(&mt.vclaim[t0 * kMaxPasses + p], 1u);
             }
             sh.tile = t;
         }
@@ -1261,9 +1265,10 @@ constexpr int64_t multi_cap(int64_t total) { return 2 * total / kTile + 1; }
 
 // Workspace layout: two ping-pong element arrays, mt_off, the key range and pass counters
 // (256 bytes), the range kernel's per-workgroup slots, the digit histograms, the look-back
-// status words, the tile descriptors and the gather's input positions.
+// status words, the tile descriptors, the per-viewer claim counters and the gather's input
+// positions.
 struct Layout {
-    int64_t buf, mt_off, range, slots, hist, status, desc, perm, bytes;
+    int64_t buf, mt_off, range, slots, hist, status, desc, vclaim, perm, bytes;
 };
 
 constexpr Layout layout_of(int64_t total, int64_t n_viewers) {
@@ -1277,7 +1282,8 @@ constexpr Layout layout_of(int64_t total, int64_t n_viewers) {
     l.hist = l.slots + round_up(2 * kRangeSlots * 8);
     l.status = l.hist + round_up(cap * kMaxPasses * kRadix * 4);
     l.desc = l.status + round_up(2 * cap * kRadix * 8);
-    l.perm = l.desc + round_up(cap * 4 * 8);
+    l.vclaim = l.desc + round_up(cap * 4 * 8);
+    l.perm = l.vclaim + round_up(cap * kMaxPasses * 4);
     l.bytes = l.perm + round_up(total * 4);
     return l;
 }
@@ -1384,7 +1390,8 @@ hipError_t launch_sort(int32_t n_viewers, const int64_t *key_offsets, const int6
     const int64_t cap = multi_cap(total);
     const Multi mt{mt_off, reinterpret_cast<int64_t *>(w + l.desc), cap,
                    reinterpret_cast<uint32_t *>(w + l.hist),
-                   reinterpret_cast<uint64_t *>(w + l.status), counters};
+                   reinterpret_cast<uint64_t *>(w + l.status), counters,
+                   reinterpret_cast<uint32_t *>(w + l.vclaim)};
     // Grids: one workgroup per viewer for the small-viewer kernel and per possible tile of the
     // multi-tile list for the others (the first two loop over any remainder; the first
     // kDirectPasses pass kernels take one tile per workgroup). Valid offsets give at most

@@ -422,8 +422,13 @@ __global__ void rollback_kernel(MapEntry *map, int64_t n, Ws w, int64_t n_old, i
     }
 }
 
-// The last occurrence of each id writes its row (one 16-byte chunk per thread) and author id,
-// at the stored position or at n_old + the rank of the id's first record.
+// The last occurrence of each id writes its row and author id, at the stored position or at
+// n_old + the rank of the id's first record. A thread takes kScatterPer 16-byte chunks of its
+// grid-stride sequence at a time and issues their loads in three rounds (last marks; position
+// fields, row chunks and author ids; ranks of new ids), so that each round trip serves
+// kScatterPer chunks; a chunk's record and column advance by the stride without a division.
+constexpr int kScatterPer = 4;
+
 __global__ __launch_bounds__(kThreads) void scatter_kernel(int64_t n, Ws w,
                                                            int64_t n_old, int64_t capacity,
                                                            const int64_t *__restrict__ author_in,
@@ -434,21 +439,63 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(int64_t n, Ws w,
                                                            chunk_t *__restrict__ rows) {
     if (!batch_fits(w, n_old, capacity))
         return;
+    constexpr int U = kScatterPer;
     const int64_t total = n * chunks;
-    for (int64_t g = global_id(); g < total; g += grid_stride()) {
-        const int64_t i = g / chunks;
-        const int32_t q = (int32_t)(g - i * chunks);
-        if (!w.last[i])
-            continue;                             // a later record carries this id's row
-        const int32_t pv = w.posv[i];
-        const int64_t target = pv >= 0 ? (int64_t)pv : n_old + w.rank[-(int64_t)pv - 3];
-        rows[target * chunks + q] = rows_in[i * chunks + q];
-        if (q == 0) {
-            const int64_t x = author_in[i];
-            author[target] = x;
-            author32[target] = (int32_t)x;
-            if (x < INT32_MIN || x > INT32_MAX)
-                atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[3]), 1ULL);
+    const int64_t stride = grid_stride();
+    const int64_t di = stride / chunks;
+    const int32_t dq = (int32_t)(stride - di * chunks);
+    int64_t i = global_id() / chunks;
+    int32_t q = (int32_t)(global_id() - i * chunks);
+    for (int64_t g = global_id(); g < total; g += U * stride) {
+        int64_t rec[U];
+        int32_t col[U];
+        bool in[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            rec[u] = i;
+            col[u] = q;
+            in[u] = g + u * stride < total;
+            i += di;
+            q += dq;
+            if (q >= chunks) {
+                q -= chunks;
+                ++i;
+            }
+        }
+        bool carry[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            carry[u] = in[u] && w.last[rec[u]];   // a later record carries this id's row
+        int32_t pv[U];
+        chunk_t c[U];
+        int64_t x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            pv[u] = 0;
+            x[u] = 0;
+            if (carry[u]) {
+                pv[u] = w.posv[rec[u]];
+                c[u] = rows_in[rec[u] * chunks + col[u]];
+                if (col[u] == 0)
+                    x[u] = author_in[rec[u]];
+            }
+        }
+        int64_t target[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            target[u] = !carry[u] || pv[u] >= 0 ? (int64_t)pv[u]
+                                                : n_old + w.rank[-(int64_t)pv[u] - 3];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (!carry[u])
+                continue;
+            rows[target[u] * chunks + col[u]] = c[u];
+            if (col[u] == 0) {
+                author[target[u]] = x[u];
+                author32[target[u]] = (int32_t)x[u];
+                if (x[u] < INT32_MIN || x[u] > INT32_MAX)
+                    atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[3]), 1ULL);
+            }
         }
     }
 }
@@ -585,7 +632,8 @@ hipError_t launch_upsert_finish(MapEntry *map, int64_t n, void *workspace, int64
         return hipSuccess;
     const Ws w = carve(workspace, n);
     const int32_t chunks = row_bytes / 16;
-    hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(n * chunks, kThreads)), dim3(kThreads), 0,
+    hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(n * chunks, kThreads * kScatterPer)),
+                       dim3(kThreads), 0,
                        stream, n, w, n_old, capacity, author_in,
                        static_cast<const chunk_t *>(rows_in), chunks, author, author32,
                        reinterpret_cast<chunk_t *>(rows));

@@ -238,3 +238,19 @@ def test_radix_with_a_key_bits_bound_that_does_not_hold():
         src = gr64[lo:hi, 1]
         assert np.array_equal(np.sort(src), np.arange(lo, hi)), f"viewer {v}: a permutation"
 
+
+def test_multi_tile_viewers_with_wide_keys():
+    """Viewers of several tiles whose keys span all 64 bits: the radix method takes the wide
+    16-byte elements (4,096-record tiles) and all 8 digit passes, the last 5 of them on the
+    looping workgroups; repeats across tiles check stability. Both methods against the oracle."""
+    note("sort: multi-tile viewers, 64-bit key span")
+    g = W.gen("cpu", 43, 3)
+    sizes = torch.tensor([12_000, 4_097, 9_000, 1])
+    ko = torch.cat([torch.zeros(1, dtype=torch.int64), torch.cumsum(sizes, 0)])
+    n = int(ko[-1])
+    keys = torch.randint(-(1 << 62), 1 << 62, (n,), generator=g) * 2
+    keys[0], keys[1] = -(1 << 63), (1 << 63) - 1                 # the full span
+    keys[::11] = 12345                                           # repeats across tiles
+    rows = torch.randint(0, 256, (n, 16), generator=g, dtype=torch.int64).to(torch.uint8)
+    _check(ko, keys, rows, "64-bit span")
+

@@ -467,9 +467,11 @@ __global__ __launch_bounds__(kRangeThreads) void range_kernel(const int64_t *__r
 
 // ---- small viewers: the whole viewer sorted in LDS -----------------------------------------
 
-// Multi-tile context shared by the kernels below: mt_off from the plan, the list's capacity
-// (the workspace bound), the per-viewer digit histograms (row = the viewer's first tile in the
-// list) and the look-back status words (two sets, used by alternate passes).
+// Multi-tile context shared by the kernels below: mt_off from the plan, each tile's descriptor,
+// the list's capacity (the workspace bound), the per-viewer digit histograms (row = the
+// viewer's first tile in the list), the look-back status words (two sets, used by alternate
+// passes) and the tile-claim counters (per viewer for the direct passes, one per pass for the
+// looping ones).
 struct Multi {
     const int64_t *mt_off;
     int64_t *desc;         // [mt_cap][4]: segment start, end and first list tile of each tile

@@ -51,6 +51,9 @@ def test_noalloc_sort_equals_the_workspace_sort_on_two_calls():
     cases = [
         # at both limits: 2^20 records over 2^16 viewers, packed 8-byte elements
         (B.SORT_NOALLOC_MAX_VIEWERS, B.SORT_NOALLOC_MAX_RECORDS, 32, 11, False),
+        # 2^20 records over 16 viewers of several tiles: the radix method's digit passes and
+        # look-back words in the fixed scratch
+        (16, B.SORT_NOALLOC_MAX_RECORDS, 32, 13, False),
         # smaller, with int64 extremes (16-byte elements) and viewers of several tiles
         (7, 60_000, 64, 12, True),
     ]

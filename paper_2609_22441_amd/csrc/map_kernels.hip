@@ -17,8 +17,9 @@
 // new ones, scatter rows, update the map only after the rows are written):
 //   claim:   every record finds or claims its id's entry, which then holds the first record
 //            index (pos = -(3 + i), only while the entry is pending) and the last record index
-//            (aux): one 64-bit compare-and-swap sets both for a new id, atomic maxima fold in
-//            its repeats; an exclusive scan over "record i is the first occurrence of a new id"
+//            (aux): the record whose swap put a new id into the entry sets both with one
+//            write-through store, its repeats wait for that store and fold in with atomic
+//            maxima; an exclusive scan over "record i is the first occurrence of a new id"
 //            gives each new id its rank, in batch order.
 //   apply:   the last occurrence of every id copies its row and author id to the stored
 //            position or to n_old + rank; then the first occurrence commits pos and every
@@ -40,6 +41,7 @@ constexpr int kThreads = 256;
 constexpr int kScanPer = 4;                          // flags per thread in the scan
 constexpr int kScanBlock = kThreads * kScanPer;      // flags per scan block
 constexpr uint64_t kMaxProbeGroups = 64;
+constexpr int kMaxPolls = 1 << 16;                  // bound on a repeat's wait for its creator
 
 typedef unsigned int chunk_t __attribute__((ext_vector_type(4)));
 
@@ -183,7 +185,9 @@ __global__ void counts_init_kernel(int64_t *counts, uint8_t *dup, int64_t n) {
 // the probe order). A failed swap that returns another id means that entry was just taken:
 // the group is read again, at most kGroup times in all. A group with no free entry sends the
 // probe on to the next one. Then one lane records the first and last record in the entry and
-// writes the record's workspace fields as they are for an id without repeats (see Ws).
+// writes the record's workspace fields as they are for an id without repeats (see Ws). The
+// entry's key and its position word are separate 8-byte words, so a new id costs one swap (the
+// key) and one store; a second swap for the position word would be a second round trip past L2.
 __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t mask,
                                                          const int64_t *__restrict__ ids,
                                                          int64_t n, Ws w) {
@@ -202,6 +206,7 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
         }
         uint64_t g = mix((uint64_t)key) & mask;
         int64_t found = -1;
+        bool created = false;             // this record's swap put the id into the entry
         bool stored = false;              // the id was stored by an earlier batch
         int32_t stored_pos = kNoPos;      // its position then
         uint64_t probe = 0;
@@ -233,11 +238,29 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
             got = __shfl(got, quad0 + e);
             if ((int64_t)got == kEmptyKey || (int64_t)got == key) {
                 found = (int64_t)(g * kGroup) + e;         // claimed now, or by the same id
+                created = (int64_t)got == kEmptyKey;
                 break;
             }
             ++retries;                                     // another id took entry e
         }
-        if (sub == 0) {
+        // A record that put a new id into the entry publishes its first and last record with
+        // one write-through store: no other record of the batch writes that word before it
+        // (they wait for it below). This runs as a region of its own, ahead of the waits, so
+        // that a creator and a repeat of its id in one wavefront (whose divergent branches run
+        // one after the other) never leave the wait spinning before the store.
+        if (sub == 0 && found >= 0 && created) {
+            const unsigned long long mine =
+                (unsigned long long)(uint32_t)(-(3 + (int32_t)i)) |
+                ((unsigned long long)(uint32_t)(int32_t)i << 32);
+            static_assert(offsetof(MapEntry, aux) == offsetof(MapEntry, pos) + 4,
+                          "pos and aux share one 8-byte word");
+            w.slot[i] = found;
+            w.posv[i] = -(3 + (int32_t)i);
+            w.last[i] = 1;
+            __hip_atomic_store(reinterpret_cast<unsigned long long *>(&map[found].pos), mine,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (sub == 0 && !(found >= 0 && created)) {
             w.slot[i] = found;
             if (found < 0) {
                 atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[2]), 1ULL);
@@ -254,37 +277,32 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
                     w.dup[prev] = 1;
                 }
             } else {
-                // A new id's first and last record: while the entry still holds its values
-                // from between batches (no position, aux -1), one 64-bit compare-and-swap sets
-                // both; only when another record of the id got there first do the two maxima
-                // fold this record in. Between batches pos and aux always hold those values
-                // (map init, commit and rollback restore them), and they are below any value a
-                // record writes, so the swap sets exactly what the maxima would.
+                // A repeat of an id that another record of this batch put into the entry: wait
+                // until that record's store is visible (its values replace the idle ones; the
+                // wait is bounded, and the creator stores right after its swap), then fold this
+                // record in with two maxima. The first repeat to read sees the creator's values,
+                // so every record of a repeated id ends up marked.
                 const unsigned long long idle =
                     (unsigned long long)(uint32_t)kNoPos | ((unsigned long long)(uint32_t)-1 << 32);
-                const unsigned long long mine =
-                    (unsigned long long)(uint32_t)(-(3 + (int32_t)i)) |
-                    ((unsigned long long)(uint32_t)(int32_t)i << 32);
-                static_assert(offsetof(MapEntry, aux) == offsetof(MapEntry, pos) + 4,
-                              "pos and aux share one 8-byte word");
+                unsigned long long old = idle;
+                for (int polls = 0; polls < kMaxPolls; ++polls) {
+                    old = __hip_atomic_load(reinterpret_cast<unsigned long long *>(&map[found].pos),
+                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (old != idle)
+                        break;
+                    __builtin_amdgcn_s_sleep(1);
+                }
                 w.posv[i] = -(3 + (int32_t)i);
                 w.last[i] = 1;
-                const unsigned long long old =
-                    atomicCAS(reinterpret_cast<unsigned long long *>(&map[found].pos), idle, mine);
-                if (old != idle) {
-                    // A repeat: mark it and the records whose indices the entry already holds
-                    // (the first swap's record is among them for the first repeat to arrive,
-                    // so every record of a repeated id ends up marked).
-                    atomicMax(&map[found].pos, -(3 + (int32_t)i));
-                    atomicMax(&map[found].aux, (int32_t)i);
-                    const int32_t p = (int32_t)(uint32_t)old;
-                    const int32_t q = (int32_t)(uint32_t)(old >> 32);
-                    w.dup[i] = 1;
-                    if (p <= -3 && -(int64_t)p - 3 < n)
-                        w.dup[-(int64_t)p - 3] = 1;
-                    if (q >= 0 && q < n)
-                        w.dup[q] = 1;
-                }
+                atomicMax(&map[found].pos, -(3 + (int32_t)i));
+                atomicMax(&map[found].aux, (int32_t)i);
+                const int32_t p = (int32_t)(uint32_t)old;
+                const int32_t q = (int32_t)(uint32_t)(old >> 32);
+                w.dup[i] = 1;
+                if (p <= -3 && -(int64_t)p - 3 < n)
+                    w.dup[-(int64_t)p - 3] = 1;
+                if (q >= 0 && q < n)
+                    w.dup[q] = 1;
             }
         }
     }

@@ -301,7 +301,8 @@ CC_API cc_status cc_store_create_indexed(cc_store **out_store, int64_t capacity,
  * fit in the remaining capacity, or an id cannot be placed within the map's probe
  * limit (64 groups; not expected below load 1/2), the batch is undone and CC_ERR_STORE_FULL is
  * returned with the store unchanged. Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_NOT_SUPPORTED,
- * CC_ERR_STORE_FULL, CC_ERR_DEVICE.
+ * CC_ERR_STORE_FULL, CC_ERR_DEVICE (also, with the store unchanged, if a bounded wait between
+ * the workgroups of the batch's scan gives up; not expected).
  */
 /* Workspace bytes cc_store_upsert needs for n_records; 0 when n_records <= 0 or > 2^30 (a
  * batch the upsert rejects). */

@@ -291,7 +291,8 @@ cc_status new_store(int64_t capacity, int32_t doc_row_bytes, bool with_map, hipS
         if ((e = hipMalloc(&s->d_author32, (size_t)(capacity > 0 ? capacity * 4 : 256))) != hipSuccess)
             return alloc_failure(s, e);
         s->compact = true;
-        if ((e = hipHostMalloc(&s->h_counts, 4 * sizeof(int64_t), hipHostMallocDefault)) != hipSuccess)
+        if ((e = hipHostMalloc(&s->h_counts, ccj::kUpsertCounts * sizeof(int64_t),
+                               hipHostMallocDefault)) != hipSuccess)
             return alloc_failure(s, e);
     }
     if ((e = hipMemsetAsync(s->d_invalid, 0, sizeof(unsigned long long), stream)) != hipSuccess)
@@ -440,13 +441,15 @@ cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc
                                       store->d_rows, stream);
     int64_t *counts = store->h_counts;        // pinned: the read-back is one small DMA
     if (e == hipSuccess)
-        e = hipMemcpyAsync(counts, ccj::upsert_counts(workspace, n_records), 4 * sizeof(int64_t),
-                           hipMemcpyDeviceToHost, stream);
+        e = hipMemcpyAsync(counts, ccj::upsert_counts(workspace, n_records),
+                           ccj::kUpsertCounts * sizeof(int64_t), hipMemcpyDeviceToHost, stream);
     if (e == hipSuccess)
         e = hipStreamSynchronize(stream);
     if (e != hipSuccess)
         return device_error(e);
     const int64_t fresh = counts[0], rejected = counts[1], unplaced = counts[2];
+    if (counts[5] > 0)
+        return CC_ERR_DEVICE;                // a bounded device wait gave up; rolled back
     if (unplaced > 0 || store->n_docs + fresh > store->capacity)
         return CC_ERR_STORE_FULL;            // rolled back on the device: the store is unchanged
     store->n_docs += fresh;

@@ -129,10 +129,12 @@ hipError_t launch_resolve(const MapEntry *map, int64_t n_groups, const int64_t *
                           int64_t *pos, hipStream_t stream);
 
 // Ingestion batch in two launches: claim (map entries for every id, first/last occurrence,
-// ranks of the new ids, and the counts {n_new, n_rejected, n_unplaced, n_wide_authors} at
-// upsert_counts(ws, n)), then finish: when the batch fits (nothing unplaced and
+// ranks of the new ids, and kUpsertCounts counts at upsert_counts(ws, n): n_new, n_rejected,
+// n_unplaced, n_wide_authors, the scan's tile counter, scan waits that reached their bound),
+// then finish: when the batch fits (nothing unplaced, no bounded wait given up and
 // n_old + n_new <= capacity) scatter the rows and commit the map, otherwise roll the claim
 // back. The decision is taken on the device from the counts.
+constexpr int kUpsertCounts = 6;
 int64_t upsert_workspace_bytes(int64_t n);
 int64_t *upsert_counts(void *workspace, int64_t n);
 hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *ids, int64_t n,

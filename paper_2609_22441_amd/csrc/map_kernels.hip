@@ -20,7 +20,8 @@
 //            (aux): the record whose swap put a new id into the entry sets both with one
 //            write-through store, its repeats wait for that store and fold in with atomic
 //            maxima; an exclusive scan over "record i is the first occurrence of a new id"
-//            gives each new id its rank, in batch order.
+//            (one pass, tiles chained by decoupled look-back) gives each new id its rank, in
+//            batch order.
 //   apply:   the last occurrence of every id copies its row and author id to the stored
 //            position or to n_old + rank; then the first occurrence commits pos and every
 //            record clears aux.
@@ -38,10 +39,14 @@ namespace ccj {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kScanPer = 4;                          // flags per thread in the scan
-constexpr int kScanBlock = kThreads * kScanPer;      // flags per scan block
+constexpr int kScanPer = 32;                         // records per thread in the scan
+constexpr int kScanBlock = kThreads * kScanPer;      // records per scan tile
 constexpr uint64_t kMaxProbeGroups = 64;
 constexpr int kMaxPolls = 1 << 16;                  // bound on a repeat's wait for its creator
+// counts[]: new ids, rejected records, unplaced ids, author ids wider than 32 bits, the scan's
+// tile counter, scan waits that reached their bound.
+constexpr int kCounts = kUpsertCounts;
+static_assert(kCounts * 8 <= 256, "the counts live in the workspace's last 256 bytes");
 
 typedef unsigned int chunk_t __attribute__((ext_vector_type(4)));
 
@@ -64,22 +69,23 @@ __device__ __forceinline__ int64_t global_id() {
 }
 
 // Workspace: slot int64[n] | rank int32[n] | posv int32[n] | last uint8[n] | dup uint8[n] |
-// partial int32[blocks + 1] | counts int64[4].
+// status uint64[blocks] | counts int64[kCounts].
 //   slot   map entry of record i (-1: reserved id or not placed)
 //   posv   the entry's position field once every record has claimed: a stored position >= 0,
 //          or -(3 + first record) for an id new in this batch, or kNoPos when slot < 0
 //   last   1 when record i is the last record with its id (it carries the row to store)
 //   dup    1 when another record of the batch has record i's id. The claim writes posv and
-//          last as they are for an id without repeats; the scan's first pass reads the map
-//          entry only for the records marked here.
+//          last as they are for an id without repeats (and kNoPos, 0 for a record without an
+//          entry); the scan reads the map entry only for the records marked here.
+//   status the scan's look-back word of each tile of kScanBlock records (cleared per batch)
 struct Ws {
     int64_t *slot;
     int32_t *rank;
     int32_t *posv;
     uint8_t *last;
     uint8_t *dup;
-    int32_t *partial;
-    int64_t *counts;     // {n_new, n_rejected, n_unplaced, n_wide_authors}
+    uint64_t *status;
+    int64_t *counts;     // kCounts entries (see kCounts)
     int64_t blocks;
 };
 
@@ -99,8 +105,8 @@ Ws carve(void *workspace, int64_t n) {
     w += round_up(n);
     s.dup = w;
     w += round_up(n);
-    s.partial = reinterpret_cast<int32_t *>(w);
-    w += round_up((s.blocks + 1) * 4);
+    s.status = reinterpret_cast<uint64_t *>(w);
+    w += round_up(s.blocks * 8);
     s.counts = reinterpret_cast<int64_t *>(w);
     return s;
 }
@@ -169,13 +175,16 @@ __global__ __launch_bounds__(kThreads) void resolve_kernel(const MapEntry *__res
     }
 }
 
-// Clears the batch's counts and its repeat marks (round_up(n) bytes, 16 at a time).
-__global__ void counts_init_kernel(int64_t *counts, uint8_t *dup, int64_t n) {
-    if (blockIdx.x == 0 && threadIdx.x < 4)
-        counts[threadIdx.x] = 0;
+// Clears the batch's counts, its repeat marks (round_up(n) bytes, 16 at a time) and the scan's
+// look-back words.
+__global__ void counts_init_kernel(Ws w, int64_t n) {
+    if (blockIdx.x == 0 && threadIdx.x < kCounts)
+        w.counts[threadIdx.x] = 0;
     const int64_t chunks = round_up(n) / 16;
     for (int64_t c = global_id(); c < chunks; c += grid_stride())
-        reinterpret_cast<chunk_t *>(dup)[c] = chunk_t{0u, 0u, 0u, 0u};
+        reinterpret_cast<chunk_t *>(w.dup)[c] = chunk_t{0u, 0u, 0u, 0u};
+    for (int64_t b = global_id(); b < w.blocks; b += grid_stride())
+        w.status[b] = 0;
 }
 
 // One record per quad of lanes: each lane reads one entry of the probed group (the quad reads
@@ -201,6 +210,8 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
             if (sub == 0) {
                 atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[1]), 1ULL);
                 w.slot[i] = -1;
+                w.posv[i] = kNoPos;
+                w.last[i] = 0;
             }
             continue;
         }
@@ -264,6 +275,8 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
             w.slot[i] = found;
             if (found < 0) {
                 atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[2]), 1ULL);
+                w.posv[i] = kNoPos;
+                w.last[i] = 0;
             } else if (stored) {
                 // Atomics on device memory are performed past the per-XCD L2 caches, so each
                 // costs a memory round trip: a stored entry's position needs none. The old
@@ -313,116 +326,165 @@ __device__ __forceinline__ int32_t first_new(const Ws &w, int64_t i) {
     return w.posv[i] == -(3 + (int32_t)i) ? 1 : 0;
 }
 
-__device__ __forceinline__ int32_t block_sum(int32_t v, int32_t *lds) {
-    // 64-lane reduction, then across the kThreads / 64 waves
+// Look-back word of one scan tile: flag in the top two bits (0 = not yet published, kAgg = the
+// tile's own count of new ids, kInc = the count over this and every earlier tile), the count
+// below them.
+constexpr uint64_t kAgg = (uint64_t)1 << 62;
+constexpr uint64_t kInc = (uint64_t)2 << 62;
+constexpr uint64_t kCountMask = kAgg - 1;
+
+__device__ __forceinline__ void put_status(uint64_t *p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint64_t get_status(const uint64_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ int64_t wave_sum(int64_t x) {
     for (int off = 32; off > 0; off >>= 1)
-        v += __shfl_down(v, off);
-    const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0)
-        lds[wave] = v;
-    __syncthreads();
-    int32_t t = 0;
-    for (int k = 0; k < kThreads / 64; ++k)
-        t += lds[k];
-    return t;
+        x += __shfl_xor(x, off);
+    return x;
 }
 
-// First pass of the scan, and the one pass that reads the claimed entries: every record keeps
-// its entry's position field and whether it is the id's last record, so that later passes
-// read the workspace in order instead of the map at random.
-__global__ __launch_bounds__(kThreads) void scan_reduce_kernel(const MapEntry *map, int64_t n,
-                                                               Ws w) {
-    __shared__ int32_t lds[kThreads / 64];
-    const int64_t base = (int64_t)blockIdx.x * kScanBlock;
-    int32_t v = 0;
+// New ids in tiles 0 .. k (k >= 0), by one whole wavefront: lane l reads the word of tile
+// k - l, so each round trip inspects 64 tiles; the words up to the nearest inclusive one are
+// added, else all 64 and the window moves down. Tiles below 0 read as inclusive zeros (tile 0
+// itself always publishes an inclusive word). Each tile waits only for tiles claimed before
+// it, by workgroups that publish their own count before they look back, so a wait lasts about
+// one tile's loads. A word still unpublished after kMaxPolls polls ends the walk and is counted
+// in counts[5]: the batch is then refused and rolled back. Every lane returns the sum.
+__device__ int64_t look_back(const Ws &w, int64_t k) {
+    const int lane = threadIdx.x & 63;
+    int64_t sum = 0;
+    int polls = 0;
+    while (true) {
+        const int64_t t = k - lane;
+        uint64_t v = t >= 0 ? get_status(w.status + t) : kInc;
+        while (__ballot((v & ~kCountMask) == 0) != 0 && polls < kMaxPolls) {
+            ++polls;
+            __builtin_amdgcn_s_sleep(1);
+            if ((v & ~kCountMask) == 0)
+                v = get_status(w.status + t);
+        }
+        if (__ballot((v & ~kCountMask) == 0) != 0) {
+            if (lane == 0)
+                atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[5]), 1ULL);
+            return sum;
+        }
+        const uint64_t inc = __ballot((v & ~kCountMask) == kInc);
+        if (inc != 0) {
+            const int m = __builtin_ctzll(inc);      // nearest inclusive word
+            return sum + wave_sum(lane <= m ? (int64_t)(v & kCountMask) : 0);
+        }
+        sum += wave_sum((int64_t)(v & kCountMask));
+        k -= 64;
+    }
+}
+
+// The scan, in one pass with decoupled look-back. A workgroup claims the next tile of
+// kScanBlock records from counts[4] (so every tile it waits for belongs to a workgroup that is
+// already running), reads each record's entry position (from the workspace; from the map for a
+// record marked as a repeat, which also gives its last mark: the one read of the map after the
+// claim, so that later passes read the workspace in order), counts the first occurrences of
+// new ids with one ballot per wavefront and round, publishes the tile's count, looks back for
+// the count before the tile, and writes rank[i] = number of first occurrences of new ids
+// before record i. Records are read in rounds of kThreads consecutive ones (coalesced); the
+// rank order inside a tile is round, then wavefront, then lane, which is record order.
+__global__ __launch_bounds__(kThreads) void scan_kernel(const MapEntry *map, int64_t n, Ws w) {
+    __shared__ int64_t s_tile, s_before;
+    __shared__ int32_t s_cnt[kScanPer][kThreads / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid == 0)
+        s_tile = (int64_t)atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[4]), 1ULL);
+    __syncthreads();
+    const int64_t tile = s_tile;
+    const int64_t base = tile * kScanBlock;
+    // Every load is issued unconditionally from a clamped index, all rounds at once: a load
+    // under a branch would be waited for before the next round's loads are issued. A record
+    // without repeats needs only its position field and mark (the claim wrote both); a repeat
+    // also reads its entry index and the entry. The others read the tile's first record's
+    // index and map entry 0 instead: one cached line each.
+    const int64_t i0 = min(base, n - 1);
+    int32_t pv[kScanPer];
+    uint8_t dp[kScanPer];
+#pragma unroll
     for (int k = 0; k < kScanPer; ++k) {
-        const int64_t i = base + k * kThreads + threadIdx.x;
+        const int64_t i = min(base + k * kThreads + tid, n - 1);
+        pv[k] = w.posv[i];
+        dp[k] = w.dup[i];
+    }
+    int64_t sl[kScanPer];
+#pragma unroll
+    for (int k = 0; k < kScanPer; ++k)
+        sl[k] = w.slot[dp[k] ? min(base + k * kThreads + tid, n - 1) : i0];
+    MapEntry e[kScanPer];
+#pragma unroll
+    for (int k = 0; k < kScanPer; ++k)
+        e[k] = map[dp[k] && sl[k] >= 0 ? sl[k] : 0];
+    uint64_t bal[kScanPer];
+#pragma unroll
+    for (int k = 0; k < kScanPer; ++k) {
+        const int64_t i = base + k * kThreads + tid;
+        bool first = false;
         if (i < n) {
-            const int64_t s = w.slot[i];
-            int32_t pv = kNoPos;
-            if (s < 0) {
-                w.posv[i] = kNoPos;
-                w.last[i] = 0;
-            } else if (w.dup[i]) {
-                const MapEntry e = map[s];
-                pv = e.pos;
-                w.posv[i] = pv;
-                w.last[i] = e.aux == (int32_t)i ? 1 : 0;
+            if (dp[k]) {                                // a repeat always has an entry
+                w.posv[i] = e[k].pos;
+                w.last[i] = e[k].aux == (int32_t)i ? 1 : 0;
+                first = e[k].pos == -(3 + (int32_t)i);
             } else {
-                pv = w.posv[i];                   // as the claim wrote it: no repeats
+                first = pv[k] == -(3 + (int32_t)i);     // as the claim wrote it: no repeats
             }
-            v += pv == -(3 + (int32_t)i) ? 1 : 0;
+        }
+        bal[k] = __ballot(first);
+        if (lane == 0)
+            s_cnt[k][wave] = __popcll(bal[k]);
+    }
+    __syncthreads();
+    if (wave == 0) {
+        int64_t tot = 0;
+        for (int k = 0; k < kScanPer; ++k)
+            for (int v = 0; v < kThreads / 64; ++v)
+                tot += s_cnt[k][v];
+        int64_t before = 0;
+        if (tile == 0) {
+            if (lane == 0)
+                put_status(w.status, kInc | (uint64_t)tot);
+        } else {
+            if (lane == 0)
+                put_status(w.status + tile, kAgg | (uint64_t)tot);
+            before = look_back(w, tile - 1);
+            if (lane == 0)
+                put_status(w.status + tile, kInc | (uint64_t)(before + tot));
+        }
+        if (lane == 0) {
+            if (tile == w.blocks - 1)
+                w.counts[0] = before + tot;        // new ids in the batch
+            s_before = before;
         }
     }
-    const int32_t t = block_sum(v, lds);
-    if (threadIdx.x == 0)
-        w.partial[blockIdx.x] = t;
-}
-
-// Exclusive scan of the block partials in place (one workgroup); the total goes to counts[0].
-__global__ __launch_bounds__(kThreads) void scan_partials_kernel(Ws w) {
-    __shared__ int32_t s[kThreads];
-    __shared__ int64_t carry;
-    const int tid = threadIdx.x;
-    if (tid == 0)
-        carry = 0;
     __syncthreads();
-    for (int64_t b0 = 0; b0 < w.blocks; b0 += kThreads) {
-        const int64_t b = b0 + tid;
-        const int32_t x = b < w.blocks ? w.partial[b] : 0;
-        s[tid] = x;
-        __syncthreads();
-        for (int d = 1; d < kThreads; d <<= 1) {
-            const int32_t y = tid >= d ? s[tid - d] : 0;
-            __syncthreads();
-            s[tid] += y;
-            __syncthreads();
+    int64_t run = s_before;
+    const uint64_t below = (lane == 0) ? 0ULL : (~0ULL >> (64 - lane));
+#pragma unroll
+    for (int k = 0; k < kScanPer; ++k) {
+        int32_t waves_before = 0, round = 0;
+        for (int v = 0; v < kThreads / 64; ++v) {
+            const int32_t c = s_cnt[k][v];
+            waves_before += v < wave ? c : 0;
+            round += c;
         }
-        if (b < w.blocks)
-            w.partial[b] = (int32_t)(carry + s[tid] - x);
-        __syncthreads();
-        if (tid == kThreads - 1)
-            carry += s[tid];
-        __syncthreads();
-    }
-    if (tid == 0)
-        w.counts[0] = carry;
-}
-
-// rank[i] = number of first occurrences of new ids before record i.
-__global__ __launch_bounds__(kThreads) void scan_apply_kernel(int64_t n, Ws w) {
-    __shared__ int32_t s[kThreads];
-    const int tid = threadIdx.x;
-    const int64_t base = (int64_t)blockIdx.x * kScanBlock + (int64_t)tid * kScanPer;
-    int32_t f[kScanPer];
-    int32_t v = 0;
-#pragma unroll
-    for (int k = 0; k < kScanPer; ++k) {
-        const int64_t i = base + k;
-        f[k] = i < n ? first_new(w, i) : 0;
-        v += f[k];
-    }
-    s[tid] = v;
-    __syncthreads();
-    for (int d = 1; d < kThreads; d <<= 1) {
-        const int32_t y = tid >= d ? s[tid - d] : 0;
-        __syncthreads();
-        s[tid] += y;
-        __syncthreads();
-    }
-    int32_t run = w.partial[blockIdx.x] + s[tid] - v;
-#pragma unroll
-    for (int k = 0; k < kScanPer; ++k) {
-        const int64_t i = base + k;
+        const int64_t i = base + k * kThreads + tid;
         if (i < n)
-            w.rank[i] = run;
-        run += f[k];
+            w.rank[i] = (int32_t)(run + waves_before + __popcll(bal[k] & below));
+        run += round;
     }
 }
 
-// The batch fits: every id was placed and the new ids fit in the remaining capacity.
+// The batch fits: every id was placed, the new ids fit in the remaining capacity and no wait of
+// the scan reached its bound.
 __device__ __forceinline__ bool batch_fits(const Ws &w, int64_t n_old, int64_t capacity) {
-    return w.counts[2] == 0 && n_old + w.counts[0] <= capacity;
+    return w.counts[2] == 0 && w.counts[5] == 0 && n_old + w.counts[0] <= capacity;
 }
 
 __global__ void rollback_kernel(MapEntry *map, int64_t n, Ws w, int64_t n_old, int64_t capacity) {
@@ -611,8 +673,7 @@ int64_t upsert_workspace_bytes(int64_t n) {
     if (n <= 0 || n > kMaxBatch)            // the upsert rejects larger batches
         return 0;
     const int64_t blocks = (n + kScanBlock - 1) / kScanBlock;
-    return round_up(n * 8) + 2 * round_up(n * 4) + 2 * round_up(n) + round_up((blocks + 1) * 4) +
-           256;
+    return round_up(n * 8) + 2 * round_up(n * 4) + 2 * round_up(n) + round_up(blocks * 8) + 256;
 }
 
 int64_t *upsert_counts(void *workspace, int64_t n) { return carve(workspace, n).counts; }
@@ -622,7 +683,7 @@ hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *i
     const Ws w = carve(workspace, n);
     const uint64_t mask = (uint64_t)(n_groups - 1);
     hipLaunchKernelGGL(counts_init_kernel, dim3(grid_for(round_up(n > 0 ? n : 0) / 16, kThreads)),
-                       dim3(kThreads), 0, stream, w.counts, w.dup, n > 0 ? n : 0);
+                       dim3(kThreads), 0, stream, w, n > 0 ? n : 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || n <= 0)
         return e;
@@ -630,15 +691,8 @@ hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *i
                        stream, map, mask, ids, n, w);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
-    hipLaunchKernelGGL(scan_reduce_kernel, dim3((unsigned)w.blocks), dim3(kThreads), 0, stream,
-                       map, n, w);
-    if ((e = hipGetLastError()) != hipSuccess)
-        return e;
-    hipLaunchKernelGGL(scan_partials_kernel, dim3(1), dim3(kThreads), 0, stream, w);
-    if ((e = hipGetLastError()) != hipSuccess)
-        return e;
-    hipLaunchKernelGGL(scan_apply_kernel, dim3((unsigned)w.blocks), dim3(kThreads), 0, stream,
-                       n, w);
+    hipLaunchKernelGGL(scan_kernel, dim3((unsigned)w.blocks), dim3(kThreads), 0, stream, map, n,
+                       w);
     return hipGetLastError();
 }
 

@@ -146,6 +146,59 @@ __device__ __forceinline__ int64_t find_key(int64_t x, const int64_t *tab, int64
     return eq ? lo + cnt : -1;
 }
 
+// Two windows of W keys, gk[w0 ..) for x0 and gk[w1 ..) for x1 (both in bounds): all loads are
+// issued before the first compare, so the two reads cost one round trip.
+template <int W>
+__device__ __forceinline__ void scan_block_pair(const int64_t *gk, int64_t w0, int64_t x0,
+                                                int64_t w1, int64_t x1, int64_t &c0, bool &e0,
+                                                int64_t &c1, bool &e1) {
+    typedef long long pair_t __attribute__((ext_vector_type(2)));
+    pair_t k0[W / 2], k1[W / 2];
+#pragma unroll
+    for (int t = 0; t < W / 2; ++t) {
+        __builtin_memcpy(&k0[t], gk + w0 + 2 * t, sizeof(pair_t));
+        __builtin_memcpy(&k1[t], gk + w1 + 2 * t, sizeof(pair_t));
+    }
+#pragma unroll
+    for (int t = 0; t < W / 2; ++t) {
+        c0 += (k0[t].x < x0 ? 1 : 0) + (k0[t].y < x0 ? 1 : 0);
+        e0 |= (k0[t].x == x0) | (k0[t].y == x0);
+        c1 += (k1[t].x < x1 ? 1 : 0) + (k1[t].y < x1 ? 1 : 0);
+        e1 |= (k1[t].x == x1) | (k1[t].y == x1);
+    }
+}
+
+// Both lookups of one candidate (the same viewer's keys): r0 and r1 as find_key gives them, or
+// -1 when !valid. With a fence stride of 2 to 8 and K >= S, both LDS searches run first and
+// both key windows are then read together, every load from an index in bounds whatever the
+// lane's values: the window starts at w = clamp((g - 1) S + 1, 0, K - S). For g = 0 that is
+// the list's first S keys, none below x (x <= k[0]), so the count is 0 and an equal key can
+// only be k[0]: the same answer as the g = 0 rule of find_key. (Two windows of 16 keys would
+// hold 64 registers; two-lookup launches run two workgroups per CU, which needs at most 256.)
+__device__ __forceinline__ void find_key_pair(int64_t x0, int64_t x1, bool valid,
+                                              const int64_t *tab, int64_t M, int S,
+                                              const int64_t *gk, int64_t K, int64_t &r0,
+                                              int64_t &r1) {
+    if (S >= 2 && S <= 8 && K >= S) {
+        const int64_t g0 = count_less(tab, M, x0);
+        const int64_t g1 = count_less(tab, M, x1);
+        const int64_t w0 = clamp64((g0 - 1) * S + 1, K - S);
+        const int64_t w1 = clamp64((g1 - 1) * S + 1, K - S);
+        int64_t c0 = 0, c1 = 0;
+        bool e0 = false, e1 = false;
+        switch (S) {
+        case 2: scan_block_pair<2>(gk, w0, x0, w1, x1, c0, e0, c1, e1); break;
+        case 4: scan_block_pair<4>(gk, w0, x0, w1, x1, c0, e0, c1, e1); break;
+        default: scan_block_pair<8>(gk, w0, x0, w1, x1, c0, e0, c1, e1); break;
+        }
+        r0 = valid && e0 ? w0 + c0 : -1;
+        r1 = valid && e1 ? w1 + c1 : -1;
+        return;
+    }
+    r0 = valid ? find_key(x0, tab, M, S, gk, K) : -1;
+    r1 = valid ? find_key(x1, tab, M, S, gk, K) : -1;
+}
+
 // Fence stride for one segment: the smallest power of two whose fence count fits the LDS
 // table and is not much larger than the number of candidates that will use it.
 __device__ __forceinline__ int choose_stride(int64_t K, int64_t seg_len, int32_t cap,
@@ -420,13 +473,20 @@ __device__ __forceinline__ void resolve_tile(const JoinArgs &a, int64_t *src,
     src[tid] = valid ? c : -1;
     if (!valid && tid >= fresh)
         atomicAdd(s_invalid, 1u);
+    if constexpr (NL == 2) {
+        int64_t r[2];
+        find_key_pair(x0, x1, valid, s_tab, M, S, gk, K, r[0], r[1]);
 #pragma unroll
-    for (int l = 0; l < NL; ++l) {
+        for (int l = 0; l < 2; ++l) {
+            row[l][tid] = r[l] >= 0 ? kb + r[l] : -1;
+            a.hit[j * NL + l] = (int8_t)(r[l] >= 0 ? 1 : 0);
+        }
+    } else {
         int64_t r = -1;
         if (valid)
-            r = find_key(l == 0 ? x0 : x1, s_tab, M, S, gk, K);
-        row[l][tid] = r >= 0 ? kb + r : -1;
-        a.hit[j * NL + l] = (int8_t)(r >= 0 ? 1 : 0);
+            r = find_key(x0, s_tab, M, S, gk, K);
+        row[0][tid] = r >= 0 ? kb + r : -1;
+        a.hit[j] = (int8_t)(r >= 0 ? 1 : 0);
     }
 }
 

@@ -183,22 +183,34 @@ class JoinCase:
         self.alg_stored = algorithmic_bytes(torch, st, self.b, wd, we, n_lookups,
                                             P.cc_store_layout(store)[0])
 
-    def __call__(self):
+    def __call__(self, key_offsets=None):
         b, P = self.b, self.P
         if self.single:
             P.cc_join(self.store, b.cand_idx, b.keys, b.edge_rows, self.out, self.hit)
         else:
-            P.cc_join_batched(self.store, b.cand_offsets, b.cand_idx, b.key_offsets, b.keys,
+            P.cc_join_batched(self.store, b.cand_offsets, b.cand_idx,
+                              b.key_offsets if key_offsets is None else key_offsets, b.keys,
                               b.edge_rows, self.out, self.hit,
                               extra_keys=[b.actor] if self.n_lookups == 2 else None)
 
-    def entry(self, torch, flush, iters):
+    def entry(self, torch, flush, iters, floor=False):
         t_cold = time_launches(torch, self, max(10, iters // 2), flush=flush)
         t_warm = time_launches(torch, self, iters)
         e = {"entry": "cc_join" if self.single else "cc_join_batched",
              "viewers": self.b.n_viewers, "candidates": self.n, "keys": self.b.keys.numel(),
              "lookups": self.n_lookups}
         e.update(rates(self.n, self.alg, self.alg_stored, t_cold, t_warm))
+        if floor and not self.single:
+            # The same launch with every key list empty: no search and no edge rows, only the
+            # positions, author ids, doc rows and output rows. Its time bounds what any search
+            # could reach on this launch; `frac_at_floor` is the launch's algorithmic bytes
+            # over that time.
+            z = torch.zeros_like(self.b.key_offsets)
+            f_cold = time_launches(torch, lambda: self(z), max(10, iters // 2), flush=flush)
+            f_warm = time_launches(torch, lambda: self(z), iters)
+            e["no_keys_floor"] = {
+                "ms_median": f_cold["median"], "ms_median_warm": f_warm["median"],
+                "frac_at_floor": self.alg / (f_cold["median"] / 1e3) / 1e9 / PEAK_GBPS}
         return e
 
 
@@ -256,16 +268,33 @@ def reference_copy(torch, dev, flush):
     nbytes = 2 * (1 << 30)
     del src, dst
     torch.cuda.empty_cache()
-    return {"reference-copy": {"entry": "torch copy_ (PyTorch's own kernel)", "bytes": nbytes,
-                               "ms_median": tc["median"], "ms_median_warm": tw["median"],
-                               "gbps": nbytes / (tc["median"] / 1e3) / 1e9,
-                               "gbps_warm": nbytes / (tw["median"] / 1e3) / 1e9}}
+    res = {"reference-copy": {"entry": "torch copy_ (PyTorch's own kernel)", "bytes": nbytes,
+                              "ms_median": tc["median"], "ms_median_warm": tw["median"],
+                              "gbps": nbytes / (tc["median"] / 1e3) / 1e9,
+                              "gbps_warm": nbytes / (tw["median"] / 1e3) / 1e9}}
+    # Random 8-byte writes, as an ingestion batch's map update makes them: 25M values into a
+    # 6.4 GB table at random distinct places, with PyTorch's own scatter kernel.
+    n, m = 25_000_000, 800_000_000
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    table = torch.zeros(m, dtype=torch.int64, device=dev)
+    idx = torch.randperm(m, generator=g, device=dev)[:n].contiguous()
+    val = torch.arange(n, dtype=torch.int64, device=dev)
+    tw = time_launches(torch, lambda: table.index_copy_(0, idx, val), 10, flush=flush)
+    res["reference-random-writes"] = {
+        "entry": "torch index_copy_ (PyTorch's own kernel)", "writes": n, "bytes_each": 8,
+        "table_bytes": m * 8, "ms_median": tw["median"],
+        "writes_per_s": n / (tw["median"] / 1e3)}
+    del table, idx, val
+    torch.cuda.empty_cache()
+    return res
 
 
 def workload_entries(torch, P, W, dev, seed, flush, only=None, sorts=True, sorts_only=False,
-                     extra=False, cpu=None):
+                     extra=False, cpu=None, floors=True):
     """Full-size entries of every workload shape (or those in `only`). With `cpu`, also collect
-    the CPU oracle tasks of each shape into cpu[shape] (host copies of the inputs)."""
+    the CPU oracle tasks of each shape into cpu[shape] (host copies of the inputs). With
+    `floors`, workloads 3, 4 x64 and 5 also time their launch with empty key lists."""
     want = lambda k: only is None or k in only
     res = {}
 
@@ -319,7 +348,7 @@ def workload_entries(torch, P, W, dev, seed, flush, only=None, sorts=True, sorts
         for tag, reqs, L, single, iters in cases:
             c = JoinCase(torch, P, st, store, reqs, 128, 64, L, single, dev)
             if not sorts_only:
-                res[tag] = c.entry(torch, flush, iters)
+                res[tag] = c.entry(torch, flush, iters, floor=floors and tag in ("3", "4x64"))
             if cpu is not None and tag in ("2", "3", "4"):
                 src = reqs if tag != "2" else W.make_requests(st, r2, seed, n_viewers=16)
                 cpu[tag] = oracle_tasks(host[0], host[1], src if tag != "4" else reqs, L)
@@ -359,7 +388,7 @@ def workload_entries(torch, P, W, dev, seed, flush, only=None, sorts=True, sorts
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
         if not sorts_only:
-            res["5"] = c.entry(torch, flush, 40)
+            res["5"] = c.entry(torch, flush, 40, floor=floors)
         if sorts:
             res["5-sort"] = sort_entry(torch, P, c.b, 128, dev, "5", s.n_authors)
         P.cc_store_destroy(store)
@@ -740,7 +769,8 @@ def main(argv=None):
     if args.only_workloads or args.only_sorts:
         ids = [x.strip() for x in (args.only_workloads or args.only_sorts).split(",")]
         res = workload_entries(torch, P, W, dev, args.seed, flush, only=set(ids),
-                               sorts=bool(args.only_sorts), sorts_only=bool(args.only_sorts))
+                               sorts=bool(args.only_sorts), sorts_only=bool(args.only_sorts),
+                               floors=False)
         if args.calibration_copy:
             calibration_copy(torch, dev)
         key = "only_workloads" if args.only_workloads else "only_sorts"

@@ -400,12 +400,11 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(const MapEntry *map, int
     __syncthreads();
     const int64_t tile = s_tile;
     const int64_t base = tile * kScanBlock;
-    // Every load is issued unconditionally from a clamped index, all rounds at once: a load
-    // under a branch would be waited for before the next round's loads are issued. A record
-    // without repeats needs only its position field and mark (the claim wrote both); a repeat
-    // also reads its entry index and the entry. The others read the tile's first record's
-    // index and map entry 0 instead: one cached line each.
-    const int64_t i0 = min(base, n - 1);
+    // The position fields and marks of all rounds are loaded at once, from clamped indices (a
+    // load under a branch would be waited for before the next round's loads are issued). A
+    // record without repeats needs nothing else: the claim wrote its position field and last
+    // mark. A repeat reads its entry index and the entry (whose pos gives the id's first record
+    // and aux its last), in a branch that wavefronts without repeats skip.
     int32_t pv[kScanPer];
     uint8_t dp[kScanPer];
 #pragma unroll
@@ -414,28 +413,29 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(const MapEntry *map, int
         pv[k] = w.posv[i];
         dp[k] = w.dup[i];
     }
-    int64_t sl[kScanPer];
+    bool any_dup = false;
 #pragma unroll
     for (int k = 0; k < kScanPer; ++k)
-        sl[k] = w.slot[dp[k] ? min(base + k * kThreads + tid, n - 1) : i0];
-    MapEntry e[kScanPer];
+        any_dup |= dp[k] != 0;
+    uint32_t dup_first = 0;                       // bit k: round k's record is a repeat and first
+    if (__ballot(any_dup) != 0) {
 #pragma unroll
-    for (int k = 0; k < kScanPer; ++k)
-        e[k] = map[dp[k] && sl[k] >= 0 ? sl[k] : 0];
+        for (int k = 0; k < kScanPer; ++k) {
+            const int64_t i = base + k * kThreads + tid;
+            if (dp[k] && i < n) {
+                const MapEntry m = map[w.slot[i]];        // a repeat always has an entry
+                w.posv[i] = m.pos;
+                w.last[i] = m.aux == (int32_t)i ? 1 : 0;
+                dup_first |= (m.pos == -(3 + (int32_t)i) ? 1u : 0u) << k;
+            }
+        }
+    }
     uint64_t bal[kScanPer];
 #pragma unroll
     for (int k = 0; k < kScanPer; ++k) {
         const int64_t i = base + k * kThreads + tid;
-        bool first = false;
-        if (i < n) {
-            if (dp[k]) {                                // a repeat always has an entry
-                w.posv[i] = e[k].pos;
-                w.last[i] = e[k].aux == (int32_t)i ? 1 : 0;
-                first = e[k].pos == -(3 + (int32_t)i);
-            } else {
-                first = pv[k] == -(3 + (int32_t)i);     // as the claim wrote it: no repeats
-            }
-        }
+        const bool first = i < n && (dp[k] ? ((dup_first >> k) & 1u) != 0
+                                            : pv[k] == -(3 + (int32_t)i));
         bal[k] = __ballot(first);
         if (lane == 0)
             s_cnt[k][wave] = __popcll(bal[k]);
@@ -716,7 +716,9 @@ hipError_t launch_upsert_finish(MapEntry *map, int64_t n, void *workspace, int64
                        n, w, n_old, capacity);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
-    hipLaunchKernelGGL(rollback_kernel, dim3(grid_for(n, kThreads)), dim3(kThreads), 0, stream,
+    // The rollback runs only for a batch that does not fit; otherwise every workgroup returns at
+    // once, so a small grid (grid-stride over the records) keeps that no-op launch short.
+    hipLaunchKernelGGL(rollback_kernel, dim3(grid_for(n, kThreads * 64)), dim3(kThreads), 0, stream,
                        map, n, w, n_old, capacity);
     return hipGetLastError();
 }

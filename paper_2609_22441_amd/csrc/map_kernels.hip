@@ -39,8 +39,14 @@ namespace ccj {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kScanPer = 32;                         // records per thread in the scan
-constexpr int kScanBlock = kThreads * kScanPer;      // records per scan tile
+// Records per thread in a scan tile: large batches take big tiles (fewer tiles to chain), small
+// ones small tiles (more workgroups, shorter per-tile chains).
+constexpr int kScanPerLarge = 32;
+constexpr int kScanPerSmall = 4;
+constexpr int64_t kScanLargeFrom = 1 << 22;        // records
+__host__ __device__ inline int scan_per(int64_t n) {
+    return n >= kScanLargeFrom ? kScanPerLarge : kScanPerSmall;
+}
 constexpr uint64_t kMaxProbeGroups = 64;
 constexpr int kMaxPolls = 1 << 16;                  // bound on a repeat's wait for its creator
 // counts[]: new ids, rejected records, unplaced ids, author ids wider than 32 bits, the scan's
@@ -77,7 +83,8 @@ __device__ __forceinline__ int64_t global_id() {
 //   dup    1 when another record of the batch has record i's id. The claim writes posv and
 //          last as they are for an id without repeats (and kNoPos, 0 for a record without an
 //          entry); the scan reads the map entry only for the records marked here.
-//   status the scan's look-back word of each tile of kScanBlock records (cleared per batch)
+//   status the scan's look-back word of each tile of kThreads * scan_per(n) records (cleared
+//          per batch; sized for the small tiles)
 struct Ws {
     int64_t *slot;
     int32_t *rank;
@@ -94,7 +101,7 @@ __host__ __device__ int64_t round_up(int64_t x) { return (x + 255) & ~int64_t(25
 Ws carve(void *workspace, int64_t n) {
     uint8_t *w = static_cast<uint8_t *>(workspace);
     Ws s;
-    s.blocks = (n + kScanBlock - 1) / kScanBlock;
+    s.blocks = (n + kThreads * scan_per(n) - 1) / (kThreads * scan_per(n));
     s.slot = reinterpret_cast<int64_t *>(w);
     w += round_up(n * 8);
     s.rank = reinterpret_cast<int32_t *>(w);
@@ -106,7 +113,7 @@ Ws carve(void *workspace, int64_t n) {
     s.dup = w;
     w += round_up(n);
     s.status = reinterpret_cast<uint64_t *>(w);
-    w += round_up(s.blocks * 8);
+    w += round_up((n + kThreads * kScanPerSmall - 1) / (kThreads * kScanPerSmall) * 8);
     s.counts = reinterpret_cast<int64_t *>(w);
     return s;
 }
@@ -383,7 +390,7 @@ __device__ int64_t look_back(const Ws &w, int64_t k) {
 }
 
 // The scan, in one pass with decoupled look-back. A workgroup claims the next tile of
-// kScanBlock records from counts[4] (so every tile it waits for belongs to a workgroup that is
+// kThreads * PER records from counts[4] (so every tile it waits for belongs to a workgroup that is
 // already running), reads each record's entry position (from the workspace; from the map for a
 // record marked as a repeat, which also gives its last mark: the one read of the map after the
 // claim, so that later passes read the workspace in order), counts the first occurrences of
@@ -391,51 +398,71 @@ __device__ int64_t look_back(const Ws &w, int64_t k) {
 // the count before the tile, and writes rank[i] = number of first occurrences of new ids
 // before record i. Records are read in rounds of kThreads consecutive ones (coalesced); the
 // rank order inside a tile is round, then wavefront, then lane, which is record order.
+template <int PER>
 __global__ __launch_bounds__(kThreads) void scan_kernel(const MapEntry *map, int64_t n, Ws w) {
     __shared__ int64_t s_tile, s_before;
-    __shared__ int32_t s_cnt[kScanPer][kThreads / 64];
+    __shared__ int32_t s_cnt[PER][kThreads / 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     if (tid == 0)
         s_tile = (int64_t)atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[4]), 1ULL);
     __syncthreads();
     const int64_t tile = s_tile;
-    const int64_t base = tile * kScanBlock;
+    const int64_t base = tile * (kThreads * PER);
     // The position fields and marks of all rounds are loaded at once, from clamped indices (a
     // load under a branch would be waited for before the next round's loads are issued). A
     // record without repeats needs nothing else: the claim wrote its position field and last
     // mark. A repeat reads its entry index and the entry (whose pos gives the id's first record
     // and aux its last), in a branch that wavefronts without repeats skip.
-    int32_t pv[kScanPer];
-    uint8_t dp[kScanPer];
+    static_assert(PER <= 32, "one bit per round in a 32-bit mask");
+    int32_t pv[PER];
+    uint32_t dup = 0;                             // bit k: round k's record is a repeat
 #pragma unroll
-    for (int k = 0; k < kScanPer; ++k) {
+    for (int k = 0; k < PER; ++k) {
         const int64_t i = min(base + k * kThreads + tid, n - 1);
         pv[k] = w.posv[i];
-        dp[k] = w.dup[i];
+        dup |= (w.dup[i] && base + k * kThreads + tid < n ? 1u : 0u) << k;
     }
-    bool any_dup = false;
+    uint32_t dup_first = 0;                       // bit k: ... and the first of its id
+    if (__ballot(dup != 0) != 0) {
+        // kDupRounds rounds at a time: their entry indices, then their entries, each group of
+        // loads issued together (from clamped indices: the tile's first record and entry 0
+        // for records that are not repeats).
+        constexpr int kDupRounds = PER < 8 ? PER : 8;
+        static_assert(PER % kDupRounds == 0, "whole groups of rounds");
+        const int64_t i0 = min(base, n - 1);
+#pragma unroll 1
+        for (int c = 0; c < PER; c += kDupRounds) {
+            int64_t sl[kDupRounds];
 #pragma unroll
-    for (int k = 0; k < kScanPer; ++k)
-        any_dup |= dp[k] != 0;
-    uint32_t dup_first = 0;                       // bit k: round k's record is a repeat and first
-    if (__ballot(any_dup) != 0) {
+            for (int u = 0; u < kDupRounds; ++u) {
+                const bool d = (dup >> (c + u)) & 1u;
+                sl[u] = w.slot[d ? base + (c + u) * kThreads + tid : i0];
+            }
+            int32_t ep[kDupRounds], ea[kDupRounds];
 #pragma unroll
-        for (int k = 0; k < kScanPer; ++k) {
-            const int64_t i = base + k * kThreads + tid;
-            if (dp[k] && i < n) {
-                const MapEntry m = map[w.slot[i]];        // a repeat always has an entry
-                w.posv[i] = m.pos;
-                w.last[i] = m.aux == (int32_t)i ? 1 : 0;
-                dup_first |= (m.pos == -(3 + (int32_t)i) ? 1u : 0u) << k;
+            for (int u = 0; u < kDupRounds; ++u) {
+                const bool d = (dup >> (c + u)) & 1u;
+                const MapEntry &m = map[d && sl[u] >= 0 ? sl[u] : 0];
+                ep[u] = m.pos;
+                ea[u] = m.aux;
+            }
+#pragma unroll
+            for (int u = 0; u < kDupRounds; ++u) {
+                const int64_t i = base + (c + u) * kThreads + tid;
+                if ((dup >> (c + u)) & 1u) {            // a repeat always has an entry
+                    w.posv[i] = ep[u];
+                    w.last[i] = ea[u] == (int32_t)i ? 1 : 0;
+                    dup_first |= (ep[u] == -(3 + (int32_t)i) ? 1u : 0u) << (c + u);
+                }
             }
         }
     }
-    uint64_t bal[kScanPer];
+    uint64_t bal[PER];
 #pragma unroll
-    for (int k = 0; k < kScanPer; ++k) {
+    for (int k = 0; k < PER; ++k) {
         const int64_t i = base + k * kThreads + tid;
-        const bool first = i < n && (dp[k] ? ((dup_first >> k) & 1u) != 0
-                                            : pv[k] == -(3 + (int32_t)i));
+        const bool first = i < n && (((dup >> k) & 1u) ? ((dup_first >> k) & 1u) != 0
+                                                        : pv[k] == -(3 + (int32_t)i));
         bal[k] = __ballot(first);
         if (lane == 0)
             s_cnt[k][wave] = __popcll(bal[k]);
@@ -443,7 +470,7 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(const MapEntry *map, int
     __syncthreads();
     if (wave == 0) {
         int64_t tot = 0;
-        for (int k = 0; k < kScanPer; ++k)
+        for (int k = 0; k < PER; ++k)
             for (int v = 0; v < kThreads / 64; ++v)
                 tot += s_cnt[k][v];
         int64_t before = 0;
@@ -467,7 +494,7 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(const MapEntry *map, int
     int64_t run = s_before;
     const uint64_t below = (lane == 0) ? 0ULL : (~0ULL >> (64 - lane));
 #pragma unroll
-    for (int k = 0; k < kScanPer; ++k) {
+    for (int k = 0; k < PER; ++k) {
         int32_t waves_before = 0, round = 0;
         for (int v = 0; v < kThreads / 64; ++v) {
             const int32_t c = s_cnt[k][v];
@@ -672,7 +699,7 @@ hipError_t launch_resolve(const MapEntry *map, int64_t n_groups, const int64_t *
 int64_t upsert_workspace_bytes(int64_t n) {
     if (n <= 0 || n > kMaxBatch)            // the upsert rejects larger batches
         return 0;
-    const int64_t blocks = (n + kScanBlock - 1) / kScanBlock;
+    const int64_t blocks = (n + kThreads * kScanPerSmall - 1) / (kThreads * kScanPerSmall);
     return round_up(n * 8) + 2 * round_up(n * 4) + 2 * round_up(n) + round_up(blocks * 8) + 256;
 }
 
@@ -691,8 +718,12 @@ hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *i
                        stream, map, mask, ids, n, w);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
-    hipLaunchKernelGGL(scan_kernel, dim3((unsigned)w.blocks), dim3(kThreads), 0, stream, map, n,
-                       w);
+    if (scan_per(n) == kScanPerLarge)
+        hipLaunchKernelGGL(scan_kernel<kScanPerLarge>, dim3((unsigned)w.blocks), dim3(kThreads), 0,
+                           stream, map, n, w);
+    else
+        hipLaunchKernelGGL(scan_kernel<kScanPerSmall>, dim3((unsigned)w.blocks), dim3(kThreads), 0,
+                           stream, map, n, w);
     return hipGetLastError();
 }
 

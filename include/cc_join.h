@@ -53,8 +53,11 @@ typedef enum cc_status {
     CC_ERR_UNSORTED_KEYS = 4,      /* only from cc_validate_keys                            */
     CC_ERR_NOT_SUPPORTED = 5,      /* no usable gfx950 device, or a store without an id map */
     CC_ERR_STORE_FULL = 6,         /* an ingestion batch does not fit; the store is unchanged */
-    CC_ERR_TOO_LARGE = 7           /* a size exceeds the fixed scratch of an allocation-free
+    CC_ERR_TOO_LARGE = 7,          /* a size exceeds the fixed scratch of an allocation-free
                                       entry point; nothing enqueued                          */
+    CC_ERR_TIMEOUT = 8             /* a bounded wait between the workgroups of an ingestion
+                                      batch gave up; the batch was rolled back, the store is
+                                      unchanged                                              */
 } cc_status;
 
 /* Where cc_store_create reads its source arrays from. */
@@ -301,9 +304,21 @@ CC_API cc_status cc_store_create_indexed(cc_store **out_store, int64_t capacity,
  * fit in the remaining capacity, or an id cannot be placed within the map's probe
  * limit (64 groups; not expected below load 1/2), the batch is undone and CC_ERR_STORE_FULL is
  * returned with the store unchanged. Errors: CC_ERR_INVALID_ARGUMENT, CC_ERR_NOT_SUPPORTED,
- * CC_ERR_STORE_FULL, CC_ERR_DEVICE (also, with the store unchanged, if a bounded wait between
- * the workgroups of the batch's scan gives up; not expected).
+ * CC_ERR_STORE_FULL, CC_ERR_TIMEOUT (a bounded device-side wait gave up, see
+ * cc_set_ingestion_wait_limit; the batch is undone and the store unchanged), CC_ERR_DEVICE.
  */
+/*
+ * cc_set_ingestion_wait_limit -- the bound, in polls (each about a microsecond), on every wait
+ * inside an ingestion batch: a record waiting for the store that put its id into the map in
+ * the same batch, and a scan tile waiting for the counts of earlier tiles. Those waits are on
+ * work of running workgroups and end within microseconds; the bound keeps every wave's exit
+ * certain. A batch in which a wait gives up is rolled back and cc_store_upsert returns
+ * CC_ERR_TIMEOUT with the store unchanged. For tests of that path: 0 makes every such wait give
+ * up at once (a batch that repeats an id new to the store is then always refused). polls < 0
+ * restores the default (65,536). Process-wide; applies to batches enqueued afterwards.
+ * Returns CC_OK.
+ */
+CC_API cc_status cc_set_ingestion_wait_limit(int32_t polls);
 /* Workspace bytes cc_store_upsert needs for n_records; 0 when n_records <= 0 or > 2^30 (a
  * batch the upsert rejects). */
 CC_API int64_t cc_upsert_workspace_bytes(int64_t n_records);

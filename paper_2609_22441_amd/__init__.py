@@ -14,6 +14,6 @@ from .binding import (  # noqa: F401
     cc_store_create, cc_store_destroy, cc_store_info, cc_store_invalid_count,
     cc_store_reset_invalid_count, cc_validate_keys, lib, LIB_PATH, EXPORTS,
     cc_store_create_indexed, cc_upsert_workspace_bytes, cc_store_upsert, cc_resolve_ids,
-    cc_store_read, cc_store_layout,
-    CC_ERR_STORE_FULL, CC_ERR_TOO_LARGE,
+    cc_store_read, cc_store_layout, cc_set_ingestion_wait_limit,
+    CC_ERR_STORE_FULL, CC_ERR_TOO_LARGE, CC_ERR_TIMEOUT,
 )

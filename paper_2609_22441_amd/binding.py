@@ -20,7 +20,8 @@ EXPORTS = (
     "cc_store_reset_invalid_count", "cc_join", "cc_join_batched", "cc_join_batched_tuned",
     "cc_join_batched_padded", "cc_sort_workspace_bytes", "cc_sort_affinity",
     "cc_sort_affinity_method", "cc_sort_affinity_noalloc",
-    "cc_store_create_indexed", "cc_upsert_workspace_bytes", "cc_store_upsert", "cc_store_read",
+    "cc_store_create_indexed", "cc_set_ingestion_wait_limit", "cc_upsert_workspace_bytes",
+    "cc_store_upsert", "cc_store_read",
     "cc_store_layout",
     "cc_resolve_ids",
     "cc_validate_keys", "cc_status_string", "cc_last_device_error",
@@ -28,6 +29,7 @@ EXPORTS = (
 
 CC_OK, CC_ERR_INVALID_ARGUMENT, CC_ERR_OUT_OF_MEMORY, CC_ERR_DEVICE = 0, 1, 2, 3
 CC_ERR_UNSORTED_KEYS, CC_ERR_NOT_SUPPORTED, CC_ERR_STORE_FULL, CC_ERR_TOO_LARGE = 4, 5, 6, 7
+CC_ERR_TIMEOUT = 8
 SORT_NOALLOC_MAX_RECORDS, SORT_NOALLOC_MAX_VIEWERS = 1 << 20, 1 << 16
 CC_SRC_HOST, CC_SRC_DEVICE = 1, 2
 
@@ -78,6 +80,7 @@ def lib():
                                         vp],
             "cc_sort_affinity_noalloc": [i32, vp, vp, vp, i32, i64, i64, vp, vp, vp],
             "cc_store_create_indexed": [ctypes.POINTER(vp), i64, i32, vp],
+            "cc_set_ingestion_wait_limit": [i32],
             "cc_store_upsert": [vp, i64, vp, vp, vp, vp, i64, P64, P64, vp],
             "cc_resolve_ids": [vp, vp, i64, vp, vp],
             "cc_store_read": [vp, i64, i64, vp, vp, vp],
@@ -292,13 +295,21 @@ def cc_store_create_indexed(capacity: int, doc_row_bytes: int, stream=None) -> i
     return h.value
 
 
+def cc_set_ingestion_wait_limit(polls: int) -> None:
+    """Bound (in polls) on every device-side wait of an ingestion batch; a batch in which one
+    gives up is rolled back and cc_store_upsert raises CCError(CC_ERR_TIMEOUT). 0 makes every
+    such wait give up at once; a negative value restores the default. Process-wide."""
+    _check(lib().cc_set_ingestion_wait_limit(int(polls)), "cc_set_ingestion_wait_limit")
+
+
 def cc_upsert_workspace_bytes(n_records: int) -> int:
     return lib().cc_upsert_workspace_bytes(n_records)
 
 
 def cc_store_upsert(store: int, doc_ids, author_ids, doc_rows, workspace, stream=None):
     """Apply one ingestion batch (§6.2); returns (n_new, n_rejected). Synchronises the stream.
-    Raises CCError with status CC_ERR_STORE_FULL (store unchanged) when the batch does not fit."""
+    Raises CCError with status CC_ERR_STORE_FULL (store unchanged) when the batch does not fit,
+    CC_ERR_TIMEOUT (store unchanged) when a bounded device-side wait gave up."""
     n = doc_ids.numel()
     pi = _arr(doc_ids, "doc_ids", _i64())
     pa = _arr(author_ids, "author_ids", _i64(), n)

@@ -3,6 +3,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <atomic>
 #include <mutex>
 #include <new>
 
@@ -399,6 +400,14 @@ cc_status cc_store_create_indexed(cc_store **out_store, int64_t capacity, int32_
     return CC_OK;
 }
 
+// Bound on the device-side waits of an ingestion batch (cc_set_ingestion_wait_limit).
+static std::atomic<int32_t> g_wait_polls{ccj::kDefaultWaitPolls};
+
+cc_status cc_set_ingestion_wait_limit(int32_t polls) {
+    g_wait_polls.store(polls < 0 ? ccj::kDefaultWaitPolls : polls, std::memory_order_relaxed);
+    return CC_OK;
+}
+
 int64_t cc_upsert_workspace_bytes(int64_t n_records) {
     return ccj::upsert_workspace_bytes(n_records);
 }
@@ -433,7 +442,8 @@ cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc
     if (guard.error() != hipSuccess)
         return device_error(guard.error());
     hipError_t e = ccj::launch_upsert_claim(store->d_map, store->map_groups, doc_ids, n_records,
-                                            workspace, stream);
+                                            workspace,
+                                            g_wait_polls.load(std::memory_order_relaxed), stream);
     if (e == hipSuccess)
         e = ccj::launch_upsert_finish(store->d_map, n_records, workspace, store->n_docs,
                                       store->capacity, author_ids, doc_rows,
@@ -449,7 +459,7 @@ cc_status cc_store_upsert(cc_store *store, int64_t n_records, const int64_t *doc
         return device_error(e);
     const int64_t fresh = counts[0], rejected = counts[1], unplaced = counts[2];
     if (counts[5] > 0)
-        return CC_ERR_DEVICE;                // a bounded device wait gave up; rolled back
+        return CC_ERR_TIMEOUT;               // a bounded device wait gave up; rolled back
     if (unplaced > 0 || store->n_docs + fresh > store->capacity)
         return CC_ERR_STORE_FULL;            // rolled back on the device: the store is unchanged
     store->n_docs += fresh;
@@ -767,6 +777,7 @@ const char *cc_status_string(int status) {
     case CC_ERR_NOT_SUPPORTED: return "CC_ERR_NOT_SUPPORTED";
     case CC_ERR_STORE_FULL: return "CC_ERR_STORE_FULL";
     case CC_ERR_TOO_LARGE: return "CC_ERR_TOO_LARGE";
+    case CC_ERR_TIMEOUT: return "CC_ERR_TIMEOUT";
     }
     return "CC_UNKNOWN_STATUS";
 }

@@ -130,15 +130,16 @@ hipError_t launch_resolve(const MapEntry *map, int64_t n_groups, const int64_t *
 
 // Ingestion batch in two launches: claim (map entries for every id, first/last occurrence,
 // ranks of the new ids, and kUpsertCounts counts at upsert_counts(ws, n): n_new, n_rejected,
-// n_unplaced, n_wide_authors, the scan's tile counter, scan waits that reached their bound),
+// n_unplaced, n_wide_authors, the scan's tile counter, waits that reached their bound),
 // then finish: when the batch fits (nothing unplaced, no bounded wait given up and
 // n_old + n_new <= capacity) scatter the rows and commit the map, otherwise roll the claim
 // back. The decision is taken on the device from the counts.
 constexpr int kUpsertCounts = 6;
+constexpr int32_t kDefaultWaitPolls = 1 << 16;   // bound on each device-side wait of a batch
 int64_t upsert_workspace_bytes(int64_t n);
 int64_t *upsert_counts(void *workspace, int64_t n);
 hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *ids, int64_t n,
-                               void *workspace, hipStream_t stream);
+                               void *workspace, int32_t max_polls, hipStream_t stream);
 hipError_t launch_upsert_finish(MapEntry *map, int64_t n, void *workspace, int64_t n_old,
                                 int64_t capacity, const int64_t *author_in, const void *rows_in,
                                 int32_t row_bytes, int64_t *author, int32_t *author32,

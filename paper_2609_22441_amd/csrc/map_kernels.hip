@@ -48,9 +48,8 @@ __host__ __device__ inline int scan_per(int64_t n) {
     return n >= kScanLargeFrom ? kScanPerLarge : kScanPerSmall;
 }
 constexpr uint64_t kMaxProbeGroups = 64;
-constexpr int kMaxPolls = 1 << 16;                  // bound on a repeat's wait for its creator
 // counts[]: new ids, rejected records, unplaced ids, author ids wider than 32 bits, the scan's
-// tile counter, scan waits that reached their bound.
+// tile counter, waits (of the claim or the scan) that reached their bound of max_polls polls.
 constexpr int kCounts = kUpsertCounts;
 static_assert(kCounts * 8 <= 256, "the counts live in the workspace's last 256 bytes");
 
@@ -206,7 +205,7 @@ __global__ void counts_init_kernel(Ws w, int64_t n) {
 // key) and one store; a second swap for the position word would be a second round trip past L2.
 __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t mask,
                                                          const int64_t *__restrict__ ids,
-                                                         int64_t n, Ws w) {
+                                                         int64_t n, Ws w, int32_t max_polls) {
     const int lane = threadIdx.x & 63;
     const int sub = lane & (kGroup - 1);
     const int quad0 = lane & ~(kGroup - 1);
@@ -299,19 +298,23 @@ __global__ __launch_bounds__(kThreads) void claim_kernel(MapEntry *map, uint64_t
             } else {
                 // A repeat of an id that another record of this batch put into the entry: wait
                 // until that record's store is visible (its values replace the idle ones; the
-                // wait is bounded, and the creator stores right after its swap), then fold this
-                // record in with two maxima. The first repeat to read sees the creator's values,
-                // so every record of a repeated id ends up marked.
+                // creator stores right after its swap), then fold this record in with two
+                // maxima. The first repeat to read sees the creator's values, so every record
+                // of a repeated id ends up marked. A wait that reaches its bound is counted in
+                // counts[5]: the first and last record may then be wrong, and the batch is
+                // refused and rolled back (pending entries are freed whatever they hold).
                 const unsigned long long idle =
                     (unsigned long long)(uint32_t)kNoPos | ((unsigned long long)(uint32_t)-1 << 32);
                 unsigned long long old = idle;
-                for (int polls = 0; polls < kMaxPolls; ++polls) {
+                for (int polls = 0; polls < max_polls; ++polls) {
                     old = __hip_atomic_load(reinterpret_cast<unsigned long long *>(&map[found].pos),
                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     if (old != idle)
                         break;
                     __builtin_amdgcn_s_sleep(1);
                 }
+                if (old == idle)
+                    atomicAdd(reinterpret_cast<unsigned long long *>(&w.counts[5]), 1ULL);
                 w.posv[i] = -(3 + (int32_t)i);
                 w.last[i] = 1;
                 atomicMax(&map[found].pos, -(3 + (int32_t)i));
@@ -359,16 +362,16 @@ __device__ __forceinline__ int64_t wave_sum(int64_t x) {
 // added, else all 64 and the window moves down. Tiles below 0 read as inclusive zeros (tile 0
 // itself always publishes an inclusive word). Each tile waits only for tiles claimed before
 // it, by workgroups that publish their own count before they look back, so a wait lasts about
-// one tile's loads. A word still unpublished after kMaxPolls polls ends the walk and is counted
+// one tile's loads. A word still unpublished after max_polls polls ends the walk and is counted
 // in counts[5]: the batch is then refused and rolled back. Every lane returns the sum.
-__device__ int64_t look_back(const Ws &w, int64_t k) {
+__device__ int64_t look_back(const Ws &w, int64_t k, int32_t max_polls) {
     const int lane = threadIdx.x & 63;
     int64_t sum = 0;
     int polls = 0;
     while (true) {
         const int64_t t = k - lane;
         uint64_t v = t >= 0 ? get_status(w.status + t) : kInc;
-        while (__ballot((v & ~kCountMask) == 0) != 0 && polls < kMaxPolls) {
+        while (__ballot((v & ~kCountMask) == 0) != 0 && polls < max_polls) {
             ++polls;
             __builtin_amdgcn_s_sleep(1);
             if ((v & ~kCountMask) == 0)
@@ -399,7 +402,8 @@ __device__ int64_t look_back(const Ws &w, int64_t k) {
 // before record i. Records are read in rounds of kThreads consecutive ones (coalesced); the
 // rank order inside a tile is round, then wavefront, then lane, which is record order.
 template <int PER>
-__global__ __launch_bounds__(kThreads) void scan_kernel(const MapEntry *map, int64_t n, Ws w) {
+__global__ __launch_bounds__(kThreads) void scan_kernel(const MapEntry *map, int64_t n, Ws w,
+                                                        int32_t max_polls) {
     __shared__ int64_t s_tile, s_before;
     __shared__ int32_t s_cnt[PER][kThreads / 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -480,7 +484,7 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(const MapEntry *map, int
         } else {
             if (lane == 0)
                 put_status(w.status + tile, kAgg | (uint64_t)tot);
-            before = look_back(w, tile - 1);
+            before = look_back(w, tile - 1, max_polls);
             if (lane == 0)
                 put_status(w.status + tile, kInc | (uint64_t)(before + tot));
         }
@@ -706,7 +710,7 @@ int64_t upsert_workspace_bytes(int64_t n) {
 int64_t *upsert_counts(void *workspace, int64_t n) { return carve(workspace, n).counts; }
 
 hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *ids, int64_t n,
-                               void *workspace, hipStream_t stream) {
+                               void *workspace, int32_t max_polls, hipStream_t stream) {
     const Ws w = carve(workspace, n);
     const uint64_t mask = (uint64_t)(n_groups - 1);
     hipLaunchKernelGGL(counts_init_kernel, dim3(grid_for(round_up(n > 0 ? n : 0) / 16, kThreads)),
@@ -715,15 +719,15 @@ hipError_t launch_upsert_claim(MapEntry *map, int64_t n_groups, const int64_t *i
     if (e != hipSuccess || n <= 0)
         return e;
     hipLaunchKernelGGL(claim_kernel, dim3(grid_for(n * kGroup, kThreads)), dim3(kThreads), 0,
-                       stream, map, mask, ids, n, w);
+                       stream, map, mask, ids, n, w, max_polls);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
     if (scan_per(n) == kScanPerLarge)
         hipLaunchKernelGGL(scan_kernel<kScanPerLarge>, dim3((unsigned)w.blocks), dim3(kThreads), 0,
-                           stream, map, n, w);
+                           stream, map, n, w, max_polls);
     else
         hipLaunchKernelGGL(scan_kernel<kScanPerSmall>, dim3((unsigned)w.blocks), dim3(kThreads), 0,
-                           stream, map, n, w);
+                           stream, map, n, w, max_polls);
     return hipGetLastError();
 }
 

@@ -34,6 +34,7 @@ def test_status_strings():
     assert P.cc_status_string(1) == "CC_ERR_INVALID_ARGUMENT"
     assert P.cc_status_string(5) == "CC_ERR_NOT_SUPPORTED"
     assert P.cc_status_string(6) == "CC_ERR_STORE_FULL"
+    assert P.cc_status_string(8) == "CC_ERR_TIMEOUT"
     assert P.cc_status_string(99) == "CC_UNKNOWN_STATUS"
     assert P.cc_last_device_error() == 0
 
@@ -203,6 +204,8 @@ def test_upsert_and_resolve_reject_bad_arguments():
     n = ctypes.c_int64()
     assert lib.cc_store_upsert(None, 1, 8, 8, 16, 16, 1 << 20, ctypes.byref(n), None, None) == 1
     assert lib.cc_resolve_ids(None, 8, 1, 8, None) == 1
+    assert lib.cc_set_ingestion_wait_limit(0) == 0    # no device touched
+    assert lib.cc_set_ingestion_wait_limit(-1) == 0   # back to the default
     assert lib.cc_upsert_workspace_bytes(0) == 0
     assert lib.cc_upsert_workspace_bytes(-3) == 0
     assert lib.cc_upsert_workspace_bytes(1000) >= 12 * 1000

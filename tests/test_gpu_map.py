@@ -416,6 +416,44 @@ def _colliding_ids(n, groups, home):
     return out
 
 
+def test_wait_bound_refuses_the_batch_and_keeps_the_store():
+    """A batch in which a device-side wait reaches its bound is rolled back: CC_ERR_TIMEOUT,
+    and positions, rows and the map stay as they were. The bound is forced from the host: with
+    zero polls, a record that repeats an id new to the store gives up at once on the record
+    that put the id into the map (deterministic for any batch with such a repeat). With the
+    default bound restored, the same batch applies and equals the oracle's replay."""
+    cap, rb = 1000, 32
+    idx = DeviceIndex(cap, rb)
+    g = torch.Generator().manual_seed(11)
+    rows = lambda n: torch.randint(0, 256, (n, rb), generator=g, dtype=torch.int64).to(torch.uint8)
+    base = [7919 * k for k in range(1, 51)]
+    note("wait bound: base batch")
+    assert idx.upsert(base, list(range(50)), rows(50)) == (50, 0)
+    idx.check_state("after the base batch")
+    # a stored id twice, new ids 111 and 222 twice each, new id 333 once
+    batch = [base[3], 111, 222, 111, 333, 222, base[3]]
+    authors = [5, 6, 7, 8, 9, 10, 11]
+    r = rows(len(batch))
+    ws = torch.empty(P.cc_upsert_workspace_bytes(len(batch)), dtype=torch.uint8, device=DEV)
+    note("wait bound: zero polls")
+    P.cc_set_ingestion_wait_limit(0)
+    try:
+        with pytest.raises(P.CCError) as e:
+            P.cc_store_upsert(idx.store, torch.tensor(batch, device=DEV),
+                              torch.tensor(authors, device=DEV), r.to(DEV), ws)
+        assert e.value.status == P.CC_ERR_TIMEOUT
+    finally:
+        P.cc_set_ingestion_wait_limit(-1)
+    idx.check_state("after the refused batch")
+    pos = idx.resolve(base + [111, 222, 333], "after the refused batch")
+    assert pos[:50].tolist() == list(range(50)) and (pos[50:] == -1).all()
+    note("wait bound: default restored")
+    assert idx.upsert(batch, authors, r) == (3, 0)
+    idx.check_state("after the applied batch")
+    idx.resolve(base + [111, 222, 333, 444], "after the applied batch")
+    idx.close()
+
+
 def test_probe_limit_refuses_the_batch_and_keeps_the_store():
     """An id that cannot be placed within the map's 64 probe groups (256 entries) fails its
     batch with CC_ERR_STORE_FULL and the store stays as it was: positions, rows and the map.

@@ -399,6 +399,10 @@ CC_API cc_status cc_sort_affinity(int32_t n_viewers, const int64_t *key_offsets,
  *   CC_SORT_RADIX  least-significant-digit radix passes of up to 9 bits over the span of the
  *                  call's keys (decoupled look-back between a viewer's tiles), then one gather
  *                  of the rows. Moves fewer bytes per record: the faster method for large calls.
+ *                  A tile waits only for earlier tiles held by running workgroups, with a bound
+ *                  of 8,192 polls so that every wave exits; a wait that reached it (not
+ *                  expected) would leave the call's output undefined, every output row still a
+ *                  copy of one of the call's input rows (memory-safe).
  *   CC_SORT_AUTO   CC_SORT_RADIX from CC_SORT_RADIX_MIN_RECORDS records on, else CC_SORT_MERGE.
  *   key_bits       0, or an upper bound on the bit length of (largest key - smallest key) over
  *                  the call (at most 64): the radix method then launches only the passes such a

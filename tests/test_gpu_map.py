@@ -267,6 +267,69 @@ def test_full_size_index_sampled():
         P.cc_store_destroy(store)
 
 
+@pytest.mark.timeout(300)
+def test_large_batch_with_repeats():
+    """A batch of 4.5M records (the scan takes its large tiles from 4M records on) that mixes
+    updates of stored ids, new ids and repeats of both. The result must be the record-by-record
+    replay's: new ids numbered from n_docs in order of first appearance, each id's row and
+    author id those of its last record, stored ids at their positions. Checked in full with
+    NumPy over the whole store (the sequential oracle replay is meant for small batches)."""
+    rb, n0, n = 16, 1_000_000, 4_500_000
+    note(f"map: {n}-record batch with repeats")
+    store = P.cc_store_create_indexed(n0 + n, rb)
+    try:
+        g = np.random.default_rng(21)
+        ids0 = (g.choice(1 << 40, n0, replace=False) + 1).astype(np.int64)
+        authors0 = g.integers(0, 1 << 31, n0).astype(np.int64)
+        rows0 = g.integers(0, 256, (n0, rb), dtype=np.uint8)
+        ws = torch.empty(P.cc_upsert_workspace_bytes(n), dtype=torch.uint8, device=DEV)
+        assert P.cc_store_upsert(store, torch.from_numpy(ids0).to(DEV),
+                                 torch.from_numpy(authors0).to(DEV),
+                                 torch.from_numpy(rows0).to(DEV), ws) == (n0, 0)
+        # 30% stored ids and 70% drawn from 4M new ids, both with replacement (repeats)
+        pool = (g.choice(1 << 40, 4_000_000, replace=False) + (1 << 41)).astype(np.int64)
+        k_old = int(0.3 * n)
+        ids1 = np.concatenate([g.choice(ids0, k_old), g.choice(pool, n - k_old)])
+        g.shuffle(ids1)
+        authors1 = g.integers(0, 1 << 31, n).astype(np.int64)
+        rows1 = g.integers(0, 256, (n, rb), dtype=np.uint8)
+        got = P.cc_store_upsert(store, torch.from_numpy(ids1).to(DEV),
+                                torch.from_numpy(authors1).to(DEV),
+                                torch.from_numpy(rows1).to(DEV), ws)
+        # the replay's result
+        uniq, first = np.unique(ids1, return_index=True)
+        last = n - 1 - np.unique(ids1[::-1], return_index=True)[1]
+        order0 = np.argsort(ids0)
+        at = np.searchsorted(ids0, uniq, sorter=order0)
+        at = np.minimum(at, n0 - 1)
+        stored = ids0[order0[at]] == uniq
+        new_first = first[~stored]
+        rank = np.empty(new_first.size, dtype=np.int64)
+        rank[np.argsort(new_first, kind="stable")] = np.arange(new_first.size)
+        pos = np.empty(uniq.size, dtype=np.int64)
+        pos[stored] = order0[at[stored]]          # ids0[i] was stored at position i
+        pos[~stored] = n0 + rank
+        n_new = int((~stored).sum())
+        assert got == (n_new, 0), f"counts {got} vs {(n_new, 0)}"
+        q = torch.from_numpy(uniq).to(DEV)
+        pq = torch.empty_like(q)
+        P.cc_resolve_ids(store, q, pq)
+        assert np.array_equal(pq.cpu().numpy(), pos), "positions"
+        want_a = np.concatenate([authors0, np.zeros(n_new, np.int64)])
+        want_r = np.concatenate([rows0, np.zeros((n_new, rb), np.uint8)])
+        want_a[pos] = authors1[last]
+        want_r[pos] = rows1[last]
+        total = n0 + n_new
+        a = torch.empty(total, dtype=torch.int64, device=DEV)
+        r = torch.empty(total, rb, dtype=torch.uint8, device=DEV)
+        P.cc_store_read(store, 0, total, a, r)
+        torch.cuda.synchronize()
+        assert np.array_equal(a.cpu().numpy(), want_a), "author ids"
+        assert np.array_equal(r.cpu().numpy(), want_r), "rows"
+    finally:
+        P.cc_store_destroy(store)
+
+
 def test_concurrent_resolves_on_two_streams():
     note("map: concurrent resolves")
     spec = W.IndexSpec(50_000, 1000, 8, torch.bfloat16, 2, 20_000, 0.1, 0, 0.0, 0.0)

@@ -171,11 +171,15 @@ class JoinCase:
     """One join launch of a workload shape: its inputs on the device, output buffers and the
     algorithmic bytes (8-byte author id, and the store's own author width)."""
 
-    def __init__(self, torch, P, st, store, reqs, wd, we, n_lookups, single, dev):
+    def __init__(self, torch, P, st, store, reqs, wd, we, n_lookups, single, dev,
+                 authors=False):
         import workload as W
         self.P, self.store, self.n_lookups, self.single = P, store, n_lookups, single
         self.reqs = reqs
         self.b = W.pack(reqs)
+        # With `authors`, every launch passes each candidate's author id (Alg. 1's input form,
+        # cc_join_batched_authors), gathered once here, outside the timed launches.
+        self.authors = st.author_id[self.b.cand_idx].contiguous() if authors else None
         self.n = self.b.cand_idx.numel()
         self.out = torch.empty(self.n, wd + n_lookups * we, dtype=torch.uint8, device=dev)
         self.hit = torch.empty(self.n, n_lookups, dtype=torch.int8, device=dev)
@@ -191,12 +195,14 @@ class JoinCase:
             P.cc_join_batched(self.store, b.cand_offsets, b.cand_idx,
                               b.key_offsets if key_offsets is None else key_offsets, b.keys,
                               b.edge_rows, self.out, self.hit,
-                              extra_keys=[b.actor] if self.n_lookups == 2 else None)
+                              extra_keys=[b.actor] if self.n_lookups == 2 else None,
+                              author_ids=self.authors)
 
     def entry(self, torch, flush, iters, floor=False):
         t_cold = time_launches(torch, self, max(10, iters // 2), flush=flush)
         t_warm = time_launches(torch, self, iters)
-        e = {"entry": "cc_join" if self.single else "cc_join_batched",
+        e = {"entry": "cc_join" if self.single else
+             ("cc_join_batched_authors" if self.authors is not None else "cc_join_batched"),
              "viewers": self.b.n_viewers, "candidates": self.n, "keys": self.b.keys.numel(),
              "lookups": self.n_lookups}
         e.update(rates(self.n, self.alg, self.alg_stored, t_cold, t_warm))
@@ -373,6 +379,8 @@ def workload_entries(torch, P, W, dev, seed, flush, only=None, sorts=True, sorts
         st._by_author = None
         store = P.cc_store_create(st.author_id, st.doc_rows)
         c = JoinCase(torch, P, st, store, reqs, 128, 128, 1, False, dev)
+        ca = JoinCase(torch, P, st, store, reqs, 128, 128, 1, False, dev, authors=True) \
+            if want("5-authors") else None
         if cpu is not None:
             # The oracle's store: only the documents the candidates name (the result is the same
             # as against the whole store; the 27 GB store never reaches the host).
@@ -389,10 +397,12 @@ def workload_entries(torch, P, W, dev, seed, flush, only=None, sorts=True, sorts
         torch.cuda.empty_cache()
         if not sorts_only:
             res["5"] = c.entry(torch, flush, 40, floor=floors)
+            if ca is not None:
+                res["5-authors"] = ca.entry(torch, flush, 40)
         if sorts:
             res["5-sort"] = sort_entry(torch, P, c.b, 128, dev, "5", s.n_authors)
         P.cc_store_destroy(store)
-        del c
+        del c, ca
         torch.cuda.empty_cache()
     return res
 
@@ -668,7 +678,24 @@ def headline(torch, P, W, dev, args, flush):
     no_keys = time_launches(torch, lambda: P.cc_join_batched(
         store, batches[0][1].cand_offsets, batches[0][1].cand_idx, nk, batches[0][1].keys[:0],
         batches[0][1].edge_rows[:0], out, hit), 20, flush=flush)
+    # The same steps with each candidate's author id passed by the caller (Alg. 1's input
+    # form, cc_join_batched_authors): no read of the store's author column. The ids are
+    # gathered once, outside the timed launches.
+    authors = [st.author_id[b.cand_idx].contiguous() for _, b in batches]
+    it = [0]
+
+    def step_authors():
+        k = it[0] % N_BATCHES
+        it[0] += 1
+        b = batches[k][1]
+        P.cc_join_batched(store, b.cand_offsets, b.cand_idx, b.key_offsets, b.keys, b.edge_rows,
+                          out, hit, author_ids=authors[k])
+
+    with_authors = time_launches(torch, step_authors, 40, flush=flush)
+    with_authors_warm = time_launches(torch, step_authors, 40)
+    del authors
     res = {"no_keys_ms": no_keys["median"], "store": store, "st": st, "batches": batches,
+           "authors_ms": with_authors["median"], "authors_ms_warm": with_authors_warm["median"],
            "wd": wd, "we": we, "total": total,
            "ms_step": ms_step, "ms_median": cold_sorted[len(cold) // 2],
            "ms_p99": cold_sorted[min(len(cold) - 1, int(0.99 * len(cold)))],
@@ -830,6 +857,13 @@ def main(argv=None):
         "ms_per_step_p99": h["ms_p99"],
         "warm": {"ms_per_step": h["ms_warm"], "candidates_per_s": total / (h["ms_warm"] / 1e3),
                  "hbm_gbps": warm_gbps, "frac": warm_gbps / PEAK_GBPS},
+        "caller_author_ids": {
+            "entry": "cc_join_batched_authors", "ms_median": h["authors_ms"],
+            "ms_median_warm": h["authors_ms_warm"],
+            "frac": h["alg8"] / (h["authors_ms"] / 1e3) / 1e9 / PEAK_GBPS,
+            "frac_warm": h["alg8"] / (h["authors_ms_warm"] / 1e3) / 1e9 / PEAK_GBPS,
+            "what": "the same steps with each candidate's author id passed by the caller (the "
+                    "input form of Alg. 1), cold and warm medians"},
         "no_keys_reference": {"ms_median": h["no_keys_ms"],
                               "what": "the same launch with every key list empty (cold)"},
         "latency": lat,

@@ -204,6 +204,29 @@ CC_API cc_status cc_join_batched(const cc_store *store, int32_t n_viewers,
                           hipStream_t stream);
 
 /*
+ * cc_join_batched_authors -- cc_join_batched with each candidate's author id supplied by the
+ * caller, the input form of Alg. 1 (§3.1: every candidate document arrives with its author
+ * id), in place of the store's author column at the candidate's position.
+ *   author_ids     [total_cand] int64 device, 8-byte aligned, not overlapping an output:
+ *                  lookup 0 searches author_ids[j] for candidate j. The doc row still comes
+ *                  from the store at cand_idx[j]; a position outside [0, n_docs) still gives
+ *                  the zero doc segment, default edge segments and hit bits 0 (its author id
+ *                  is not looked up) and is counted as invalid.
+ * Other arguments, alignment rules, output and errors as in cc_join_batched; author_ids may be
+ * NULL only when total_cand == 0.
+ */
+CC_API cc_status cc_join_batched_authors(const cc_store *store, int32_t n_viewers,
+                                         const int64_t *cand_offsets, const int64_t *cand_idx,
+                                         const int64_t *author_ids, int64_t total_cand,
+                                         const int64_t *key_offsets, const int64_t *edge_keys,
+                                         int64_t total_keys,
+                                         const void *edge_feats, int32_t edge_row_bytes,
+                                         const void *default_row,
+                                         int32_t n_lookups, const int64_t *const *extra_keys,
+                                         void *out, int64_t out_row_stride, int8_t *hit_mask,
+                                         hipStream_t stream);
+
+/*
  * cc_join_batched_padded -- cc_join_batched writing the padded batch layout of §6.3 (batching
  * and padding for variable-length requests, where requests with n_v candidates are scattered
  * into one [B, n_max, features] tensor and padded slots are masked downstream).

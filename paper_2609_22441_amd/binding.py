@@ -17,7 +17,8 @@ LIB_PATH = Path(__file__).resolve().with_name("libccjoin.so")
 # Every symbol that include/cc_join.h declares.
 EXPORTS = (
     "cc_store_create", "cc_store_destroy", "cc_store_info", "cc_store_invalid_count",
-    "cc_store_reset_invalid_count", "cc_join", "cc_join_batched", "cc_join_batched_tuned",
+    "cc_store_reset_invalid_count", "cc_join", "cc_join_batched", "cc_join_batched_authors",
+    "cc_join_batched_tuned",
     "cc_join_batched_padded", "cc_sort_workspace_bytes", "cc_sort_affinity",
     "cc_sort_affinity_method", "cc_sort_affinity_noalloc",
     "cc_store_create_indexed", "cc_set_ingestion_wait_limit", "cc_upsert_workspace_bytes",
@@ -70,6 +71,8 @@ def lib():
             "cc_join": [vp, vp, i64, vp, i64, vp, i32, vp, vp, i64, vp, vp],
             "cc_join_batched": [vp, i32, vp, vp, i64, vp, vp, i64, vp, i32, vp, i32,
                                 ctypes.POINTER(vp), vp, i64, vp, vp],
+            "cc_join_batched_authors": [vp, i32, vp, vp, vp, i64, vp, vp, i64, vp, i32, vp, i32,
+                                        ctypes.POINTER(vp), vp, i64, vp, vp],
             "cc_join_batched_tuned": [vp, i32, vp, vp, i64, vp, vp, i64, vp, i32, vp, i32,
                                       ctypes.POINTER(vp), vp, i64, vp, ctypes.POINTER(Tuning),
                                       vp],
@@ -488,13 +491,23 @@ def _batched_args(store, cand_offsets, cand_idx, key_offsets, edge_keys, edge_fe
 def cc_join_batched(store: int, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats, out,
                     hit_mask, default_row=None, extra_keys: Optional[Sequence] = None,
                     total_cand: Optional[int] = None, total_keys: Optional[int] = None,
-                    tuning: Optional[Tuning] = None, stream=None) -> None:
-    """B viewers in CSR form, 1 + len(extra_keys) lookups (see include/cc_join.h)."""
+                    tuning: Optional[Tuning] = None, stream=None, author_ids=None) -> None:
+    """B viewers in CSR form, 1 + len(extra_keys) lookups (see include/cc_join.h). With
+    `author_ids` ([total_cand] int64), lookup 0 searches the caller's author id of each
+    candidate instead of the store's (cc_join_batched_authors)."""
     B, L, tc, tk, pco, pc, pko, pk, pf, pd, ex, ew = _batched_args(
         store, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats, default_row,
         extra_keys, total_cand, total_keys)
     po, stride = _out_rows(out, "out", tc, _doc_row_bytes(store) + L * ew)
     ph = _arr(hit_mask, "hit_mask", _i8(), tc * L)
+    if author_ids is not None:
+        if tuning is not None:
+            raise ValueError("author_ids and tuning cannot be combined")
+        pa = _arr(author_ids, "author_ids", _i64(), tc)
+        _check(lib().cc_join_batched_authors(store, B, pco, pc, pa, tc, pko, pk, tk, pf, ew, pd,
+                                             L, ex, po, stride, ph, _stream(stream)),
+               "cc_join_batched_authors")
+        return
     args = (store, B, pco, pc, tc, pko, pk, tk, pf, ew, pd, L, ex, po, stride, ph)
     if tuning is None:
         _check(lib().cc_join_batched(*args, _stream(stream)), "cc_join_batched")

@@ -74,7 +74,8 @@ private:
 };
 
 cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *cand_offsets,
-                    const int64_t *cand_idx, int64_t total_cand, const int64_t *key_offsets,
+                    const int64_t *cand_idx, const int64_t *cand_author, int64_t total_cand,
+                    const int64_t *key_offsets,
                     const int64_t *edge_keys, int64_t total_keys, const void *edge_feats,
                     int32_t edge_row_bytes, const void *default_row, int32_t n_lookups,
                     const int64_t *extra, void *out, int64_t out_row_stride, int8_t *hit_mask,
@@ -119,7 +120,7 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
         return CC_ERR_INVALID_ARGUMENT;
     if (!aligned(out, 16) || !aligned(edge_feats, 16) || !aligned(default_row, 16) ||
         !aligned(cand_idx, 8) || !aligned(edge_keys, 8) || !aligned(cand_offsets, 8) ||
-        !aligned(key_offsets, 8) || !aligned(extra, 8))
+        !aligned(key_offsets, 8) || !aligned(extra, 8) || !aligned(cand_author, 8))
         return CC_ERR_INVALID_ARGUMENT;
     {
         // The outputs must not overlap any input or each other.
@@ -128,6 +129,7 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
         const struct { const void *p; int64_t n; } in[] = {
             {cand_idx, total_cand * 8}, {edge_keys, total_keys * 8},
             {edge_feats, total_keys * edge_row_bytes}, {extra, extra ? total_cand * 8 : 0},
+            {cand_author, cand_author ? total_cand * 8 : 0},
             {cand_offsets, nv1 * 8}, {key_offsets, nv1 * 8},
             {default_row, default_row ? edge_row_bytes : 0}};
         const struct { const void *p; int64_t n; } outs[] = {
@@ -175,7 +177,9 @@ cc_status join_impl(const cc_store *store, int32_t n_viewers, const int64_t *can
 
     ccj::JoinArgs a;
     a.author = store->d_author;
-    a.author32 = store->compact ? store->d_author32 : nullptr;
+    // The caller's author ids are read by the 64-bit form of the kernel.
+    a.author32 = store->compact && !cand_author ? store->d_author32 : nullptr;
+    a.cand_author = cand_author;
     a.doc = store->d_rows;
     a.n_docs = store->n_docs;
     a.doc_bytes = store->doc_row_bytes;
@@ -574,7 +578,8 @@ cc_status cc_join(const cc_store *store, const int64_t *cand_idx, int64_t n_cand
                   const int64_t *edge_keys, int64_t n_keys, const void *edge_feats,
                   int32_t edge_row_bytes, const void *default_row, void *out,
                   int64_t out_row_stride, int8_t *hit_mask, hipStream_t stream) {
-    return join_impl(store, 1, nullptr, cand_idx, n_cand, nullptr, edge_keys, n_keys, edge_feats,
+    return join_impl(store, 1, nullptr, cand_idx, nullptr, n_cand, nullptr, edge_keys, n_keys,
+                     edge_feats,
                      edge_row_bytes, default_row, 1, nullptr, out, out_row_stride, hit_mask, 0,
                      nullptr, nullptr, stream);
 }
@@ -593,7 +598,7 @@ cc_status cc_join_batched_tuned(const cc_store *store, int32_t n_viewers,
     if (n_lookups == 2 && !extra_keys)
         return CC_ERR_INVALID_ARGUMENT;
     const int64_t *extra = (n_lookups == 2) ? extra_keys[0] : nullptr;
-    return join_impl(store, n_viewers, cand_offsets, cand_idx, total_cand, key_offsets,
+    return join_impl(store, n_viewers, cand_offsets, cand_idx, nullptr, total_cand, key_offsets,
                      edge_keys, total_keys, edge_feats, edge_row_bytes, default_row, n_lookups,
                      extra, out, out_row_stride, hit_mask, 0, nullptr, tuning, stream);
 }
@@ -613,12 +618,33 @@ cc_status cc_join_batched_padded(const cc_store *store, int32_t n_viewers,
         return CC_ERR_INVALID_ARGUMENT;
     const int64_t *extra = (n_lookups == 2) ? extra_keys[0] : nullptr;
     if (n_viewers == 0)
-        return join_impl(store, 0, cand_offsets, cand_idx, total_cand, key_offsets, edge_keys,
-                         total_keys, edge_feats, edge_row_bytes, default_row, n_lookups, extra,
-                         out, out_row_stride, hit_mask, 0, nullptr, nullptr, stream);
-    return join_impl(store, n_viewers, cand_offsets, cand_idx, total_cand, key_offsets,
+        return join_impl(store, 0, cand_offsets, cand_idx, nullptr, total_cand, key_offsets,
+                         edge_keys, total_keys, edge_feats, edge_row_bytes, default_row, n_lookups,
+                         extra, out, out_row_stride, hit_mask, 0, nullptr, nullptr, stream);
+    return join_impl(store, n_viewers, cand_offsets, cand_idx, nullptr, total_cand, key_offsets,
                      edge_keys, total_keys, edge_feats, edge_row_bytes, default_row, n_lookups,
                      extra, out, out_row_stride, hit_mask, n_max, valid_mask, nullptr, stream);
+}
+
+cc_status cc_join_batched_authors(const cc_store *store, int32_t n_viewers,
+                                  const int64_t *cand_offsets, const int64_t *cand_idx,
+                                  const int64_t *author_ids, int64_t total_cand,
+                                  const int64_t *key_offsets, const int64_t *edge_keys,
+                                  int64_t total_keys, const void *edge_feats,
+                                  int32_t edge_row_bytes, const void *default_row,
+                                  int32_t n_lookups, const int64_t *const *extra_keys, void *out,
+                                  int64_t out_row_stride, int8_t *hit_mask, hipStream_t stream) {
+    if (n_viewers > 0 && (!cand_offsets || !key_offsets))
+        return CC_ERR_INVALID_ARGUMENT;
+    if (n_lookups == 2 && !extra_keys)
+        return CC_ERR_INVALID_ARGUMENT;
+    if (total_cand > 0 && !author_ids)
+        return CC_ERR_INVALID_ARGUMENT;
+    const int64_t *extra = (n_lookups == 2) ? extra_keys[0] : nullptr;
+    return join_impl(store, n_viewers, cand_offsets, cand_idx, author_ids, total_cand,
+                     key_offsets, edge_keys, total_keys, edge_feats, edge_row_bytes, default_row,
+                     n_lookups, extra, out, out_row_stride, hit_mask, 0, nullptr, nullptr,
+                     stream);
 }
 
 cc_status cc_join_batched(const cc_store *store, int32_t n_viewers, const int64_t *cand_offsets,

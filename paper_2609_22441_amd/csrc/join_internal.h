@@ -33,6 +33,7 @@ struct JoinArgs {
     int32_t edge_bytes;
     const int64_t *cand_offsets; // [B+1] or nullptr for one viewer
     const int64_t *cand_idx;
+    const int64_t *cand_author;  // [total_cand] author id per candidate, or nullptr: the store's
     int64_t total_cand;
     const int64_t *key_offsets;  // [B+1] or nullptr for one viewer
     const int64_t *keys;

@@ -210,16 +210,18 @@ __device__ __forceinline__ int choose_stride(int64_t K, int64_t seg_len, int32_t
     return S;
 }
 
-// Author id of a store position: from the 32-bit column when the store has one (every id fits
-// in 32 bits, so a 64-byte sector holds 16 ids instead of 8), else from the 64-bit column. The
-// column is a compile-time choice: a branch in the prefetch would split the pipeline's basic
-// blocks and cost more than the narrower reads save.
+// Author id of candidate j at store position c: the caller's id for the candidate when the
+// call supplies them (Alg. 1's input form), else the store's, from the 32-bit column when the
+// store has one (every id fits in 32 bits, so a 64-byte sector holds 16 ids instead of 8) or the
+// 64-bit column. The column is a compile-time choice: a branch in the prefetch would split the
+// pipeline's basic blocks and cost more than the narrower reads save; the caller's ids share
+// the 64-bit form, by address (one unconditional load either way).
 template <bool A32>
-__device__ __forceinline__ int64_t author_of(const JoinArgs &a, int64_t c) {
+__device__ __forceinline__ int64_t author_of(const JoinArgs &a, int64_t c, int64_t j) {
     if constexpr (A32)
         return (int64_t)a.author32[c];
     else
-        return a.author[c];
+        return *(a.cand_author ? a.cand_author + j : a.author + c);
 }
 
 __device__ __forceinline__ int64_t range_index(int b, int n) {
@@ -529,8 +531,8 @@ __device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t (*s_src)[k
     {
         const int64_t c0 = a.cand_idx[base(0) + tid];
         const int64_t e0 = extra(0);
-        const int64_t x0 = author_of<A32>(a, clamp64(c0, last_doc));
-        x1 = author_of<A32>(a, clamp64(c1, last_doc));
+        const int64_t x0 = author_of<A32>(a, clamp64(c0, last_doc), base(0) + tid);
+        x1 = author_of<A32>(a, clamp64(c1, last_doc), base(1) + tid);
         stage();
         resolve_tile<NL>(a, s_src[0], s_row[0], s_invalid, s_tab, M, S, gk, K, kb, base(0),
                          shift, fresh(0), c0, x0, e0);
@@ -548,7 +550,7 @@ __device__ __forceinline__ void full_tiles(const JoinArgs &a, int64_t (*s_src)[k
                                  kb, base(k + 1), shift, fresh(k + 1), c1, x1, e1);
                 const int64_t c3 = a.cand_idx[base(k + 3) + tid];
                 const int64_t e2 = extra(k + 2);
-                const int64_t x2 = author_of<A32>(a, clamp64(c2, last_doc));
+                const int64_t x2 = author_of<A32>(a, clamp64(c2, last_doc), base(k + 2) + tid);
                 c1 = c2;
                 c2 = c3;
                 x1 = x2;
@@ -644,7 +646,7 @@ __global__ __launch_bounds__(kBlock) void join_kernel(JoinArgs a) {
             if (tid < n) {
                 const int64_t c = a.cand_idx[t0 + tid];
                 const bool ok = c >= 0 && c < a.n_docs;
-                const int64_t x0 = ok ? author_of<A32>(a, c) : 0;
+                const int64_t x0 = ok ? author_of<A32>(a, c, t0 + tid) : 0;
                 const int64_t x1 = NL == 2 ? a.extra[t0 + tid] : 0;
                 resolve_tile<NL>(a, s_src[0], s_row[0], &s_invalid, s_tab, M, S, gk, K, kb, t0,
                                  shift, 0, c, x0, x1);

@@ -66,6 +66,11 @@ def test_join_rejects_null_store():
     assert lib.cc_join(None, None, 0, None, 0, None, 16, None, None, 32, None, None) == 1
     assert lib.cc_join_batched(None, 0, None, None, 0, None, None, 0, None, 16, None, 1, None,
                                None, 32, None, None) == 1
+    assert lib.cc_join_batched_authors(None, 0, None, None, None, 0, None, None, 0, None, 16,
+                                       None, 1, None, None, 32, None, None) == 1
+    # candidates without their author ids: refused before the store is looked at
+    assert lib.cc_join_batched_authors(None, 1, 8, 8, None, 5, 8, None, 0, None, 16, None, 1,
+                                       None, 16, 32, 8, None) == 1
 
 
 def test_store_queries_reject_null():

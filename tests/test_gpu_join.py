@@ -51,6 +51,68 @@ def test_tiny_random_cases(tuning):
         _tiny(tc, tuning, stride_extra=16 * (seed % 2), what=f"seed {seed} tuning {tuning}")
 
 
+def _caller_authors(tc, seed):
+    """Per-candidate author ids for the caller-supplied form: the store's id at the candidate's
+    position for a third of them, a key of the batch (a likely hit) for a third, an arbitrary
+    int64 for the rest."""
+    c = tc.batch.cand_idx
+    n, nd = c.numel(), tc.author_id.numel()
+    g = torch.Generator().manual_seed(seed)
+    own = tc.author_id[c.clamp(0, nd - 1)] if nd else torch.zeros_like(c)
+    keys = tc.batch.keys
+    pick = keys[torch.randint(0, keys.numel(), (n,), generator=g)] if keys.numel() else own
+    wild = torch.randint(-(1 << 62), 1 << 62, (n,), generator=g, dtype=torch.int64)
+    which = torch.randint(0, 3, (n,), generator=g)
+    return torch.where(which == 0, own, torch.where(which == 1, pick, wild)).contiguous()
+
+
+def _oracle_caller_authors(tc, authors, stride):
+    """Eq. 1 with caller-supplied author ids, as the plain oracle join over a store holding one
+    document per candidate (its doc row, the caller's author id), each valid candidate pointing
+    at its own document and each invalid one at -1."""
+    c = tc.batch.cand_idx
+    n, nd = c.numel(), tc.author_id.numel()
+    valid = (c >= 0) & (c < nd)
+    rows = torch.zeros((n,) + tuple(tc.doc_rows.shape[1:]), dtype=tc.doc_rows.dtype)
+    rows[valid] = tc.doc_rows[c[valid]]
+    own_pos = torch.where(valid, torch.arange(n), torch.full_like(c, -1))
+    b = tc.batch
+    b2 = W.Batch(b.cand_offsets, own_pos, b.key_offsets, b.keys, b.edge_rows, b.actor)
+    return oracle_join(authors, rows, b2, tc.n_lookups, default_row=tc.default_row,
+                       stride=stride)
+
+
+def test_caller_supplied_author_ids():
+    """cc_join_batched_authors (lookup 0 searches the caller's author id of each candidate, Alg.
+    1's input form) against the oracle over a store remapped to those ids, on random tiny
+    cases with one and two lookups, invalid positions and defaults."""
+    note("caller-supplied author ids")
+    for seed in range(30):
+        tc = W.tiny_case(4000 + seed, max_k=150, max_n=900, max_viewers=5)
+        if tc.batch.cand_idx.numel() == 0:
+            continue
+        authors = _caller_authors(tc, seed)
+        b = tc.batch.to(DEV)
+        wd, we = row_bytes(tc.doc_rows), row_bytes(tc.batch.edge_rows)
+        stride = wd + tc.n_lookups * we + 16 * (seed % 2)
+        store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+        try:
+            n = b.cand_idx.numel()
+            out = torch.full((n, stride), FILL, dtype=torch.uint8, device=DEV)
+            hit = torch.full((n, tc.n_lookups), -7, dtype=torch.int8, device=DEV)
+            d = None if tc.default_row is None else tc.default_row.to(DEV)
+            P.cc_join_batched(store, b.cand_offsets, b.cand_idx, b.key_offsets, b.keys,
+                              b.edge_rows, out, hit, default_row=d,
+                              extra_keys=[b.actor] if tc.n_lookups == 2 else None,
+                              author_ids=authors.to(DEV))
+            torch.cuda.synchronize()
+            want = _oracle_caller_authors(tc, authors, stride)
+            assert_same((out.cpu().numpy(), hit.cpu().numpy()), want, f"seed {seed}")
+            assert P.cc_store_invalid_count(store) == want[2], f"seed {seed}: invalid count"
+        finally:
+            P.cc_store_destroy(store)
+
+
 def test_duplicate_keys_leftmost():
     note("duplicate keys")
     for seed in range(20):

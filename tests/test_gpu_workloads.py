@@ -75,6 +75,27 @@ def test_workload2_batched_as_benchmarked(store10m):
 
 
 @pytest.mark.timeout(300)
+def test_workload2_batched_with_caller_author_ids(store10m):
+    """The benchmark's step with each candidate's author id passed by the caller
+    (cc_join_batched_authors): the ids are the store's own, so the result is the oracle's join
+    of the same batch, bit for bit."""
+    st, h, cpu = store10m
+    _, r = W.SHAPES[2]
+    b = W.pack(W.make_requests(st, r, 2, n_viewers=64))
+    wd, we = row_bytes(st.doc_rows), row_bytes(b.edge_rows)
+    note(f"workload 2 x64 with caller author ids: {b.cand_idx.numel()} candidates")
+    authors = st.author_id[b.cand_idx].contiguous()
+    n = b.cand_idx.numel()
+    out = torch.empty(n, wd + we, dtype=torch.uint8, device=DEV)
+    hit = torch.empty(n, 1, dtype=torch.int8, device=DEV)
+    P.cc_join_batched(h, b.cand_offsets, b.cand_idx, b.key_offsets, b.keys, b.edge_rows, out,
+                      hit, author_ids=authors)
+    torch.cuda.synchronize()
+    want = oracle_join(cpu[0], cpu[1], b.to("cpu"), 1)
+    assert_same((out.cpu().numpy(), hit.cpu().numpy()), want, "workload 2 x64, caller ids")
+
+
+@pytest.mark.timeout(300)
 def test_workload3_batched_ragged(store10m):
     st, h, cpu = store10m
     _, r = W.SHAPES[3]

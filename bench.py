@@ -353,6 +353,11 @@ def workload_entries(torch, P, W, dev, seed, flush, only=None, sorts=True, sorts
             cases.append(("4x64", W.make_requests(st, r4, seed, n_viewers=64), 2, False, 20))
         for tag, reqs, L, single, iters in cases:
             c = JoinCase(torch, P, st, store, reqs, 128, 64, L, single, dev)
+            if tag in ("3", "4x64") and want(tag + "-authors") and not sorts_only:
+                # the same launch with the candidates' author ids passed by the caller
+                ca = JoinCase(torch, P, st, store, reqs, 128, 64, L, single, dev, authors=True)
+                res[tag + "-authors"] = ca.entry(torch, flush, iters)
+                del ca
             if not sorts_only:
                 res[tag] = c.entry(torch, flush, iters, floor=floors and tag in ("3", "4x64"))
             if cpu is not None and tag in ("2", "3", "4"):

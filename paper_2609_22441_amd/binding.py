@@ -443,7 +443,8 @@ class PreparedJoinBatched:
     """
 
     def __init__(self, store: int, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats,
-                 out, hit_mask, default_row=None, extra_keys: Optional[Sequence] = None):
+                 out, hit_mask, default_row=None, extra_keys: Optional[Sequence] = None,
+                 author_ids=None):
         B, L, tc, tk, pco, pc, pko, pk, pf, pd, ex, ew = _batched_args(
             store, cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats, default_row,
             extra_keys, None, None)
@@ -451,8 +452,10 @@ class PreparedJoinBatched:
         ph = _arr(hit_mask, "hit_mask", _i8(), tc * L)
         self._cap = (B, tc, tk)
         self._keep = (cand_offsets, cand_idx, key_offsets, edge_keys, edge_feats, out, hit_mask,
-                      default_row, extra_keys, ex)
+                      default_row, extra_keys, ex, author_ids)
         self._a = (store, pco, pc, pko, pk, pf, ew, pd, L, ex, po, stride, ph)
+        # With author_ids ([total_cand] int64 buffer), cc_join_batched_authors.
+        self._pa = None if author_ids is None else _arr(author_ids, "author_ids", _i64(), tc)
         self._fn = lib().cc_join_batched
 
     def __call__(self, n_viewers: Optional[int] = None, total_cand: Optional[int] = None,
@@ -464,6 +467,12 @@ class PreparedJoinBatched:
         if not (0 <= b <= B and 0 <= n <= tc and 0 <= k <= tk):
             _fail("counts", f"must lie in [0, {B}], [0, {tc}] and [0, {tk}] (got {b}, {n}, {k})")
         store, pco, pc, pko, pk, pf, ew, pd, L, ex, po, stride, ph = self._a
+        if self._pa is not None:
+            st = lib().cc_join_batched_authors(store, b, pco, pc, self._pa, n, pko, pk, k, pf, ew,
+                                               pd, L, ex, po, stride, ph, _stream(stream))
+            if st != CC_OK:
+                raise CCError(st, "cc_join_batched_authors")
+            return
         st = self._fn(store, b, pco, pc, n, pko, pk, k, pf, ew, pd, L, ex, po, stride, ph,
                       _stream(stream))
         if st != CC_OK:

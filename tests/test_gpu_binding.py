@@ -80,6 +80,44 @@ def test_prepared_join_equals_cc_join():
         P.cc_store_destroy(store)
 
 
+def test_prepared_batched_join_with_author_ids():
+    """PreparedJoinBatched with caller-supplied author ids gives the bytes of
+    cc_join_batched(..., author_ids=...) for every CSR prefix (that call is checked against
+    the oracle in test_gpu_join.py)."""
+    note("binding: prepared batched join, caller author ids")
+    tc = W.tiny_case(94, max_n=400, max_k=200, max_viewers=5)
+    b = tc.batch
+    wd, we = row_bytes(tc.doc_rows), row_bytes(b.edge_rows)
+    store = P.cc_store_create(tc.author_id.to(DEV), tc.doc_rows.to(DEV))
+    try:
+        d = b.to(DEV)
+        n_all = d.cand_idx.numel()
+        g = torch.Generator().manual_seed(3)
+        pool = torch.cat([b.keys, tc.author_id]) if b.keys.numel() + tc.author_id.numel() else \
+            torch.zeros(1, dtype=torch.int64)
+        authors = pool[torch.randint(0, pool.numel(), (n_all,), generator=g)].to(DEV)
+        out = torch.full((n_all, wd + we), 0x5A, dtype=torch.uint8, device=DEV)
+        hit = torch.full((n_all, 1), -7, dtype=torch.int8, device=DEV)
+        prepared = P.PreparedJoinBatched(store, d.cand_offsets, d.cand_idx, d.key_offsets, d.keys,
+                                         d.edge_rows, out, hit, author_ids=authors)
+        co, ko = b.cand_offsets.tolist(), b.key_offsets.tolist()
+        for nv in range(len(co) - 1, -1, -1):
+            n, k = co[nv], ko[nv]
+            out.fill_(0x5A)
+            hit.fill_(-7)
+            prepared(nv, n, k)
+            ref_out = torch.full((n, wd + we), 0x5A, dtype=torch.uint8, device=DEV)
+            ref_hit = torch.full((n, 1), -7, dtype=torch.int8, device=DEV)
+            P.cc_join_batched(store, d.cand_offsets[:nv + 1], d.cand_idx[:n],
+                              d.key_offsets[:nv + 1], d.keys[:k], d.edge_rows[:k], ref_out,
+                              ref_hit, author_ids=authors[:n])
+            torch.cuda.synchronize()
+            assert torch.equal(out[:n], ref_out) and torch.equal(hit[:n], ref_hit), nv
+            assert bool((hit[n:] == -7).all()), nv
+    finally:
+        P.cc_store_destroy(store)
+
+
 def test_prepared_batched_join_equals_cc_join_batched():
     """PreparedJoinBatched on its first b viewers gives the bytes cc_join_batched gives for the
     same CSR prefix, two lookups, b from all viewers down to none."""
